@@ -1,0 +1,184 @@
+/*
+ * dmc.h -- C ABI of the MI355X (gfx950) Dynamic Memory Compression decode path.
+ *
+ * Method: Nawrot et al., "Dynamic Memory Compression: Retrofitting LLMs for
+ * Accelerated Inference" (ICML 2024).
+ *   - Sec. 3.1 (Inference), the equation re-using the first key/query neurons:
+ *     alpha_t = round(sigmoid(k_t[0])), omega_t = sigmoid(q_t[0]).
+ *   - Algorithm 1 (single-head KV cache update): alpha_t = 1 merges k_t, v_t
+ *     into the last slot as an omega-weighted running mean (z_t = z_{t-1} +
+ *     omega_t), alpha_t = 0 appends a slot (z_t = omega_t); k_t[0] and q_t[0]
+ *     are zeroed.
+ *   - Sec. 3.1, last paragraph: attention (Sec. 2.1, softmax of q.k/sqrt(d_h))
+ *     runs over the compressed per-head sequences; heads are independent.
+ *   - Sec. 3.3 (Practical considerations): variable-length per-head caches
+ *     stored in pages allocated on demand per head; Sec. 5.2 uses 32-token
+ *     pages.
+ *
+ * A "unit" is one (layer, batch row b, kv head g); u = b * num_kv_heads + g.
+ * Query heads g*G .. g*G+G-1 (G = num_q_heads / num_kv_heads) read unit u.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named *_dev are device pointers (HIP), owned by the caller and
+ *     kept alive until the stream has consumed them.  The library never
+ *     allocates device memory and keeps no input pointer past a call.
+ *   - Inputs are const: the zeroing of k[0] / q[0] (Algorithm 1) happens
+ *     inside the kernels, not in caller memory.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream) and return after enqueueing.  Every host-detectable error
+ *     (NULL or misaligned pointer, layer out of range, unsupported shape,
+ *     bad stride) returns a status before anything is enqueued; the message
+ *     is available from dmc_last_error() on the same thread.
+ *   - Device-detected failures (page pool exhausted, per-unit slot capacity
+ *     reached, invalid imported lengths) never write out of bounds: the
+ *     affected token is dropped, a sticky device flag is raised, and
+ *     dmc_cache_check() reports it.  Outputs of such a call are undefined.
+ *   - One handle is used by one stream at a time; the ABI is not reentrant on
+ *     the same handle.  No exception or abort crosses the ABI.
+ *   - Floating point: inputs, cache slots and outputs use the configured dtype
+ *     (bf16 or fp32); all arithmetic accumulates in fp32; bf16 results are
+ *     rounded to nearest even.
+ */
+#ifndef DMC_H
+#define DMC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void *dmc_stream_t; /* a hipStream_t */
+
+typedef enum {
+  DMC_OK = 0,
+  DMC_ERR_INVALID_ARG = 1, /* bad pointer, layer, shape, stride or config   */
+  DMC_ERR_UNSUPPORTED = 2, /* valid request outside what the kernels handle */
+  DMC_ERR_CAPACITY = 3,    /* page pool or per-unit slot capacity exhausted */
+  DMC_ERR_HIP = 4          /* a HIP runtime call failed                     */
+} dmc_status;
+
+typedef enum { DMC_BF16 = 0, DMC_FP32 = 1 } dmc_dtype;
+
+/* Which query neuron supplies omega for a kv head shared by G query heads
+ * (grouped-query attention; the paper combines DMC with GQA, Sec. 5, but
+ * does not name the head).  LEAD: query head g*G.  GROUP_MEAN: mean of the
+ * G heads' sigmoid(q[0]). */
+typedef enum { DMC_OMEGA_LEAD_QHEAD = 0, DMC_OMEGA_GROUP_MEAN = 1 } dmc_omega_src;
+
+typedef struct dmc_cache_config {
+  int32_t num_layers;
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;      /* num_q_heads % num_kv_heads == 0, G in {1,2,4,8} */
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t dtype;             /* dmc_dtype: inputs, cache slots and outputs */
+  int32_t page_size;         /* slots per page, power of two in [8, 256]; the paper uses 32 */
+  int32_t max_slots_per_seq; /* slot capacity of one unit; page-table width = ceil(/page_size) */
+  int64_t num_pages;         /* pool capacity in pages, shared by all units, < 2^31 */
+  float decision_bias;       /* c: alpha = round(sigmoid(k[0] - c)) = (k[0] > c); 0 = Algorithm 1 */
+  int32_t omega_src;         /* dmc_omega_src */
+  int32_t split_tile;        /* slots per split-K attention tile; 0 = 256 */
+  int32_t max_prompt_len;    /* largest n for dmc_prefill_compress; 0 = max_slots_per_seq */
+} dmc_cache_config;
+
+typedef struct dmc_cache dmc_cache; /* opaque host handle */
+
+/* Bytes of device workspace a cache with this configuration needs (page pool,
+ * page tables, lengths, z, control words, decode split-K partials and prefill
+ * staging).  Returns 0 for an invalid configuration (see dmc_last_error). */
+size_t dmc_cache_workspace_bytes(const dmc_cache_config *cfg);
+
+/* Create a cache inside the caller-owned device buffer `workspace_dev` of
+ * `bytes` bytes (>= dmc_cache_workspace_bytes(cfg), 256-byte aligned, on the
+ * current HIP device).  Enqueues the initialisation (all lengths and z zero,
+ * empty pool, flags clear) on `stream`.  *out receives the host handle. */
+dmc_status dmc_cache_alloc(const dmc_cache_config *cfg, void *workspace_dev, size_t bytes,
+                           dmc_stream_t stream, dmc_cache **out);
+
+/* Release the host handle (the workspace stays the caller's). */
+dmc_status dmc_cache_free(dmc_cache *cache);
+
+/* Empty every layer: lengths, z, page pool and flags back to the initial state. */
+dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream);
+
+/* Prompt phase of one layer (Algorithm 1 applied to n prompt tokens in order,
+ * without attention): per unit, the first token opens a slot, then every
+ * token with k[0] > c merges into the open slot and every other token opens
+ * a new one.  The result equals n sequential decode-step updates: slot s of
+ * a unit is the omega-weighted mean of its segment's keys (element 0 zeroed)
+ * and values, z is the omega sum of the last segment.
+ *   k_dev, v_dev: logical [B, n, Hkv, d] of the config dtype; k_strides /
+ *     v_strides give the element strides of the B, n and Hkv axes (the d axis
+ *     is contiguous); base pointers 16-byte aligned, strides multiples of 8.
+ *   q_dev: logical [B, n, Hq, d] with q_strides for B, n, Hq; only element 0
+ *     of each query row is read (a [B, n, Hq] tensor of q[..., 0] with
+ *     strides (n*Hq, Hq, 1) is accepted), no alignment requirement.
+ *   n: prompt length, 0 <= n <= max_prompt_len.
+ *   prompt_lens_dev: optional int32 [B]; row b uses tokens t < prompt_lens[b]
+ *     (values outside [0, n] raise the invalid-argument device flag and are
+ *     clamped).  NULL = n for every row.
+ *   slot_index_dev: optional int32 [B, Hkv, n]: slot each token went to, -1
+ *     for tokens past the row's prompt length.
+ * The layer's previous contents are discarded (its pages are not reclaimed:
+ * the pool is a bump allocator emptied only by dmc_cache_reset). */
+dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer,
+                                const void *k_dev, const int64_t k_strides[3],
+                                const void *v_dev, const int64_t v_strides[3],
+                                const void *q_dev, const int64_t q_strides[3],
+                                int32_t n, const int32_t *prompt_lens_dev,
+                                int32_t *slot_index_dev, dmc_stream_t stream);
+
+/* One auto-regressive decode step of one layer: for every unit, the DMC
+ * update of Algorithm 1 with the new token (alpha from the unit's own k[0];
+ * the first token of an empty unit always appends), then softmax attention
+ * of each of the G query heads over the updated compressed sequence with
+ * scale 1/sqrt(d) and q[0] treated as 0.
+ *   q_dev:   [B, Hq, d] contiguous, config dtype, 16-byte aligned.
+ *   k_dev, v_dev: [B, Hkv, d] contiguous, 16-byte aligned.
+ *   out_dev: [B, Hq, d] contiguous, 16-byte aligned, written.
+ *   slot_index_dev: optional int32 [B, Hkv]: slot index the token went to
+ *     (-1 when it was dropped for lack of capacity). */
+dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q_dev,
+                           const void *k_dev, const void *v_dev, void *out_dev,
+                           int32_t *slot_index_dev, dmc_stream_t stream);
+
+/* Copy the slot counts of one layer into lengths_dev (int32 [B, Hkv]). */
+dmc_status dmc_cache_lengths(const dmc_cache *cache, int32_t layer, int32_t *lengths_dev,
+                             dmc_stream_t stream);
+
+/* Gather one layer into dense tensors k_dense_dev, v_dense_dev
+ * [B, Hkv, dense_slots, d] (config dtype; slots at or past a unit's length
+ * are zero-filled; units longer than dense_slots are truncated) and its
+ * running importance sums into z_dev (fp32 [B, Hkv]). */
+dmc_status dmc_cache_export(const dmc_cache *cache, int32_t layer, void *k_dense_dev,
+                            void *v_dense_dev, int32_t dense_slots, float *z_dev,
+                            dmc_stream_t stream);
+
+/* Install an already-compressed layer: unit u gets lengths_dev[u] slots
+ * taken from k_dense_dev / v_dense_dev [B, Hkv, dense_slots, d] and the
+ * running sum z_dev[u] of its open slot.  Pages come from the pool.  Lengths
+ * outside [0, min(dense_slots, max_slots_per_seq)] raise the device flag and
+ * are treated as 0. */
+dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense_dev,
+                            const void *v_dense_dev, int32_t dense_slots,
+                            const int32_t *lengths_dev, const float *z_dev,
+                            dmc_stream_t stream);
+
+/* Synchronise `stream` and report the sticky device flags: DMC_OK,
+ * DMC_ERR_CAPACITY (pool or slot capacity exhausted) or DMC_ERR_INVALID_ARG
+ * (bad imported lengths or prompt lengths).  Flags clear only on reset. */
+dmc_status dmc_cache_check(dmc_cache *cache, dmc_stream_t stream);
+
+/* Synchronise `stream` and return the number of pool pages handed out. */
+dmc_status dmc_cache_pages_used(dmc_cache *cache, int64_t *pages_out, dmc_stream_t stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char *dmc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DMC_H */

@@ -1,0 +1,211 @@
+"""ctypes binding of libdmc.so (the gfx950 DMC decode-path library).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch supplies device memory and the current HIP stream.  If the
+library is missing or fails to load, importing this module raises -- there
+is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_size_t, c_void_p
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdmc.so")
+
+DMC_OK, DMC_ERR_INVALID_ARG, DMC_ERR_UNSUPPORTED, DMC_ERR_CAPACITY, DMC_ERR_HIP = range(5)
+DMC_BF16, DMC_FP32 = 0, 1
+DMC_OMEGA_LEAD_QHEAD, DMC_OMEGA_GROUP_MEAN = 0, 1
+STATUS_NAMES = {0: "DMC_OK", 1: "DMC_ERR_INVALID_ARG", 2: "DMC_ERR_UNSUPPORTED",
+                3: "DMC_ERR_CAPACITY", 4: "DMC_ERR_HIP"}
+
+#: Every entry point declared in include/dmc.h.
+EXPORTS = ("dmc_cache_workspace_bytes", "dmc_cache_alloc", "dmc_cache_free", "dmc_cache_reset",
+           "dmc_prefill_compress", "dmc_decode_step", "dmc_cache_lengths", "dmc_cache_export",
+           "dmc_cache_import", "dmc_cache_check", "dmc_cache_pages_used", "dmc_last_error")
+
+
+class CacheConfig(ctypes.Structure):
+    """Mirror of dmc_cache_config."""
+    _fields_ = [("num_layers", c_int32), ("batch", c_int32), ("num_q_heads", c_int32),
+                ("num_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int32),
+                ("page_size", c_int32), ("max_slots_per_seq", c_int32), ("num_pages", c_int64),
+                ("decision_bias", c_float), ("omega_src", c_int32), ("split_tile", c_int32),
+                ("max_prompt_len", c_int32)]
+
+
+class DMCError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "or python -m paper_2403_09636_amd.csrc.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64p = POINTER(c_int64)
+    lib.dmc_cache_workspace_bytes.argtypes = [POINTER(CacheConfig)]
+    lib.dmc_cache_workspace_bytes.restype = c_size_t
+    lib.dmc_cache_alloc.argtypes = [POINTER(CacheConfig), c_void_p, c_size_t, c_void_p,
+                                    POINTER(c_void_p)]
+    lib.dmc_cache_free.argtypes = [c_void_p]
+    lib.dmc_cache_reset.argtypes = [c_void_p, c_void_p]
+    lib.dmc_prefill_compress.argtypes = [c_void_p, c_int32, c_void_p, i64p, c_void_p, i64p,
+                                         c_void_p, i64p, c_int32, c_void_p, c_void_p, c_void_p]
+    lib.dmc_decode_step.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                    c_void_p, c_void_p]
+    lib.dmc_cache_lengths.argtypes = [c_void_p, c_int32, c_void_p, c_void_p]
+    lib.dmc_cache_export.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
+                                     c_void_p]
+    lib.dmc_cache_import.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
+                                     c_void_p, c_void_p]
+    lib.dmc_cache_check.argtypes = [c_void_p, c_void_p]
+    lib.dmc_cache_pages_used.argtypes = [c_void_p, i64p, c_void_p]
+    lib.dmc_last_error.argtypes = []
+    lib.dmc_last_error.restype = c_char_p
+    for name in EXPORTS:
+        if name not in ("dmc_cache_workspace_bytes", "dmc_last_error"):
+            getattr(lib, name).restype = c_int32
+    return lib
+
+
+lib = _load()
+
+
+def last_error() -> str:
+    msg = lib.dmc_last_error()
+    return msg.decode() if msg else ""
+
+
+def check(status: int):
+    if status != DMC_OK:
+        raise DMCError(status, last_error())
+
+
+def make_config(num_layers, batch, num_q_heads, num_kv_heads, head_dim, dtype="bf16",
+                page_size=32, max_slots_per_seq=4096, num_pages=None, decision_bias=0.0,
+                omega_src="lead", split_tile=0, max_prompt_len=0) -> CacheConfig:
+    """A dmc_cache_config; num_pages defaults to room for every unit at capacity."""
+    units = num_layers * batch * num_kv_heads
+    if num_pages is None:
+        num_pages = units * -(-max_slots_per_seq // page_size)
+    return CacheConfig(num_layers, batch, num_q_heads, num_kv_heads, head_dim,
+                       DMC_FP32 if dtype in ("fp32", "float32") else DMC_BF16, page_size,
+                       max_slots_per_seq, num_pages, decision_bias,
+                       DMC_OMEGA_GROUP_MEAN if omega_src == "group_mean" else DMC_OMEGA_LEAD_QHEAD,
+                       split_tile, max_prompt_len)
+
+
+def workspace_bytes(cfg: CacheConfig) -> int:
+    n = lib.dmc_cache_workspace_bytes(ctypes.byref(cfg))
+    if n == 0:
+        raise DMCError(DMC_ERR_INVALID_ARG, last_error())
+    return n
+
+
+def _ptr(t):
+    return None if t is None else c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return c_void_p(s.cuda_stream)
+
+
+class DMCCache:
+    """A paged DMC cache in one torch-allocated workspace on the current GPU.
+
+    Thin wrapper over the C ABI: shapes and dtypes are checked here only to
+    give Python errors; the library validates everything again.
+    """
+
+    def __init__(self, cfg: CacheConfig, device="cuda", stream=None):
+        import torch
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.dtype = torch.float32 if cfg.dtype == DMC_FP32 else torch.bfloat16
+        self.G = cfg.num_q_heads // cfg.num_kv_heads
+        nbytes = workspace_bytes(cfg)
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+        base = self.workspace.data_ptr()
+        self._ws_ptr = (base + 255) // 256 * 256
+        self._ws_bytes = nbytes
+        handle = c_void_p()
+        check(lib.dmc_cache_alloc(ctypes.byref(cfg), c_void_p(self._ws_ptr), nbytes,
+                                  _stream(stream), ctypes.byref(handle)))
+        self.handle = handle
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib.dmc_cache_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- hot path -------------------------------------------------------------
+    def decode_step(self, layer, q, k, v, out=None, slot_index=None, stream=None):
+        """Algorithm 1 update + attention for one layer; returns out [B, Hq, d]."""
+        if out is None:
+            out = torch_empty_like(q)
+        check(lib.dmc_decode_step(self.handle, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                  _ptr(slot_index), _stream(stream)))
+        return out
+
+    def prefill(self, layer, k, v, q, n=None, prompt_lens=None, slot_index=None, stream=None):
+        """Compress a prompt: k, v [B, n, Hkv, d] (strided), q [B, n, Hq, (d)]."""
+        n = k.shape[1] if n is None else n
+        ks = (c_int64 * 3)(k.stride(0), k.stride(1), k.stride(2))
+        vs = (c_int64 * 3)(v.stride(0), v.stride(1), v.stride(2))
+        qs = (c_int64 * 3)(q.stride(0), q.stride(1), q.stride(2))
+        check(lib.dmc_prefill_compress(self.handle, layer, _ptr(k), ks, _ptr(v), vs, _ptr(q), qs,
+                                       n, _ptr(prompt_lens), _ptr(slot_index), _stream(stream)))
+
+    # -- accessors --------------------------------------------------------------
+    def lengths(self, layer, stream=None):
+        import torch
+        out = torch.empty((self.cfg.batch, self.cfg.num_kv_heads), dtype=torch.int32,
+                          device=self.device)
+        check(lib.dmc_cache_lengths(self.handle, layer, _ptr(out), _stream(stream)))
+        return out
+
+    def export(self, layer, dense_slots=None, stream=None):
+        import torch
+        dense_slots = self.cfg.max_slots_per_seq if dense_slots is None else dense_slots
+        shape = (self.cfg.batch, self.cfg.num_kv_heads, dense_slots, self.cfg.head_dim)
+        K = torch.empty(shape, dtype=self.dtype, device=self.device)
+        V = torch.empty(shape, dtype=self.dtype, device=self.device)
+        z = torch.empty(shape[:2], dtype=torch.float32, device=self.device)
+        check(lib.dmc_cache_export(self.handle, layer, _ptr(K), _ptr(V), dense_slots, _ptr(z),
+                                   _stream(stream)))
+        return K, V, z
+
+    def import_(self, layer, K, V, lengths, z, stream=None):
+        check(lib.dmc_cache_import(self.handle, layer, _ptr(K), _ptr(V), K.shape[2],
+                                   _ptr(lengths), _ptr(z), _stream(stream)))
+
+    def check(self, stream=None):
+        check(lib.dmc_cache_check(self.handle, _stream(stream)))
+
+    def status(self, stream=None) -> int:
+        return lib.dmc_cache_check(self.handle, _stream(stream))
+
+    def pages_used(self, stream=None) -> int:
+        n = c_int64()
+        check(lib.dmc_cache_pages_used(self.handle, ctypes.byref(n), _stream(stream)))
+        return n.value
+
+    def reset(self, stream=None):
+        check(lib.dmc_cache_reset(self.handle, _stream(stream)))
+
+
+def torch_empty_like(t):
+    import torch
+    return torch.empty_like(t, memory_format=torch.contiguous_format)

@@ -1,0 +1,466 @@
+// Host side of the DMC C ABI: configuration and argument validation,
+// workspace layout, per-layer state and kernel launches.
+//
+// Every validation runs before the first HIP call of an entry point, so an
+// invalid request returns its status without touching the device (and can
+// be exercised on a machine with no GPU).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/dmc.h"
+#include "dmc_internal.h"
+
+using dmc::align_up;
+
+struct dmc_cache {
+  dmc_cache_config cfg;
+  dmc::Layout lay;
+  char *ws;
+  size_t ws_bytes;
+  int device;
+  int cu_count;
+  std::vector<uint8_t> parity;  // per layer: which lengths buffer is current
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+dmc_status fail(dmc_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+dmc_status hip_fail(hipError_t e, const char *what) {
+  return fail(DMC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+int ilog2(int64_t x) {
+  int r = 0;
+  while ((int64_t(1) << r) < x) ++r;
+  return r;
+}
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kDefaultTile = 256;
+constexpr size_t kMaxDecodeLds = 64 * 1024;
+
+int elem_bytes(const dmc_cache_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
+
+dmc_status validate_config(const dmc_cache_config *c) {
+  if (!c) return fail(DMC_ERR_INVALID_ARG, "config is NULL");
+  if (c->num_layers < 1 || c->batch < 1 || c->num_kv_heads < 1 || c->num_q_heads < 1)
+    return fail(DMC_ERR_INVALID_ARG, "layers, batch and head counts must be >= 1");
+  if (c->num_q_heads % c->num_kv_heads != 0)
+    return fail(DMC_ERR_INVALID_ARG, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)",
+                c->num_q_heads, c->num_kv_heads);
+  const int G = c->num_q_heads / c->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(DMC_ERR_UNSUPPORTED, "query group size %d not in {1,2,4,8}", G);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(DMC_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", c->head_dim);
+  if (c->dtype != DMC_BF16 && c->dtype != DMC_FP32)
+    return fail(DMC_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+  if (!pow2(c->page_size) || c->page_size < 8 || c->page_size > 256)
+    return fail(DMC_ERR_UNSUPPORTED, "page_size %d must be a power of two in [8,256]", c->page_size);
+  if (c->max_slots_per_seq < 1)
+    return fail(DMC_ERR_INVALID_ARG, "max_slots_per_seq must be >= 1");
+  if (c->num_pages < 1 || c->num_pages >= (int64_t(1) << 31))
+    return fail(DMC_ERR_INVALID_ARG, "num_pages %lld outside [1, 2^31)",
+                static_cast<long long>(c->num_pages));
+  if (!std::isfinite(c->decision_bias)) return fail(DMC_ERR_INVALID_ARG, "decision_bias not finite");
+  if (c->omega_src != DMC_OMEGA_LEAD_QHEAD && c->omega_src != DMC_OMEGA_GROUP_MEAN)
+    return fail(DMC_ERR_INVALID_ARG, "unknown omega_src %d", c->omega_src);
+  if (c->split_tile < 0) return fail(DMC_ERR_INVALID_ARG, "split_tile must be >= 0");
+  if (c->max_prompt_len < 0 || c->max_prompt_len > c->max_slots_per_seq)
+    return fail(DMC_ERR_INVALID_ARG, "max_prompt_len must be in [0, max_slots_per_seq]");
+  const int64_t units = int64_t(c->batch) * c->num_kv_heads;
+  if (units > (int64_t(1) << 20)) return fail(DMC_ERR_UNSUPPORTED, "too many units per layer");
+  if (dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim) > kMaxDecodeLds)
+    return fail(DMC_ERR_UNSUPPORTED,
+                "batch * num_kv_heads = %lld units exceed the decode kernel's LDS tile table",
+                static_cast<long long>(units));
+  return DMC_OK;
+}
+
+dmc::Layout make_layout(const dmc_cache_config &c) {
+  dmc::Layout L{};
+  const int es = elem_bytes(c);
+  L.units = c.batch * c.num_kv_heads;
+  L.group = c.num_q_heads / c.num_kv_heads;
+  L.maxpages = static_cast<int32_t>((int64_t(c.max_slots_per_seq) + c.page_size - 1) / c.page_size);
+  L.split_tile = c.split_tile > 0 ? c.split_tile : kDefaultTile;
+  L.tiles_per_unit = (c.max_slots_per_seq > 0 ? c.max_slots_per_seq - 1 : 0) / L.split_tile + 1;
+  L.max_prompt = c.max_prompt_len > 0 ? c.max_prompt_len : c.max_slots_per_seq;
+  L.prompt_chunks = (L.max_prompt + 63) / 64;
+  L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
+  const size_t U = size_t(L.units), NL = size_t(c.num_layers);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  L.pool = take(size_t(c.num_pages) * size_t(L.page_bytes));
+  L.ptab = take(NL * U * size_t(L.maxpages) * 4);
+  L.lens = take(2 * NL * U * 4);
+  L.z = take(NL * U * 4);
+  L.ctrl = take(sizeof(dmc::Control));
+  L.meta = take(U * 2 * 4);
+  L.partials = take(U * size_t(L.tiles_per_unit) * L.group * (c.head_dim + 4) * 4);
+  L.pf_alpha = take(U * size_t(L.max_prompt));
+  L.pf_omega = take(U * size_t(L.max_prompt) * 4);
+  L.pf_count = take(U * size_t(L.prompt_chunks) * 4);
+  L.pf_pagebase = take(U * 4);
+  L.total = off;
+  return L;
+}
+
+// Runs the enqueue on the cache's device, restoring the caller's afterwards.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) {
+      ok = false;
+      return;
+    }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+template <typename T>
+T *at(const dmc_cache *c, size_t off) {
+  return reinterpret_cast<T *>(c->ws + off);
+}
+
+int32_t *lens_of(const dmc_cache *c, int layer, int parity) {
+  return at<int32_t>(c, c->lay.lens) + (size_t(parity) * c->cfg.num_layers + layer) * c->lay.units;
+}
+
+dmc_status check_layer(const dmc_cache *c, int32_t layer) {
+  if (!c) return fail(DMC_ERR_INVALID_ARG, "cache is NULL");
+  if (layer < 0 || layer >= c->cfg.num_layers)
+    return fail(DMC_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, c->cfg.num_layers);
+  return DMC_OK;
+}
+
+dmc_status enqueue_reset(dmc_cache *c, hipStream_t s) {
+  const size_t U = c->lay.units, NL = c->cfg.num_layers;
+  hipError_t e;
+  if ((e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.lens), 0, 2 * NL * U, s)) != hipSuccess)
+    return hip_fail(e, "reset lengths");
+  if ((e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.z), 0, NL * U, s)) != hipSuccess)
+    return hip_fail(e, "reset z");
+  if ((e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.ptab), -1, NL * U * c->lay.maxpages, s)) !=
+      hipSuccess)
+    return hip_fail(e, "reset page table");
+  if ((e = dmc::launch_fill_u8(c->ws + c->lay.ctrl, sizeof(dmc::Control), s)) != hipSuccess)
+    return hip_fail(e, "reset control block");
+  if ((e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.meta), 0, 2 * U, s)) != hipSuccess)
+    return hip_fail(e, "reset tile table");
+  for (auto &p : c->parity) p = 0;
+  return DMC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *dmc_last_error(void) { return g_err.c_str(); }
+
+size_t dmc_cache_workspace_bytes(const dmc_cache_config *cfg) {
+  if (validate_config(cfg) != DMC_OK) return 0;
+  return make_layout(*cfg).total;
+}
+
+dmc_status dmc_cache_alloc(const dmc_cache_config *cfg, void *workspace, size_t bytes,
+                           dmc_stream_t stream, dmc_cache **out) {
+  if (!out) return fail(DMC_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  dmc_status st = validate_config(cfg);
+  if (st != DMC_OK) return st;
+  if (!workspace) return fail(DMC_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(DMC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const dmc::Layout lay = make_layout(*cfg);
+  if (bytes < lay.total)
+    return fail(DMC_ERR_INVALID_ARG, "workspace has %zu bytes, needs %zu", bytes, lay.total);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  dmc_cache *c = new (std::nothrow) dmc_cache();
+  if (!c) return fail(DMC_ERR_INVALID_ARG, "out of host memory");
+  c->cfg = *cfg;
+  c->lay = lay;
+  c->ws = static_cast<char *>(workspace);
+  c->ws_bytes = bytes;
+  c->device = dev;
+  c->cu_count = cus > 0 ? cus : 256;
+  c->parity.assign(cfg->num_layers, 0);
+  st = enqueue_reset(c, static_cast<hipStream_t>(stream));
+  if (st != DMC_OK) {
+    delete c;
+    return st;
+  }
+  *out = c;
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_free(dmc_cache *cache) {
+  if (!cache) return fail(DMC_ERR_INVALID_ARG, "cache is NULL");
+  delete cache;
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream) {
+  if (!cache) return fail(DMC_ERR_INVALID_ARG, "cache is NULL");
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  return enqueue_reset(cache, static_cast<hipStream_t>(stream));
+}
+
+dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const void *k,
+                           const void *v, void *out, int32_t *slot_index, dmc_stream_t stream) {
+  dmc_status st = check_layer(cache, layer);
+  if (st != DMC_OK) return st;
+  if (!q || !k || !v || !out) return fail(DMC_ERR_INVALID_ARG, "q, k, v and out must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(DMC_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
+  const dmc_cache_config &c = cache->cfg;
+  const dmc::Layout &L = cache->lay;
+  const int par = cache->parity[layer];
+  dmc::DecodeParams p{};
+  p.pool = cache->ws + L.pool;
+  p.page_bytes = L.page_bytes;
+  p.num_pages = c.num_pages;
+  p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
+  p.len_in = lens_of(cache, layer, par);
+  p.len_out = lens_of(cache, layer, par ^ 1);
+  p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
+  p.ctrl = at<dmc::Control>(cache, L.ctrl);
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.out = out;
+  p.slot_index = slot_index;
+  p.partials = at<float>(cache, L.partials);
+  p.meta = at<int32_t>(cache, L.meta);
+  p.c = c.decision_bias;
+  p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(c.head_dim)));
+  p.units = L.units;
+  p.hkv = c.num_kv_heads;
+  p.hq = c.num_q_heads;
+  p.maxpages = L.maxpages;
+  p.max_slots = c.max_slots_per_seq;
+  p.log2p = ilog2(c.page_size);
+  p.split_tile = L.split_tile;
+  p.omega_src = c.omega_src;
+  const int64_t tiles = int64_t(L.units) * L.tiles_per_unit;
+  const int64_t cap = int64_t(cache->cu_count) * 8;
+  const int grid = static_cast<int>(tiles < cap ? tiles : cap);
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, p, grid,
+                                    static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  cache->parity[layer] = static_cast<uint8_t>(par ^ 1);
+  return DMC_OK;
+}
+
+dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
+                                const int64_t k_strides[3], const void *v,
+                                const int64_t v_strides[3], const void *q,
+                                const int64_t q_strides[3], int32_t n,
+                                const int32_t *prompt_lens, int32_t *slot_index,
+                                dmc_stream_t stream) {
+  dmc_status st = check_layer(cache, layer);
+  if (st != DMC_OK) return st;
+  const dmc_cache_config &c = cache->cfg;
+  const dmc::Layout &L = cache->lay;
+  if (n < 0 || n > L.max_prompt)
+    return fail(DMC_ERR_INVALID_ARG, "prompt length %d outside [0, %d]", n, L.max_prompt);
+  if (n > 0) {
+    if (!k || !v || !q) return fail(DMC_ERR_INVALID_ARG, "k, v and q must be non-NULL");
+    if (!k_strides || !v_strides || !q_strides)
+      return fail(DMC_ERR_INVALID_ARG, "stride arrays must be non-NULL");
+    if (!aligned16(k) || !aligned16(v))
+      return fail(DMC_ERR_INVALID_ARG, "k and v must be 16-byte aligned");
+    for (int i = 0; i < 3; ++i) {
+      if (k_strides[i] < 0 || v_strides[i] < 0 || q_strides[i] < 0)
+        return fail(DMC_ERR_INVALID_ARG, "strides must be non-negative");
+      if (k_strides[i] % 8 || v_strides[i] % 8)
+        return fail(DMC_ERR_INVALID_ARG, "k and v strides must be multiples of 8 elements");
+    }
+  }
+  dmc::PrefillParams p{};
+  p.pool = cache->ws + L.pool;
+  p.page_bytes = L.page_bytes;
+  p.num_pages = c.num_pages;
+  p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
+  p.len = lens_of(cache, layer, cache->parity[layer]);
+  p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
+  p.ctrl = at<dmc::Control>(cache, L.ctrl);
+  p.k = k;
+  p.v = v;
+  p.q = q;
+  for (int i = 0; i < 3; ++i) {
+    p.ks[i] = n > 0 ? k_strides[i] : 0;
+    p.vs[i] = n > 0 ? v_strides[i] : 0;
+    p.qs[i] = n > 0 ? q_strides[i] : 0;
+  }
+  p.prompt_lens = prompt_lens;
+  p.slot_index = slot_index;
+  p.alpha = at<uint8_t>(cache, L.pf_alpha);
+  p.omega = at<float>(cache, L.pf_omega);
+  p.count = at<int32_t>(cache, L.pf_count);
+  p.page_base = at<int32_t>(cache, L.pf_pagebase);
+  p.c = c.decision_bias;
+  p.n = n;
+  p.units = L.units;
+  p.hkv = c.num_kv_heads;
+  p.hq = c.num_q_heads;
+  p.maxpages = L.maxpages;
+  p.log2p = ilog2(c.page_size);
+  p.omega_src = c.omega_src;
+  p.max_prompt = L.max_prompt;
+  p.prompt_chunks = L.prompt_chunks;
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_lengths(const dmc_cache *cache, int32_t layer, int32_t *lengths,
+                             dmc_stream_t stream) {
+  dmc_status st = check_layer(cache, layer);
+  if (st != DMC_OK) return st;
+  if (!lengths) return fail(DMC_ERR_INVALID_ARG, "lengths is NULL");
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipError_t e = dmc::launch_copy_i32(lengths, lens_of(cache, layer, cache->parity[layer]),
+                                      cache->lay.units, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "lengths copy");
+  return DMC_OK;
+}
+
+static dmc::DenseParams dense_params(const dmc_cache *cache, int32_t layer, int32_t dense_slots) {
+  const dmc::Layout &L = cache->lay;
+  dmc::DenseParams p{};
+  p.pool = cache->ws + L.pool;
+  p.page_bytes = L.page_bytes;
+  p.num_pages = cache->cfg.num_pages;
+  p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
+  p.len = lens_of(cache, layer, cache->parity[layer]);
+  p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
+  p.ctrl = at<dmc::Control>(cache, L.ctrl);
+  p.page_base = at<int32_t>(cache, L.pf_pagebase);
+  p.dense_slots = dense_slots;
+  p.units = L.units;
+  p.maxpages = L.maxpages;
+  p.log2p = ilog2(cache->cfg.page_size);
+  p.max_slots = cache->cfg.max_slots_per_seq;
+  return p;
+}
+
+dmc_status dmc_cache_export(const dmc_cache *cache, int32_t layer, void *k_dense, void *v_dense,
+                            int32_t dense_slots, float *z, dmc_stream_t stream) {
+  dmc_status st = check_layer(cache, layer);
+  if (st != DMC_OK) return st;
+  if (dense_slots < 0) return fail(DMC_ERR_INVALID_ARG, "dense_slots must be >= 0");
+  if (!z || (dense_slots > 0 && (!k_dense || !v_dense)))
+    return fail(DMC_ERR_INVALID_ARG, "k_dense, v_dense and z must be non-NULL");
+  if (!aligned16(k_dense) || !aligned16(v_dense))
+    return fail(DMC_ERR_INVALID_ARG, "dense tensors must be 16-byte aligned");
+  dmc::DenseParams p = dense_params(cache, layer, dense_slots);
+  p.kd = k_dense;
+  p.vd = v_dense;
+  p.z_out = z;
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipError_t e = dmc::launch_export(elem_bytes(cache->cfg), cache->cfg.head_dim, p,
+                                    static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "export launch");
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense,
+                            const void *v_dense, int32_t dense_slots, const int32_t *lengths,
+                            const float *z, dmc_stream_t stream) {
+  dmc_status st = check_layer(cache, layer);
+  if (st != DMC_OK) return st;
+  if (dense_slots < 0) return fail(DMC_ERR_INVALID_ARG, "dense_slots must be >= 0");
+  if (!lengths || !z || (dense_slots > 0 && (!k_dense || !v_dense)))
+    return fail(DMC_ERR_INVALID_ARG, "k_dense, v_dense, lengths and z must be non-NULL");
+  if (!aligned16(k_dense) || !aligned16(v_dense))
+    return fail(DMC_ERR_INVALID_ARG, "dense tensors must be 16-byte aligned");
+  dmc::DenseParams p = dense_params(cache, layer, dense_slots);
+  p.kd = const_cast<void *>(k_dense);
+  p.vd = const_cast<void *>(v_dense);
+  p.lengths_in = lengths;
+  p.z_in = z;
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipError_t e = dmc::launch_import(elem_bytes(cache->cfg), cache->cfg.head_dim, p,
+                                    static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "import launch");
+  return DMC_OK;
+}
+
+static dmc_status read_control(dmc_cache *cache, dmc_stream_t stream, dmc::Control *out) {
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  e = hipMemcpy(out, cache->ws + cache->lay.ctrl, sizeof(dmc::Control), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "reading the control block");
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_check(dmc_cache *cache, dmc_stream_t stream) {
+  if (!cache) return fail(DMC_ERR_INVALID_ARG, "cache is NULL");
+  dmc::Control ctl{};
+  dmc_status st = read_control(cache, stream, &ctl);
+  if (st != DMC_OK) return st;
+  if (ctl.flags & (dmc::FLAG_POOL_EXHAUSTED | dmc::FLAG_SLOTS_EXHAUSTED))
+    return fail(DMC_ERR_CAPACITY, "cache capacity exhausted (flags 0x%x: %s%s)", ctl.flags,
+                (ctl.flags & dmc::FLAG_POOL_EXHAUSTED) ? "page pool " : "",
+                (ctl.flags & dmc::FLAG_SLOTS_EXHAUSTED) ? "slots per unit" : "");
+  if (ctl.flags & dmc::FLAG_BAD_LENGTH)
+    return fail(DMC_ERR_INVALID_ARG, "an imported or prompt length was out of range");
+  return DMC_OK;
+}
+
+dmc_status dmc_cache_pages_used(dmc_cache *cache, int64_t *pages_out, dmc_stream_t stream) {
+  if (!cache || !pages_out) return fail(DMC_ERR_INVALID_ARG, "cache and pages_out must be non-NULL");
+  dmc::Control ctl{};
+  dmc_status st = read_control(cache, stream, &ctl);
+  if (st != DMC_OK) return st;
+  const unsigned long long used = ctl.pages_used;
+  const unsigned long long cap = static_cast<unsigned long long>(cache->cfg.num_pages);
+  *pages_out = static_cast<int64_t>(used < cap ? used : cap);
+  return DMC_OK;
+}
+
+}  // extern "C"

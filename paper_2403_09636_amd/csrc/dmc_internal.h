@@ -1,0 +1,111 @@
+// Internal declarations shared by the host API (dmc_api.cpp) and the gfx950
+// kernels (dmc_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dmc {
+
+__host__ __device__ constexpr inline size_t align_up(size_t x, size_t a) {
+  return (x + a - 1) / a * a;
+}
+
+// Device flag bits (sticky until reset).
+enum : int32_t {
+  FLAG_POOL_EXHAUSTED = 1,   // no free page for an append
+  FLAG_SLOTS_EXHAUSTED = 2,  // unit already holds max_slots_per_seq slots
+  FLAG_BAD_LENGTH = 4,       // imported length or prompt length out of range
+};
+
+// Control block at the start of the control section.
+struct Control {
+  unsigned long long pages_used;  // bump allocator of the page pool
+  int32_t flags;
+  int32_t pad[13];
+};
+
+// Byte offsets of the workspace sections (all 256-byte aligned).
+struct Layout {
+  size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_pagebase;
+  size_t total;
+  int64_t page_bytes;     // 2 * P * d * elem_bytes (K rows, then V rows)
+  int32_t units;          // B * Hkv per layer
+  int32_t maxpages;       // page-table width per unit
+  int32_t group;          // G
+  int32_t split_tile;     // T
+  int32_t tiles_per_unit; // upper bound of decode tiles per unit
+  int32_t max_prompt;     // prefill staging capacity (tokens)
+  int32_t prompt_chunks;  // ceil(max_prompt / 64)
+};
+
+// Everything the decode kernel needs for one layer.
+struct DecodeParams {
+  char *pool;
+  int64_t page_bytes;
+  int64_t num_pages;
+  int32_t *ptab;           // [U, maxpages] of this layer
+  const int32_t *len_in;   // [U] lengths before this step
+  int32_t *len_out;        // [U] lengths after this step (other parity buffer)
+  float *z;                // [U]
+  Control *ctrl;
+  const void *q, *k, *v;
+  void *out;
+  int32_t *slot_index;     // optional [U]
+  float *partials;         // [tiles, G, d + 4]
+  int32_t *meta;           // [U, 2]: first tile, tile count
+  float c;                 // decision bias
+  float scale_log2;        // log2(e) / sqrt(d)
+  int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src;
+};
+
+struct PrefillParams {
+  char *pool;
+  int64_t page_bytes;
+  int64_t num_pages;
+  int32_t *ptab;
+  int32_t *len;            // [U] current-parity lengths of this layer
+  float *z;
+  Control *ctrl;
+  const void *k, *v, *q;
+  int64_t ks[3], vs[3], qs[3];
+  const int32_t *prompt_lens;
+  int32_t *slot_index;     // optional [U, n]
+  uint8_t *alpha;          // [U, max_prompt]
+  float *omega;            // [U, max_prompt]
+  int32_t *count;          // [U, prompt_chunks]
+  int32_t *page_base;      // [U]
+  float c;
+  int32_t n, units, hkv, hq, maxpages, log2p, omega_src, max_prompt, prompt_chunks;
+};
+
+struct DenseParams {
+  char *pool;
+  int64_t page_bytes;
+  int64_t num_pages;
+  int32_t *ptab;
+  int32_t *len;
+  float *z;
+  Control *ctrl;
+  void *kd, *vd;           // dense [U, dense_slots, d]
+  const int32_t *lengths_in;
+  const float *z_in;
+  float *z_out;
+  int32_t *page_base;
+  int32_t dense_slots, units, maxpages, log2p, max_slots;
+};
+
+// Launchers (return hipGetLastError() after enqueueing).
+hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s);
+hipError_t launch_fill_u8(void *p, size_t bytes, hipStream_t s);
+hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, size_t count, hipStream_t s);
+hipError_t launch_decode(int elem_bytes, int head_dim, int group, const DecodeParams &p,
+                         int grid, hipStream_t s);
+hipError_t launch_prefill(int elem_bytes, int head_dim, const PrefillParams &p, hipStream_t s);
+hipError_t launch_import(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s);
+hipError_t launch_export(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s);
+
+// Dynamic LDS bytes of the decode kernel for a unit count / group / head dim.
+size_t decode_lds_bytes(int units, int group, int head_dim);
+
+}  // namespace dmc

@@ -1,0 +1,899 @@
+// gfx950 kernels of the DMC decode path.
+//
+// Method: Nawrot et al., "Dynamic Memory Compression" (ICML 2024).
+//   Sec. 3.1 + Algorithm 1: per-head decision alpha = round(sigmoid(k[0] - c))
+//   (= k[0] > c), importance omega = sigmoid(q[0]); accumulate into the last
+//   slot as an omega-weighted running mean, or append a slot.
+//   Sec. 3.1 (last paragraph) + Sec. 2.1: softmax attention over the ragged,
+//   per-head compressed cache.  Sec. 3.3: paged storage, pages per head.
+//
+// Memory layout (one workspace, see dmc_api.cpp):
+//   page pool: page = P key rows then P value rows, each row d contiguous
+//              elements; a row is 128..512 bytes, a page 2*P*row bytes.
+//   page table [L][U][maxpages] int32, lengths [2][L][U] int32 (double
+//   buffered: a decode step reads one parity and writes the other, so every
+//   workgroup sees the same pre-step lengths), z [L][U] fp32.
+//
+// Decode = one fused launch (update + split-K attention) plus a combine
+// launch for units split over several tiles.  Tiles come from the pre-step
+// lengths: unit u has nt = floor(max(l-1, 0) / T) + 1 tiles; tiles 0..nt-2
+// cover closed slots only, the last ("tail") tile covers the rest, owns the
+// open slot and performs the unit's Algorithm 1 update before attending to
+// it.  No other tile touches the open slot, so the fusion is race free.
+#include "dmc_internal.h"
+
+namespace dmc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kChunk = 32;  // max rows a wave streams per chunk
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (quiet NaN preserved).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) | 0x40u) & 0xffffu;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int ES>
+__device__ __forceinline__ float load_elem(const void *base, int64_t idx);
+template <>
+__device__ __forceinline__ float load_elem<2>(const void *base, int64_t idx) {
+  return __uint_as_float(uint32_t(static_cast<const uint16_t *>(base)[idx]) << 16);
+}
+template <>
+__device__ __forceinline__ float load_elem<4>(const void *base, int64_t idx) {
+  return static_cast<const float *>(base)[idx];
+}
+
+// 16-byte vector <-> floats.
+template <int ES>
+struct V16;
+template <>
+struct V16<2> {
+  static constexpr int N = 8;
+  __device__ static __forceinline__ void unpack(const uint4 &r, float *f) {
+    f[0] = bf16_lo(r.x); f[1] = bf16_hi(r.x); f[2] = bf16_lo(r.y); f[3] = bf16_hi(r.y);
+    f[4] = bf16_lo(r.z); f[5] = bf16_hi(r.z); f[6] = bf16_lo(r.w); f[7] = bf16_hi(r.w);
+  }
+  // Round to storage; f is replaced by the widened stored values.
+  __device__ static __forceinline__ uint4 pack(float *f) {
+    uint32_t h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      h[i] = bf16_bits(f[i]);
+      f[i] = __uint_as_float(h[i] << 16);
+    }
+    return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                      h[6] | (h[7] << 16));
+  }
+};
+template <>
+struct V16<4> {
+  static constexpr int N = 4;
+  __device__ static __forceinline__ void unpack(const uint4 &r, float *f) {
+    f[0] = __uint_as_float(r.x); f[1] = __uint_as_float(r.y);
+    f[2] = __uint_as_float(r.z); f[3] = __uint_as_float(r.w);
+  }
+  __device__ static __forceinline__ uint4 pack(float *f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                      __float_as_uint(f[3]));
+  }
+};
+
+__device__ __forceinline__ uint4 ld16(const char *p) { return *reinterpret_cast<const uint4 *>(p); }
+__device__ __forceinline__ void st16(char *p, const uint4 &v) { *reinterpret_cast<uint4 *>(p) = v; }
+
+// E consecutive elements (E = 1 or 2) <-> floats, for the prefill/combine paths.
+template <int ES, int E>
+__device__ __forceinline__ void load_e(const char *p, float *f) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) f[e] = load_elem<ES>(p, e);
+}
+template <int ES, int E>
+__device__ __forceinline__ void store_e(char *p, const float *f) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if (ES == 2)
+      reinterpret_cast<uint16_t *>(p)[e] = static_cast<uint16_t>(bf16_bits(f[e]));
+    else
+      reinterpret_cast<float *>(p)[e] = f[e];
+  }
+}
+
+__device__ __forceinline__ float sigmoid_floor(float x) {
+  // omega = sigmoid(x), floored at 2^-100 so a running sum never reaches 0.
+  return fmaxf(1.0f / (1.0f + expf(-x)), 0x1p-100f);
+}
+
+template <int LPR>
+__device__ __forceinline__ float row_sum(float x) {
+#pragma unroll
+  for (int o = 1; o < LPR; o <<= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+
+// Merge (m2, l2, a2) into (m, l, a); scores are in the log2 domain.
+template <int N>
+__device__ __forceinline__ void merge_state(float &m, float &l, float *a, float m2, float l2,
+                                            const float *a2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == neg_inf()) return;
+  const float s1 = exp2f(m - mn), s2 = exp2f(m2 - mn);
+  l = l * s1 + l2 * s2;
+#pragma unroll
+  for (int e = 0; e < N; ++e) a[e] = a[e] * s1 + a2[e] * s2;
+  m = mn;
+}
+
+// ---------------------------------------------------------------------------
+// Fused decode: Algorithm 1 update + split-K attention partials.
+// ---------------------------------------------------------------------------
+template <int ES, int D, int G>
+__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+  using V = V16<ES>;
+  constexpr int VN = V::N;        // elements per 16-byte lane chunk
+  constexpr int LPR = D / VN;     // lanes per cache row
+  constexpr int RPI = 64 / LPR;   // rows per wave-wide load
+  constexpr int NI = kChunk / RPI;
+  constexpr int REC = D + 4;      // partial record: m, l, -, -, acc[D]
+  constexpr int RB = D * ES;      // bytes per row
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_wsum[kWaves];
+  __shared__ int s_has_cur;
+  const int U = p.units;
+  int *s_pre = reinterpret_cast<int *>(smem);
+  float *s_mrg = reinterpret_cast<float *>(smem + align_up(size_t(U + 1) * 4, 16));
+  float *s_cur = s_mrg + kWaves * G * REC;  // [2][D] key, value of the current slot
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = lane / LPR, part = lane % LPR;
+  const int T = p.split_tile;
+  const int P = 1 << p.log2p;
+  const int CS = P < kChunk ? P : kChunk;
+  const int log2cs = p.log2p < 5 ? p.log2p : 5;
+
+  // Exclusive prefix of per-unit tile counts over the pre-step lengths.
+  {
+    const int per = (U + kThreads - 1) / kThreads;
+    const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
+    int sum = 0;
+    for (int i = i0; i < i1; ++i) {
+      const int l = p.len_in[i];
+      const int nt = (l > 0 ? l - 1 : 0) / T + 1;
+      s_pre[i] = nt;
+      sum += nt;
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int run = incl - sum, total = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) run += s_wsum[w];
+      total += s_wsum[w];
+    }
+    for (int i = i0; i < i1; ++i) {
+      const int nt = s_pre[i];
+      s_pre[i] = run;
+      run += nt;
+    }
+    if (tid == 0) s_pre[U] = total;
+    __syncthreads();
+  }
+  const int NT = s_pre[U];
+
+  for (int t = blockIdx.x; t < NT; t += gridDim.x) {
+    int lo = 0, hi = U - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_pre[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const int u = lo;
+    const int first = s_pre[u], nt = s_pre[u + 1] - first, ti = t - first;
+    const bool tail = ti == nt - 1;
+    const int l = p.len_in[u];
+    const int b = u / p.hkv, g = u - b * p.hkv;
+    const int start = ti * T;
+    int end = start + T;
+    int alpha = 0;
+    if (tail) {
+      const float k0 = load_elem<ES>(p.k, int64_t(u) * D);
+      alpha = (l > 0 && k0 > p.c) ? 1 : 0;
+      end = alpha ? l - 1 : l;
+    }
+
+    // This tile's query heads, element 0 zeroed, pre-scaled by log2(e)/sqrt(d).
+    float qf[G][VN];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const char *qp = static_cast<const char *>(p.q) +
+                       (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
+      V::unpack(ld16(qp), qf[h]);
+      if (part == 0) qf[h][0] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < VN; ++e) qf[h][e] *= p.scale_log2;
+    }
+
+    // Tail tile: Algorithm 1 for unit u (wave 0; lanes of row group 0 store).
+    if (tail && wave == 0) {
+      float om;
+      if (p.omega_src == 0) {
+        om = sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D));
+      } else {
+        float s = 0.0f;
+        for (int h = 0; h < G; ++h)
+          s += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
+        om = fmaxf(s / G, 0x1p-100f);
+      }
+      float kf[VN], vf[VN];
+      V::unpack(ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES), kf);
+      V::unpack(ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES), vf);
+      if (part == 0) kf[0] = 0.0f;  // Algorithm 1: k_t[0] <- 0
+      const int64_t pt = int64_t(u) * p.maxpages;
+      int has_cur = 1, flag = 0, slot, page = -1;
+      float znew;
+      if (alpha) {
+        slot = l - 1;
+        page = p.ptab[pt + (slot >> p.log2p)];
+        const char *kr = p.pool + int64_t(page) * p.page_bytes +
+                         int64_t(slot & (P - 1)) * RB + part * 16;
+        float ok[VN], ov[VN];
+        V::unpack(ld16(kr), ok);
+        V::unpack(ld16(kr + int64_t(P) * RB), ov);
+        const float zold = p.z[u];
+        znew = zold + om;
+#pragma unroll
+        for (int e = 0; e < VN; ++e) {
+          kf[e] = (ok[e] * zold + kf[e] * om) / znew;
+          vf[e] = (ov[e] * zold + vf[e] * om) / znew;
+        }
+      } else {
+        slot = l;
+        znew = om;
+        if (l >= p.max_slots) {
+          has_cur = 0;
+          flag = FLAG_SLOTS_EXHAUSTED;
+        } else if ((l & (P - 1)) == 0) {
+          int pg = 0;
+          if (lane == 0) {
+            const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
+            pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
+          }
+          pg = __shfl(pg, 0, 64);
+          if (pg < 0) {
+            has_cur = 0;
+            flag = FLAG_POOL_EXHAUSTED;
+          } else {
+            page = pg;
+            if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
+          }
+        } else {
+          page = p.ptab[pt + (l >> p.log2p)];
+        }
+      }
+      if (has_cur) {
+        const uint4 kp = V::pack(kf), vp = V::pack(vf);
+        if (grp == 0) {
+          char *kr = p.pool + int64_t(page) * p.page_bytes + int64_t(slot & (P - 1)) * RB + part * 16;
+          st16(kr, kp);
+          st16(kr + int64_t(P) * RB, vp);
+#pragma unroll
+          for (int e = 0; e < VN; ++e) {
+            s_cur[part * VN + e] = kf[e];
+            s_cur[D + part * VN + e] = vf[e];
+          }
+        }
+      }
+      if (lane == 0) {
+        if (has_cur) p.z[u] = znew;
+        p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
+        if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
+        p.meta[2 * u] = first;
+        p.meta[2 * u + 1] = nt;
+        if (flag) atomicOr(&p.ctrl->flags, flag);
+        s_has_cur = has_cur;
+      }
+    }
+
+    // Split-K attention over the closed slots [start, end) of this tile.
+    float m[G], ls[G], acc[G][VN];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      m[h] = neg_inf();
+      ls[h] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < VN; ++e) acc[h][e] = 0.0f;
+    }
+    if (end > start) {
+      const int c0 = start >> log2cs, c1 = (end - 1) >> log2cs;
+      const int64_t pt = int64_t(u) * p.maxpages;
+      for (int ch = c0 + wave; ch <= c1; ch += kWaves) {
+        const int row0 = ch << log2cs;
+        const int rlo = max(start, row0) - row0, rhi = min(end, row0 + CS) - row0;
+        const int page = p.ptab[pt + (row0 >> p.log2p)];
+        const char *kb = p.pool + int64_t(page) * p.page_bytes + int64_t(row0 & (P - 1)) * RB +
+                         part * 16;
+        const char *vb = kb + int64_t(P) * RB;
+        uint4 kr[NI], vr[NI];
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int r = min(max(i * RPI + grp, rlo), rhi - 1);
+          kr[i] = ld16(kb + r * RB);
+        }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int r = min(max(i * RPI + grp, rlo), rhi - 1);
+          vr[i] = ld16(vb + r * RB);
+        }
+        float s[G][NI];
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          float kf[VN];
+          V::unpack(kr[i], kf);
+          const int r = i * RPI + grp;
+          const bool valid = r >= rlo && r < rhi;
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            float d = 0.0f;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], kf[e], d);
+            d = row_sum<LPR>(d);
+            s[h][i] = valid ? d : neg_inf();
+          }
+        }
+        float mn[G];
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          float mc = s[h][0];
+#pragma unroll
+          for (int i = 1; i < NI; ++i) mc = fmaxf(mc, s[h][i]);
+          mn[h] = fmaxf(m[h], mc);
+          if (mn[h] != neg_inf()) {
+            const float sc = exp2f(m[h] - mn[h]);
+            ls[h] *= sc;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) acc[h][e] *= sc;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+              s[h][i] = exp2f(s[h][i] - mn[h]);
+              ls[h] += s[h][i];
+            }
+            m[h] = mn[h];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          float vf[VN];
+          V::unpack(vr[i], vf);
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            if (mn[h] == neg_inf()) continue;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) acc[h][e] = fmaf(s[h][i], vf[e], acc[h][e]);
+          }
+        }
+      }
+    }
+
+    // Merge the RPI row groups of the wave, then the waves of the workgroup.
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float a2[VN];
+#pragma unroll
+        for (int e = 0; e < VN; ++e) a2[e] = __shfl_xor(acc[h][e], o, 64);
+        const float m2 = __shfl_xor(m[h], o, 64), l2 = __shfl_xor(ls[h], o, 64);
+        merge_state<VN>(m[h], ls[h], acc[h], m2, l2, a2);
+      }
+    }
+    if (grp == 0) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float *rec = s_mrg + (wave * G + h) * REC;
+        if (part == 0) {
+          rec[0] = m[h];
+          rec[1] = ls[h];
+        }
+#pragma unroll
+        for (int e = 0; e < VN; ++e) rec[4 + part * VN + e] = acc[h][e];
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const bool cur = tail && s_has_cur;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float M = neg_inf(), L = 0.0f, A[VN];
+#pragma unroll
+        for (int e = 0; e < VN; ++e) A[e] = 0.0f;
+        for (int w = 0; w < kWaves; ++w) {
+          const float *rec = s_mrg + (w * G + h) * REC;
+          float a2[VN];
+#pragma unroll
+          for (int e = 0; e < VN; ++e) a2[e] = rec[4 + part * VN + e];
+          merge_state<VN>(M, L, A, rec[0], rec[1], a2);
+        }
+        if (cur) {  // the slot Algorithm 1 just merged or appended
+          float d = 0.0f;
+#pragma unroll
+          for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], s_cur[part * VN + e], d);
+          d = row_sum<LPR>(d);
+          float a2[VN];
+#pragma unroll
+          for (int e = 0; e < VN; ++e) a2[e] = s_cur[D + part * VN + e];
+          merge_state<VN>(M, L, A, d, 1.0f, a2);
+        }
+        if (grp == 0) {
+          if (nt == 1) {
+            const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) A[e] *= inv;
+            char *op = static_cast<char *>(p.out) +
+                       (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
+            st16(op, V::pack(A));
+          } else {
+            float *rec = p.partials + (int64_t(t) * G + h) * REC;
+            if (part == 0) {
+              rec[0] = M;
+              rec[1] = L;
+            }
+#pragma unroll
+            for (int e = 0; e < VN; ++e) rec[4 + part * VN + e] = A[e];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Combine the split-K partials of units with more than one tile.
+template <int ES, int D, int G>
+__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int batch) {
+  constexpr int REC = D + 4;
+  constexpr int E = D / 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int bh = blockIdx.x * kWaves + wave;
+  if (bh >= batch * p.hq) return;
+  const int b = bh / p.hq, h = bh - b * p.hq;
+  const int g = h / G, hg = h - g * G;
+  const int u = b * p.hkv + g;
+  const int first = p.meta[2 * u], nt = p.meta[2 * u + 1];
+  if (nt <= 1) return;
+  float M = neg_inf();
+  for (int i = 0; i < nt; ++i) M = fmaxf(M, p.partials[(int64_t(first + i) * G + hg) * REC]);
+  float L = 0.0f, A[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) A[e] = 0.0f;
+  if (M != neg_inf()) {
+    for (int i = 0; i < nt; ++i) {
+      const float *rec = p.partials + (int64_t(first + i) * G + hg) * REC;
+      const float w = exp2f(rec[0] - M);
+      L = fmaf(w, rec[1], L);
+#pragma unroll
+      for (int e = 0; e < E; ++e) A[e] = fmaf(w, rec[4 + lane * E + e], A[e]);
+    }
+  }
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) A[e] *= inv;
+  store_e<ES, E>(static_cast<char *>(p.out) + (int64_t(bh) * D + lane * E) * ES, A);
+}
+
+// ---------------------------------------------------------------------------
+// Prefill compactor.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int prompt_len(const PrefillParams &p, int b, bool raise) {
+  if (!p.prompt_lens) return p.n;
+  int x = p.prompt_lens[b];
+  if (x < 0 || x > p.n) {
+    if (raise) atomicOr(&p.ctrl->flags, FLAG_BAD_LENGTH);
+    x = x < 0 ? 0 : p.n;
+  }
+  return x;
+}
+
+// Pass 1, one workgroup per unit: decisions (the first token always opens a
+// slot), importance scores, per-64-token start counts and the unit length.
+template <int ES>
+__global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams p) {
+  __shared__ int s_tot[kWaves];
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = u / p.hkv, g = u - b * p.hkv, G = p.hq / p.hkv;
+  const int nb = prompt_len(p, b, tid == 0);
+  int total = 0;
+  for (int t0 = 0; t0 < p.n; t0 += kThreads) {
+    const int t = t0 + tid;
+    int start = 0;
+    if (t < p.n) {
+      const bool valid = t < nb;
+      const float k0 = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + g * p.ks[2]);
+      const int a = (t > 0 && k0 > p.c) ? 1 : 0;
+      float om;
+      if (p.omega_src == 0) {
+        om = sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G) * p.qs[2]));
+      } else {
+        float s = 0.0f;
+        for (int h = 0; h < G; ++h)
+          s += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G + h) * p.qs[2]));
+        om = fmaxf(s / G, 0x1p-100f);
+      }
+      p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
+      p.omega[int64_t(u) * p.max_prompt + t] = om;
+      if (p.slot_index && !valid) p.slot_index[int64_t(u) * p.n + t] = -1;
+      start = (valid && !a) ? 1 : 0;
+    }
+    const unsigned long long mask = __ballot(start);
+    const int chunk = (t0 >> 6) + wave;
+    if (lane == 0 && chunk * 64 < p.n) {
+      p.count[int64_t(u) * p.prompt_chunks + chunk] = __popcll(mask);
+      total += __popcll(mask);
+    }
+  }
+  if (lane == 0) s_tot[wave] = total;
+  __syncthreads();
+  if (tid == 0) {
+    int l = 0;
+    for (int w = 0; w < kWaves; ++w) l += s_tot[w];
+    p.len[u] = l;
+  }
+}
+
+// Pass 2 (also used by import), one workgroup: pages for every unit by an
+// exclusive scan of ceil(l / P), contiguous per unit, from the bump pointer.
+__global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *z,
+                                                           int32_t *ptab, int32_t *page_base,
+                                                           Control *ctrl, int64_t num_pages,
+                                                           const int32_t *lengths_in,
+                                                           const float *z_in, int32_t limit,
+                                                           int units, int maxpages, int log2p) {
+  __shared__ int s_wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nthreads = blockDim.x;
+  const int nw = nthreads / 64;
+  const int per = (units + nthreads - 1) / nthreads;
+  const int i0 = min(tid * per, units), i1 = min(i0 + per, units);
+  const int P = 1 << log2p;
+  const long long base = static_cast<long long>(ctrl->pages_used);
+  int sum = 0, bad = 0;
+  for (int i = i0; i < i1; ++i) {
+    int l;
+    if (lengths_in) {
+      l = lengths_in[i];
+      if (l < 0 || l > limit) {
+        bad = 1;
+        l = 0;
+      }
+      len[i] = l;
+      z[i] = (l > 0) ? z_in[i] : 0.0f;
+    } else {
+      l = len[i];
+      z[i] = 0.0f;
+    }
+    sum += (l + P - 1) >> log2p;
+  }
+  if (bad) atomicOr(&ctrl->flags, FLAG_BAD_LENGTH);
+  int incl = sum;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) s_wsum[wave] = incl;
+  __syncthreads();
+  long long run = incl - sum, total = 0;
+  for (int w = 0; w < nw; ++w) {
+    if (w < wave) run += s_wsum[w];
+    total += s_wsum[w];
+  }
+  const bool fail = base + total > num_pages;
+  for (int i = i0; i < i1; ++i) {
+    const int l = len[i];
+    const int np = (l + P - 1) >> log2p;
+    if (fail) {
+      page_base[i] = -1;
+      len[i] = 0;
+    } else {
+      const int pb = static_cast<int>(base + run);
+      page_base[i] = pb;
+      for (int j = 0; j < np; ++j) ptab[int64_t(i) * maxpages + j] = pb + j;
+    }
+    run += np;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    if (fail)
+      atomicOr(&ctrl->flags, FLAG_POOL_EXHAUSTED);
+    else
+      ctrl->pages_used = static_cast<unsigned long long>(base + total);
+  }
+}
+
+// Pass 3, one wave per (unit, 64-token chunk): every segment whose first
+// token lies in the chunk is reduced by this wave -- the omega-weighted sums
+// of its keys (element 0 zeroed) and values divided by its omega sum, which
+// equals the running mean of Algorithm 1 -- reading past the chunk end when
+// the segment continues.  Each token is therefore read exactly once.
+template <int ES, int D>
+__global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams p) {
+  constexpr int E = D / 64;  // elements per lane
+  constexpr int RB = D * ES;
+  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ch = blockIdx.x * kWaves + wave;
+  const int tlo = ch * 64;
+  if (tlo >= p.n) return;
+  const int pb = p.page_base[u];
+  if (pb < 0) return;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int nb = prompt_len(p, b, false);
+  if (tlo >= nb) return;
+  const uint8_t *al = p.alpha + int64_t(u) * p.max_prompt;
+  const float *om = p.omega + int64_t(u) * p.max_prompt;
+  auto starts = [&](int wb) -> unsigned long long {
+    const int t = wb + lane;
+    return __ballot(t < nb && al[t] == 0);
+  };
+  const unsigned long long m0 = starts(tlo);
+  if (m0 == 0) return;
+  int before = 0;
+  for (int j = lane; j < ch; j += 64) before += p.count[int64_t(u) * p.prompt_chunks + j];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o, 64);
+
+  const int P = 1 << p.log2p;
+  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
+  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
+  const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
+  int s = before;
+  int t = tlo + __ffsll(static_cast<long long>(m0)) - 1;
+  while (true) {
+    // End of this segment: the next start after t, or the prompt end.
+    int wb = (t + 1) & ~63;
+    unsigned long long mk = (wb < nb) ? (starts(wb) & (~0ull << ((t + 1) - wb))) : 0ull;
+    while (mk == 0 && wb + 64 < nb) {
+      wb += 64;
+      mk = starts(wb);
+    }
+    const int te = mk ? wb + __ffsll(static_cast<long long>(mk)) - 1 : nb;
+
+    float ak[E], av[E], zs = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+    for (int t2 = t; t2 < te; t2 += 8) {
+      const int cnt = min(8, te - t2);
+      float kk[8][E], vv[8][E], ww[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int tj = t2 + min(j, cnt - 1);
+        load_e<ES, E>(kbase + tj * kst, kk[j]);
+        load_e<ES, E>(vbase + tj * vst, vv[j]);
+        ww[j] = om[tj];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < cnt) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const float kv = (lane * E + e == 0) ? 0.0f : kk[j][e];  // k_t[0] <- 0
+            ak[e] = fmaf(ww[j], kv, ak[e]);
+            av[e] = fmaf(ww[j], vv[j][e], av[e]);
+          }
+          zs += ww[j];
+        }
+      }
+      if (p.slot_index && lane < cnt) p.slot_index[int64_t(u) * p.n + t2 + lane] = s;
+    }
+    const float inv = 1.0f / zs;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      ak[e] = ak[e] * inv;
+      av[e] = av[e] * inv;
+    }
+    char *row = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB +
+                lane * E * ES;
+    store_e<ES, E>(row, ak);
+    store_e<ES, E>(row + int64_t(P) * RB, av);
+    if (te >= nb) {
+      if (lane == 0) p.z[u] = zs;
+      break;
+    }
+    if (te >= tlo + 64) break;  // the next segment starts in the next chunk
+    t = te;
+    ++s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dense <-> paged copies (import / export) and small utilities.
+// ---------------------------------------------------------------------------
+constexpr int kDenseRows = 16;
+
+template <int ES, int D>
+__global__ __launch_bounds__(kThreads) void import_kernel(DenseParams p) {
+  constexpr int RB = D * ES, CPR = RB / 16;
+  const int u = blockIdx.y;
+  const int pb = p.page_base[u];
+  if (pb < 0) return;
+  const int l = p.len[u];
+  const int P = 1 << p.log2p;
+  for (int idx = threadIdx.x; idx < kDenseRows * CPR; idx += kThreads) {
+    const int r = idx / CPR, c = idx - r * CPR;
+    const int s = blockIdx.x * kDenseRows + r;
+    if (s >= l) continue;
+    const int64_t src = (int64_t(u) * p.dense_slots + s) * RB + c * 16;
+    char *dst = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB + c * 16;
+    st16(dst, ld16(static_cast<const char *>(p.kd) + src));
+    st16(dst + int64_t(P) * RB, ld16(static_cast<const char *>(p.vd) + src));
+  }
+}
+
+template <int ES, int D>
+__global__ __launch_bounds__(kThreads) void export_kernel(DenseParams p) {
+  constexpr int RB = D * ES, CPR = RB / 16;
+  const int u = blockIdx.y;
+  const int l = p.len[u];
+  const int P = 1 << p.log2p;
+  if (blockIdx.x == 0 && threadIdx.x == 0) p.z_out[u] = p.z[u];
+  for (int idx = threadIdx.x; idx < kDenseRows * CPR; idx += kThreads) {
+    const int r = idx / CPR, c = idx - r * CPR;
+    const int s = blockIdx.x * kDenseRows + r;
+    if (s >= p.dense_slots) continue;
+    const int64_t dst = (int64_t(u) * p.dense_slots + s) * RB + c * 16;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (s < l) {
+      const int page = p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)];
+      const char *src = p.pool + int64_t(page) * p.page_bytes + int64_t(s & (P - 1)) * RB + c * 16;
+      kv = ld16(src);
+      vv = ld16(src + int64_t(P) * RB);
+    }
+    st16(static_cast<char *>(p.kd) + dst, kv);
+    st16(static_cast<char *>(p.vd) + dst, vv);
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t *p, int32_t v, size_t n) {
+  for (size_t i = blockIdx.x * size_t(blockDim.x) + threadIdx.x; i < n; i += size_t(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void zero_u8_kernel(uint8_t *p, size_t n) {
+  for (size_t i = blockIdx.x * size_t(blockDim.x) + threadIdx.x; i < n; i += size_t(gridDim.x) * blockDim.x)
+    p[i] = 0;
+}
+
+__global__ void copy_i32_kernel(int32_t *d, const int32_t *s, size_t n) {
+  for (size_t i = blockIdx.x * size_t(blockDim.x) + threadIdx.x; i < n; i += size_t(gridDim.x) * blockDim.x)
+    d[i] = s[i];
+}
+
+int grid_for(size_t n) {
+  const size_t g = (n + kThreads - 1) / kThreads;
+  return static_cast<int>(g < 4096 ? (g > 0 ? g : 1) : 4096);
+}
+
+template <int ES, int D, int G>
+hipError_t decode_impl(const DecodeParams &p, int grid, hipStream_t s) {
+  const size_t lds = decode_lds_bytes(p.units, G, D);
+  hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int batch = p.units / p.hkv;
+  const int blocks = (batch * p.hq + kWaves - 1) / kWaves;
+  hipLaunchKernelGGL((combine_kernel<ES, D, G>), dim3(blocks), dim3(kThreads), 0, s, p, batch);
+  return hipGetLastError();
+}
+
+template <int ES, int D>
+hipError_t decode_by_group(int group, const DecodeParams &p, int grid, hipStream_t s) {
+  switch (group) {
+    case 1: return decode_impl<ES, D, 1>(p, grid, s);
+    case 2: return decode_impl<ES, D, 2>(p, grid, s);
+    case 4: return decode_impl<ES, D, 4>(p, grid, s);
+    case 8: return decode_impl<ES, D, 8>(p, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int ES, int D>
+hipError_t prefill_impl(const PrefillParams &p, hipStream_t s) {
+  if (p.n > 0) {
+    hipLaunchKernelGGL((prefill_decide_kernel<ES>), dim3(p.units), dim3(kThreads), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(p.units)), dim3(kThreads), 0, s, p.len, 0,
+                       size_t(p.units));
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(alloc_pages_kernel, dim3(1), dim3(1024), 0, s, p.len, p.z, p.ptab,
+                     p.page_base, p.ctrl, p.num_pages, nullptr, nullptr, 0, p.units, p.maxpages,
+                     p.log2p);
+  e = hipGetLastError();
+  if (e != hipSuccess || p.n == 0) return e;
+  const int nch = (p.n + 63) / 64;
+  hipLaunchKernelGGL((prefill_reduce_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
+                     dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int ES, int D>
+hipError_t import_impl(const DenseParams &p, hipStream_t s) {
+  const int limit = p.dense_slots < p.max_slots ? p.dense_slots : p.max_slots;
+  hipLaunchKernelGGL(alloc_pages_kernel, dim3(1), dim3(1024), 0, s, p.len, p.z, p.ptab,
+                     p.page_base, p.ctrl, p.num_pages, p.lengths_in, p.z_in, limit, p.units,
+                     p.maxpages, p.log2p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.dense_slots == 0) return e;
+  hipLaunchKernelGGL((import_kernel<ES, D>),
+                     dim3((p.dense_slots + kDenseRows - 1) / kDenseRows, p.units), dim3(kThreads), 0,
+                     s, p);
+  return hipGetLastError();
+}
+
+template <int ES, int D>
+hipError_t export_impl(const DenseParams &p, hipStream_t s) {
+  const int bx = p.dense_slots > 0 ? (p.dense_slots + kDenseRows - 1) / kDenseRows : 1;
+  hipLaunchKernelGGL((export_kernel<ES, D>), dim3(bx, p.units), dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t decode_lds_bytes(int units, int group, int head_dim) {
+  return align_up(size_t(units + 1) * 4, 16) + size_t(kWaves) * group * (head_dim + 4) * 4 +
+         size_t(2) * head_dim * 4;
+}
+
+hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(count)), dim3(kThreads), 0, s, p, value, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_u8(void *p, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_u8_kernel, dim3(grid_for(bytes)), dim3(kThreads), 0, s,
+                     static_cast<uint8_t *>(p), bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, size_t count, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_i32_kernel, dim3(grid_for(count)), dim3(kThreads), 0, s, dst, src, count);
+  return hipGetLastError();
+}
+
+#define DMC_DISPATCH_ES_D(fn, es, d, ...)                           \
+  ((es) == 2 ? ((d) == 128 ? fn<2, 128>(__VA_ARGS__) : fn<2, 64>(__VA_ARGS__)) \
+             : ((d) == 128 ? fn<4, 128>(__VA_ARGS__) : fn<4, 64>(__VA_ARGS__)))
+
+hipError_t launch_decode(int elem_bytes, int head_dim, int group, const DecodeParams &p, int grid,
+                         hipStream_t s) {
+  return DMC_DISPATCH_ES_D(decode_by_group, elem_bytes, head_dim, group, p, grid, s);
+}
+
+hipError_t launch_prefill(int elem_bytes, int head_dim, const PrefillParams &p, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(prefill_impl, elem_bytes, head_dim, p, s);
+}
+
+hipError_t launch_import(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(import_impl, elem_bytes, head_dim, p, s);
+}
+
+hipError_t launch_export(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(export_impl, elem_bytes, head_dim, p, s);
+}
+
+}  // namespace dmc
