@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--split-tile", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="finish with plain 1 GiB device copies (counter calibration)")
     return ap.parse_args()
 
 
@@ -214,7 +216,7 @@ def main():
                    "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
                    "context": w.prompt_len, "page_size": P_SIZE,
                    "global_cr": round(float(w.prompt_len * lens0.size / lens0.sum()), 3),
-                   "split_tile": cache.cfg.split_tile or 256, "parallelism": "none (1 GPU)"},
+                   "split_tile": cache.cfg.split_tile, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "dmc_decode_step (decode_kernel + combine_kernel)",
@@ -231,6 +233,14 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, lens0[:, 0, :], args.cpu_seconds)
     print(json.dumps(res), flush=True)
+    if args.calib_copy:
+        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings give
+        # the scale factor between the counters and bytes moved.
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -79,7 +79,9 @@ typedef struct dmc_cache_config {
   int64_t num_pages;         /* pool capacity in pages, shared by all units, < 2^31 */
   float decision_bias;       /* c: alpha = round(sigmoid(k[0] - c)) = (k[0] > c); 0 = Algorithm 1 */
   int32_t omega_src;         /* dmc_omega_src */
-  int32_t split_tile;        /* slots per split-K attention tile; 0 = 256 */
+  int32_t split_tile;        /* cap on slots per split-K range; 0 = no cap: each wave of
+                                a decode launch gets an equal share of the layer's actual
+                                (compressed) slots */
   int32_t max_prompt_len;    /* largest n for dmc_prefill_compress; 0 = max_slots_per_seq */
 } dmc_cache_config;
 

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <new>
 #include <string>
@@ -55,7 +56,13 @@ int ilog2(int64_t x) {
 }
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-constexpr int kDefaultTile = 256;
+#ifndef DMC_DECODE_WG_PER_CU
+#define DMC_DECODE_WG_PER_CU 2
+#endif
+// Persistent decode grid: workgroups per compute unit (4 waves each), and
+// the largest number of waves a decode launch uses.
+constexpr int kDecodeWgPerCu = DMC_DECODE_WG_PER_CU;
+constexpr int64_t kMaxDecodeWaves = 8192;
 constexpr size_t kMaxDecodeLds = 64 * 1024;
 
 int elem_bytes(const dmc_cache_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
@@ -102,8 +109,15 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.units = c.batch * c.num_kv_heads;
   L.group = c.num_q_heads / c.num_kv_heads;
   L.maxpages = static_cast<int32_t>((int64_t(c.max_slots_per_seq) + c.page_size - 1) / c.page_size);
-  L.split_tile = c.split_tile > 0 ? c.split_tile : kDefaultTile;
-  L.tiles_per_unit = (c.max_slots_per_seq > 0 ? c.max_slots_per_seq - 1 : 0) / L.split_tile + 1;
+  L.split_tile = c.split_tile;
+  {
+    // ranges <= max(waves, ceil(S / split_tile)) with S <= U * max_slots; one
+    // record per (range, unit) piece is indexed range + unit.
+    const int64_t S = int64_t(L.units) * c.max_slots_per_seq;
+    int64_t ranges = kMaxDecodeWaves;
+    if (c.split_tile > 0) ranges = std::max<int64_t>(ranges, (S + c.split_tile - 1) / c.split_tile);
+    L.max_records = ranges + L.units + 1;
+  }
   L.max_prompt = c.max_prompt_len > 0 ? c.max_prompt_len : c.max_slots_per_seq;
   L.prompt_chunks = (L.max_prompt + 63) / 64;
   L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
@@ -120,7 +134,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.z = take(NL * U * 4);
   L.ctrl = take(sizeof(dmc::Control));
   L.meta = take(U * 2 * 4);
-  L.partials = take(U * size_t(L.tiles_per_unit) * L.group * (c.head_dim + 4) * 4);
+  L.partials = take(size_t(L.max_records) * L.group * (c.head_dim + 4) * 4);
   L.pf_alpha = take(U * size_t(L.max_prompt));
   L.pf_omega = take(U * size_t(L.max_prompt) * 4);
   L.pf_count = take(U * size_t(L.prompt_chunks) * 4);
@@ -275,9 +289,9 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   p.log2p = ilog2(c.page_size);
   p.split_tile = L.split_tile;
   p.omega_src = c.omega_src;
-  const int64_t tiles = int64_t(L.units) * L.tiles_per_unit;
-  const int64_t cap = int64_t(cache->cu_count) * 8;
-  const int grid = static_cast<int>(tiles < cap ? tiles : cap);
+  const int64_t grid64 = std::min<int64_t>(int64_t(cache->cu_count) * kDecodeWgPerCu,
+                                            kMaxDecodeWaves / 4);
+  const int grid = static_cast<int>(grid64);
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
   hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, p, grid,

@@ -33,8 +33,8 @@ struct Layout {
   int32_t units;          // B * Hkv per layer
   int32_t maxpages;       // page-table width per unit
   int32_t group;          // G
-  int32_t split_tile;     // T
-  int32_t tiles_per_unit; // upper bound of decode tiles per unit
+  int32_t split_tile;     // cap on positions per decode range (0 = none)
+  int64_t max_records;    // decode partial records: ranges + units
   int32_t max_prompt;     // prefill staging capacity (tokens)
   int32_t prompt_chunks;  // ceil(max_prompt / 64)
 };
@@ -53,7 +53,7 @@ struct DecodeParams {
   void *out;
   int32_t *slot_index;     // optional [U]
   float *partials;         // [tiles, G, d + 4]
-  int32_t *meta;           // [U, 2]: first tile, tile count
+  int32_t *meta;           // [U, 2]: first partial record, record count (for the combine)
   float c;                 // decision bias
   float scale_log2;        // log2(e) / sqrt(d)
   int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src;

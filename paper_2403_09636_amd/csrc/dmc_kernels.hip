@@ -14,12 +14,9 @@
 //   buffered: a decode step reads one parity and writes the other, so every
 //   workgroup sees the same pre-step lengths), z [L][U] fp32.
 //
-// Decode = one fused launch (update + split-K attention) plus a combine
-// launch for units split over several tiles.  Tiles come from the pre-step
-// lengths: unit u has nt = floor(max(l-1, 0) / T) + 1 tiles; tiles 0..nt-2
-// cover closed slots only, the last ("tail") tile covers the rest, owns the
-// open slot and performs the unit's Algorithm 1 update before attending to
-// it.  No other tile touches the open slot, so the fusion is race free.
+// Decode = one fused launch per layer (Algorithm 1 update + split-K
+// attention, balanced by actual compressed length) plus a small combine
+// launch for units split over several pieces.
 #include "dmc_internal.h"
 
 namespace dmc {
@@ -112,13 +109,40 @@ __device__ __forceinline__ float sigmoid_floor(float x) {
   return fmaxf(1.0f / (1.0f + expf(-x)), 0x1p-100f);
 }
 
+
+
+// ---------------------------------------------------------------------------
+// Fused decode: Algorithm 1 update + split-K attention + combine.
+//
+// Load balance by actual compressed length: the layer's units are laid end
+// to end in one "slot space" of S = sum_u max(l_u, 1) positions, cut into
+// equal ranges, one per wave (at most split_tile positions each, when set).
+// A range may cover the end of one unit and the start of the next; each
+// (range, unit) piece keeps an online-softmax state (max, sum, acc[d]) per
+// query head of the group.  The piece holding a unit's last position owns
+// the open slot and runs the unit's Algorithm 1 update before attending to
+// it; every other piece reads closed slots only, so the fusion is race free.
+// A unit covered by one piece writes its output directly; otherwise each
+// piece writes a partial record (index range + unit), combined by a second,
+// small launch.  No barrier and no atomic is taken after the slot space is
+// built (the page allocator's bump counter aside).
+// ---------------------------------------------------------------------------
+
+// Reduction over the LPR lanes of a row group (lanes are grouped in runs of
+// LPR); every lane of the group receives the sum.
 template <int LPR>
 __device__ __forceinline__ float row_sum(float x) {
-#pragma unroll
-  for (int o = 1; o < LPR; o <<= 1) x += __shfl_xor(x, o, 64);
+  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "row width");
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x141, 0xF, 0xF, false));  // row_half_mirror
+  if (LPR >= 16)
+    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x140, 0xF, 0xF, false));  // row_mirror
+  if (LPR >= 32) x += __shfl_xor(x, 16, 64);
   return x;
 }
 
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Merge (m2, l2, a2) into (m, l, a); scores are in the log2 domain.
 template <int N>
@@ -126,16 +150,21 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float *a, float 
                                             const float *a2) {
   const float mn = fmaxf(m, m2);
   if (mn == neg_inf()) return;
-  const float s1 = exp2f(m - mn), s2 = exp2f(m2 - mn);
+  const float s1 = fast_exp2(m - mn), s2 = fast_exp2(m2 - mn);
   l = l * s1 + l2 * s2;
 #pragma unroll
   for (int e = 0; e < N; ++e) a[e] = a[e] * s1 + a2[e] * s2;
   m = mn;
 }
 
-// ---------------------------------------------------------------------------
-// Fused decode: Algorithm 1 update + split-K attention partials.
-// ---------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming 16-byte load of cache data that is read once per step.
+__device__ __forceinline__ uint4 ld16_stream(const char *p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 template <int ES, int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   using V = V16<ES>;
@@ -148,29 +177,26 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
 
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_wsum[kWaves];
-  __shared__ int s_has_cur;
   const int U = p.units;
-  int *s_pre = reinterpret_cast<int *>(smem);
-  float *s_mrg = reinterpret_cast<float *>(smem + align_up(size_t(U + 1) * 4, 16));
-  float *s_cur = s_mrg + kWaves * G * REC;  // [2][D] key, value of the current slot
+  int *s_off = reinterpret_cast<int *>(smem);   // [U + 1] unit offsets in the slot space
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane / LPR, part = lane % LPR;
-  const int T = p.split_tile;
   const int P = 1 << p.log2p;
   const int CS = P < kChunk ? P : kChunk;
   const int log2cs = p.log2p < 5 ? p.log2p : 5;
 
-  // Exclusive prefix of per-unit tile counts over the pre-step lengths.
+  // Slot space of the layer: unit u owns positions [off_u, off_u + n_u) with
+  // n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
+  // unit's open slot (or, for an empty unit, the slot its first token opens).
   {
     const int per = (U + kThreads - 1) / kThreads;
     const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
     int sum = 0;
     for (int i = i0; i < i1; ++i) {
-      const int l = p.len_in[i];
-      const int nt = (l > 0 ? l - 1 : 0) / T + 1;
-      s_pre[i] = nt;
-      sum += nt;
+      const int n = max(p.len_in[i], 1);
+      s_off[i] = n;
+      sum += n;
     }
     int incl = sum;
 #pragma unroll
@@ -186,282 +212,264 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       total += s_wsum[w];
     }
     for (int i = i0; i < i1; ++i) {
-      const int nt = s_pre[i];
-      s_pre[i] = run;
-      run += nt;
+      const int n = s_off[i];
+      s_off[i] = run;
+      run += n;
     }
-    if (tid == 0) s_pre[U] = total;
+    if (tid == 0) s_off[U] = total;
     __syncthreads();
   }
-  const int NT = s_pre[U];
+  const int S = s_off[U];
+  const int nwaves = gridDim.x * kWaves;
+  int span = (S + nwaves - 1) / nwaves;          // equal share of actual slots per range
+  if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
+  const int nranges = (S + span - 1) / span;
 
-  for (int t = blockIdx.x; t < NT; t += gridDim.x) {
-    int lo = 0, hi = U - 1;
+  for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
+    int pos = r * span;
+    const int pos_end = min(pos + span, S);
+    int lo = 0, hi = U - 1;                       // unit holding position pos
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (s_pre[mid] <= t) lo = mid; else hi = mid - 1;
+      if (s_off[mid] <= pos) lo = mid; else hi = mid - 1;
     }
-    const int u = lo;
-    const int first = s_pre[u], nt = s_pre[u + 1] - first, ti = t - first;
-    const bool tail = ti == nt - 1;
-    const int l = p.len_in[u];
-    const int b = u / p.hkv, g = u - b * p.hkv;
-    const int start = ti * T;
-    int end = start + T;
-    int alpha = 0;
-    if (tail) {
-      const float k0 = load_elem<ES>(p.k, int64_t(u) * D);
-      alpha = (l > 0 && k0 > p.c) ? 1 : 0;
-      end = alpha ? l - 1 : l;
-    }
-
-    // This tile's query heads, element 0 zeroed, pre-scaled by log2(e)/sqrt(d).
-    float qf[G][VN];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const char *qp = static_cast<const char *>(p.q) +
-                       (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
-      V::unpack(ld16(qp), qf[h]);
-      if (part == 0) qf[h][0] = 0.0f;
-#pragma unroll
-      for (int e = 0; e < VN; ++e) qf[h][e] *= p.scale_log2;
-    }
-
-    // Tail tile: Algorithm 1 for unit u (wave 0; lanes of row group 0 store).
-    if (tail && wave == 0) {
-      float om;
-      if (p.omega_src == 0) {
-        om = sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D));
-      } else {
-        float s = 0.0f;
-        for (int h = 0; h < G; ++h)
-          s += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
-        om = fmaxf(s / G, 0x1p-100f);
-      }
-      float kf[VN], vf[VN];
-      V::unpack(ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES), kf);
-      V::unpack(ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES), vf);
-      if (part == 0) kf[0] = 0.0f;  // Algorithm 1: k_t[0] <- 0
+    for (int u = lo; pos < pos_end; ++u) {
+      const int off = s_off[u], n_u = s_off[u + 1] - off;
+      const int start = pos - off;
+      const int stop = min(pos_end, off + n_u) - off;   // this piece: [start, stop)
+      pos = off + stop;
+      const bool owner = stop == n_u;                   // holds the open slot
+      const int l = p.len_in[u];
+      const int b = u / p.hkv, g = u - b * p.hkv;
       const int64_t pt = int64_t(u) * p.maxpages;
-      int has_cur = 1, flag = 0, slot, page = -1;
-      float znew;
-      if (alpha) {
-        slot = l - 1;
-        page = p.ptab[pt + (slot >> p.log2p)];
-        const char *kr = p.pool + int64_t(page) * p.page_bytes +
-                         int64_t(slot & (P - 1)) * RB + part * 16;
-        float ok[VN], ov[VN];
-        V::unpack(ld16(kr), ok);
-        V::unpack(ld16(kr + int64_t(P) * RB), ov);
-        const float zold = p.z[u];
-        znew = zold + om;
+      int end = owner ? n_u - 1 : stop;                 // closed slots [start, end)
+
+      // The unit's query heads, element 0 zeroed, pre-scaled by log2(e)/sqrt(d).
+      float qf[G][VN];
 #pragma unroll
-        for (int e = 0; e < VN; ++e) {
-          kf[e] = (ok[e] * zold + kf[e] * om) / znew;
-          vf[e] = (ov[e] * zold + vf[e] * om) / znew;
+      for (int h = 0; h < G; ++h) {
+        const char *qp = static_cast<const char *>(p.q) +
+                         (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
+        V::unpack(ld16(qp), qf[h]);
+        if (part == 0) qf[h][0] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < VN; ++e) qf[h][e] *= p.scale_log2;
+      }
+
+      // Owner: Algorithm 1 for unit u.  ck/cv hold the current slot.
+      float ck[VN], cv[VN];
+      bool has_cur = false;
+      if (owner) {
+        const float k0 = load_elem<ES>(p.k, int64_t(u) * D);
+        const int alpha = (l > 0 && k0 > p.c) ? 1 : 0;
+        end = alpha ? l - 1 : l;
+        float om;
+        if (p.omega_src == 0) {
+          om = sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D));
+        } else {
+          float s = 0.0f;
+          for (int h = 0; h < G; ++h)
+            s += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
+          om = fmaxf(s / G, 0x1p-100f);
         }
-      } else {
-        slot = l;
-        znew = om;
-        if (l >= p.max_slots) {
-          has_cur = 0;
-          flag = FLAG_SLOTS_EXHAUSTED;
-        } else if ((l & (P - 1)) == 0) {
-          int pg = 0;
-          if (lane == 0) {
-            const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
-            pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
-          }
-          pg = __shfl(pg, 0, 64);
-          if (pg < 0) {
-            has_cur = 0;
-            flag = FLAG_POOL_EXHAUSTED;
-          } else {
-            page = pg;
-            if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
+        V::unpack(ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES), ck);
+        V::unpack(ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES), cv);
+        if (part == 0) ck[0] = 0.0f;  // Algorithm 1: k_t[0] <- 0
+        int flag = 0, slot, page = -1;
+        float znew;
+        has_cur = true;
+        if (alpha) {
+          slot = l - 1;
+          page = p.ptab[pt + (slot >> p.log2p)];
+          const char *kr = p.pool + int64_t(page) * p.page_bytes +
+                           int64_t(slot & (P - 1)) * RB + part * 16;
+          float ok[VN], ov[VN];
+          V::unpack(ld16(kr), ok);
+          V::unpack(ld16(kr + int64_t(P) * RB), ov);
+          const float zold = p.z[u];
+          znew = zold + om;
+#pragma unroll
+          for (int e = 0; e < VN; ++e) {
+            ck[e] = (ok[e] * zold + ck[e] * om) / znew;
+            cv[e] = (ov[e] * zold + cv[e] * om) / znew;
           }
         } else {
-          page = p.ptab[pt + (l >> p.log2p)];
+          slot = l;
+          znew = om;
+          if (l >= p.max_slots) {
+            has_cur = false;
+            flag = FLAG_SLOTS_EXHAUSTED;
+          } else if ((l & (P - 1)) == 0) {
+            int pg = 0;
+            if (lane == 0) {
+              const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
+              pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
+            }
+            pg = __shfl(pg, 0, 64);
+            if (pg < 0) {
+              has_cur = false;
+              flag = FLAG_POOL_EXHAUSTED;
+            } else {
+              page = pg;
+              if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
+            }
+          } else {
+            page = p.ptab[pt + (l >> p.log2p)];
+          }
+        }
+        if (has_cur) {
+          const uint4 kp = V::pack(ck), vp = V::pack(cv);   // ck, cv become the stored values
+          if (grp == 0) {
+            char *kr = p.pool + int64_t(page) * p.page_bytes + int64_t(slot & (P - 1)) * RB + part * 16;
+            st16(kr, kp);
+            st16(kr + int64_t(P) * RB, vp);
+          }
+        }
+        if (lane == 0) {
+          if (has_cur) p.z[u] = znew;
+          p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
+          if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
+          if (flag) atomicOr(&p.ctrl->flags, flag);
+          const int r0 = off / span;                  // range holding the unit's first slot
+          p.meta[2 * u] = r0 + u;                     // its first partial record
+          p.meta[2 * u + 1] = r - r0 + 1;             // number of pieces
+        }
+      }
+
+      // Attention over the closed slots [start, end) of this piece.
+      float m[G], ls[G], acc[G][VN];
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        m[h] = neg_inf();
+        ls[h] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < VN; ++e) acc[h][e] = 0.0f;
+      }
+      if (end > start) {
+        const int c0 = start >> log2cs, c1 = (end - 1) >> log2cs;
+        for (int ch = c0; ch <= c1; ++ch) {
+          const int row0 = ch << log2cs;
+          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + CS) - row0;
+          const int page = p.ptab[pt + (row0 >> p.log2p)];
+          const char *kb = p.pool + int64_t(page) * p.page_bytes + int64_t(row0 & (P - 1)) * RB +
+                           part * 16;
+          const char *vb = kb + int64_t(P) * RB;
+          uint4 kr[NI], vr[NI];
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            const int rr = min(max(i * RPI + grp, rlo), rhi - 1);
+            kr[i] = ld16_stream(kb + rr * RB);
+          }
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            const int rr = min(max(i * RPI + grp, rlo), rhi - 1);
+            vr[i] = ld16_stream(vb + rr * RB);
+          }
+          float s[G][NI];
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            float kf[VN];
+            V::unpack(kr[i], kf);
+            const int rr = i * RPI + grp;
+            const bool valid = rr >= rlo && rr < rhi;
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+              float d = 0.0f;
+#pragma unroll
+              for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], kf[e], d);
+              d = row_sum<LPR>(d);
+              s[h][i] = valid ? d : neg_inf();
+            }
+          }
+          float mn[G];
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            float mc = s[h][0];
+#pragma unroll
+            for (int i = 1; i < NI; ++i) mc = fmaxf(mc, s[h][i]);
+            mn[h] = fmaxf(m[h], mc);
+            if (mn[h] != neg_inf()) {
+              const float sc = fast_exp2(m[h] - mn[h]);
+              ls[h] *= sc;
+#pragma unroll
+              for (int e = 0; e < VN; ++e) acc[h][e] *= sc;
+#pragma unroll
+              for (int i = 0; i < NI; ++i) {
+                s[h][i] = fast_exp2(s[h][i] - mn[h]);
+                ls[h] += s[h][i];
+              }
+              m[h] = mn[h];
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            float vf[VN];
+            V::unpack(vr[i], vf);
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+              if (mn[h] == neg_inf()) continue;
+#pragma unroll
+              for (int e = 0; e < VN; ++e) acc[h][e] = fmaf(s[h][i], vf[e], acc[h][e]);
+            }
+          }
+        }
+      }
+
+      // Merge the RPI row groups of the wave; add the current slot.
+#pragma unroll
+      for (int o = LPR; o < 64; o <<= 1) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          float a2[VN];
+#pragma unroll
+          for (int e = 0; e < VN; ++e) a2[e] = __shfl_xor(acc[h][e], o, 64);
+          const float m2 = __shfl_xor(m[h], o, 64), l2 = __shfl_xor(ls[h], o, 64);
+          merge_state<VN>(m[h], ls[h], acc[h], m2, l2, a2);
         }
       }
       if (has_cur) {
-        const uint4 kp = V::pack(kf), vp = V::pack(vf);
-        if (grp == 0) {
-          char *kr = p.pool + int64_t(page) * p.page_bytes + int64_t(slot & (P - 1)) * RB + part * 16;
-          st16(kr, kp);
-          st16(kr + int64_t(P) * RB, vp);
-#pragma unroll
-          for (int e = 0; e < VN; ++e) {
-            s_cur[part * VN + e] = kf[e];
-            s_cur[D + part * VN + e] = vf[e];
-          }
-        }
-      }
-      if (lane == 0) {
-        if (has_cur) p.z[u] = znew;
-        p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
-        if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
-        p.meta[2 * u] = first;
-        p.meta[2 * u + 1] = nt;
-        if (flag) atomicOr(&p.ctrl->flags, flag);
-        s_has_cur = has_cur;
-      }
-    }
-
-    // Split-K attention over the closed slots [start, end) of this tile.
-    float m[G], ls[G], acc[G][VN];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      m[h] = neg_inf();
-      ls[h] = 0.0f;
-#pragma unroll
-      for (int e = 0; e < VN; ++e) acc[h][e] = 0.0f;
-    }
-    if (end > start) {
-      const int c0 = start >> log2cs, c1 = (end - 1) >> log2cs;
-      const int64_t pt = int64_t(u) * p.maxpages;
-      for (int ch = c0 + wave; ch <= c1; ch += kWaves) {
-        const int row0 = ch << log2cs;
-        const int rlo = max(start, row0) - row0, rhi = min(end, row0 + CS) - row0;
-        const int page = p.ptab[pt + (row0 >> p.log2p)];
-        const char *kb = p.pool + int64_t(page) * p.page_bytes + int64_t(row0 & (P - 1)) * RB +
-                         part * 16;
-        const char *vb = kb + int64_t(P) * RB;
-        uint4 kr[NI], vr[NI];
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const int r = min(max(i * RPI + grp, rlo), rhi - 1);
-          kr[i] = ld16(kb + r * RB);
-        }
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const int r = min(max(i * RPI + grp, rlo), rhi - 1);
-          vr[i] = ld16(vb + r * RB);
-        }
-        float s[G][NI];
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          float kf[VN];
-          V::unpack(kr[i], kf);
-          const int r = i * RPI + grp;
-          const bool valid = r >= rlo && r < rhi;
-#pragma unroll
-          for (int h = 0; h < G; ++h) {
-            float d = 0.0f;
-#pragma unroll
-            for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], kf[e], d);
-            d = row_sum<LPR>(d);
-            s[h][i] = valid ? d : neg_inf();
-          }
-        }
-        float mn[G];
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          float mc = s[h][0];
-#pragma unroll
-          for (int i = 1; i < NI; ++i) mc = fmaxf(mc, s[h][i]);
-          mn[h] = fmaxf(m[h], mc);
-          if (mn[h] != neg_inf()) {
-            const float sc = exp2f(m[h] - mn[h]);
-            ls[h] *= sc;
-#pragma unroll
-            for (int e = 0; e < VN; ++e) acc[h][e] *= sc;
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-              s[h][i] = exp2f(s[h][i] - mn[h]);
-              ls[h] += s[h][i];
-            }
-            m[h] = mn[h];
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          float vf[VN];
-          V::unpack(vr[i], vf);
-#pragma unroll
-          for (int h = 0; h < G; ++h) {
-            if (mn[h] == neg_inf()) continue;
-#pragma unroll
-            for (int e = 0; e < VN; ++e) acc[h][e] = fmaf(s[h][i], vf[e], acc[h][e]);
-          }
-        }
-      }
-    }
-
-    // Merge the RPI row groups of the wave, then the waves of the workgroup.
-#pragma unroll
-    for (int o = LPR; o < 64; o <<= 1) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float a2[VN];
-#pragma unroll
-        for (int e = 0; e < VN; ++e) a2[e] = __shfl_xor(acc[h][e], o, 64);
-        const float m2 = __shfl_xor(m[h], o, 64), l2 = __shfl_xor(ls[h], o, 64);
-        merge_state<VN>(m[h], ls[h], acc[h], m2, l2, a2);
-      }
-    }
-    if (grp == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float *rec = s_mrg + (wave * G + h) * REC;
-        if (part == 0) {
-          rec[0] = m[h];
-          rec[1] = ls[h];
-        }
-#pragma unroll
-        for (int e = 0; e < VN; ++e) rec[4 + part * VN + e] = acc[h][e];
-      }
-    }
-    __syncthreads();
-    if (wave == 0) {
-      const bool cur = tail && s_has_cur;
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float M = neg_inf(), L = 0.0f, A[VN];
-#pragma unroll
-        for (int e = 0; e < VN; ++e) A[e] = 0.0f;
-        for (int w = 0; w < kWaves; ++w) {
-          const float *rec = s_mrg + (w * G + h) * REC;
-          float a2[VN];
-#pragma unroll
-          for (int e = 0; e < VN; ++e) a2[e] = rec[4 + part * VN + e];
-          merge_state<VN>(M, L, A, rec[0], rec[1], a2);
-        }
-        if (cur) {  // the slot Algorithm 1 just merged or appended
           float d = 0.0f;
 #pragma unroll
-          for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], s_cur[part * VN + e], d);
+          for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ck[e], d);
           d = row_sum<LPR>(d);
-          float a2[VN];
-#pragma unroll
-          for (int e = 0; e < VN; ++e) a2[e] = s_cur[D + part * VN + e];
-          merge_state<VN>(M, L, A, d, 1.0f, a2);
+          merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, cv);
         }
-        if (grp == 0) {
-          if (nt == 1) {
-            const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+      }
+
+      if (grp == 0) {
+        if (start == 0 && owner) {     // the whole unit in one piece: final output
 #pragma unroll
-            for (int e = 0; e < VN; ++e) A[e] *= inv;
+          for (int h = 0; h < G; ++h) {
+            const float inv = ls[h] > 0.0f ? 1.0f / ls[h] : 0.0f;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) acc[h][e] *= inv;
             char *op = static_cast<char *>(p.out) +
                        (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
-            st16(op, V::pack(A));
-          } else {
-            float *rec = p.partials + (int64_t(t) * G + h) * REC;
+            st16(op, V::pack(acc[h]));
+          }
+        } else {                       // partial record r + u for the combine launch
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            float *rec = p.partials + (int64_t(r + u) * G + h) * REC;
             if (part == 0) {
-              rec[0] = M;
-              rec[1] = L;
+              rec[0] = m[h];
+              rec[1] = ls[h];
             }
 #pragma unroll
-            for (int e = 0; e < VN; ++e) rec[4 + part * VN + e] = A[e];
+            for (int e = 0; e < VN; ++e) rec[4 + part * VN + e] = acc[h][e];
           }
         }
       }
     }
-    __syncthreads();
   }
 }
 
-// Combine the split-K partials of units with more than one tile.
+// Combine the split-K partial records of units with more than one tile:
+// o = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i.  One wave per
+// (b, query head); lane i fetches record i's max and sum, then every lane
+// accumulates its E dims over the records.
 template <int ES, int D, int G>
 __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int batch) {
   constexpr int REC = D + 4;
@@ -472,20 +480,52 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int b
   const int b = bh / p.hq, h = bh - b * p.hq;
   const int g = h / G, hg = h - g * G;
   const int u = b * p.hkv + g;
-  const int first = p.meta[2 * u], nt = p.meta[2 * u + 1];
+  const int first = p.meta[2 * u], nt = p.meta[2 * u + 1];   // records first .. first+nt-1
   if (nt <= 1) return;
-  float M = neg_inf();
-  for (int i = 0; i < nt; ++i) M = fmaxf(M, p.partials[(int64_t(first + i) * G + hg) * REC]);
   float L = 0.0f, A[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) A[e] = 0.0f;
-  if (M != neg_inf()) {
-    for (int i = 0; i < nt; ++i) {
-      const float *rec = p.partials + (int64_t(first + i) * G + hg) * REC;
-      const float w = exp2f(rec[0] - M);
-      L = fmaf(w, rec[1], L);
+  float M = neg_inf();
+  for (int i0 = 0; i0 < nt; i0 += 64) {           // running max over chunks of 64 records
+    const int i = i0 + lane;
+    const float mi = i < nt ? p.partials[(int64_t(first + i) * G + hg) * REC] : neg_inf();
+    float mc = mi;
 #pragma unroll
-      for (int e = 0; e < E; ++e) A[e] = fmaf(w, rec[4 + lane * E + e], A[e]);
+    for (int o = 32; o > 0; o >>= 1) mc = fmaxf(mc, __shfl_xor(mc, o, 64));
+    const float mn = fmaxf(M, mc);
+    if (mn == neg_inf()) continue;
+    const float sc = fast_exp2(M - mn);
+    L *= sc;
+#pragma unroll
+    for (int e = 0; e < E; ++e) A[e] *= sc;
+    M = mn;
+    const float wi = i < nt ? fast_exp2(mi - M) : 0.0f;
+    const float li = i < nt ? p.partials[(int64_t(first + i) * G + hg) * REC + 1] : 0.0f;
+    float lw = wi * li;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) lw += __shfl_xor(lw, o, 64);
+    L += lw;
+    const int cnt = min(64, nt - i0);
+    int j = 0;
+    for (; j + 4 <= cnt; j += 4) {
+      float w4[4], a4[4][E];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        w4[q] = __shfl(wi, j + q, 64);
+        const float *rec = p.partials + (int64_t(first + i0 + j + q) * G + hg) * REC + 4 + lane * E;
+#pragma unroll
+        for (int e = 0; e < E; ++e) a4[q][e] = rec[e];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < E; ++e) A[e] = fmaf(w4[q], a4[q][e], A[e]);
+    }
+    for (; j < cnt; ++j) {
+      const float w = __shfl(wi, j, 64);
+      const float *rec = p.partials + (int64_t(first + i0 + j) * G + hg) * REC + 4 + lane * E;
+#pragma unroll
+      for (int e = 0; e < E; ++e) A[e] = fmaf(w, rec[e], A[e]);
     }
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
@@ -493,6 +533,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int b
   for (int e = 0; e < E; ++e) A[e] *= inv;
   store_e<ES, E>(static_cast<char *>(p.out) + (int64_t(bh) * D + lane * E) * ES, A);
 }
+
 
 // ---------------------------------------------------------------------------
 // Prefill compactor.
@@ -852,8 +893,9 @@ hipError_t export_impl(const DenseParams &p, hipStream_t s) {
 }  // namespace
 
 size_t decode_lds_bytes(int units, int group, int head_dim) {
-  return align_up(size_t(units + 1) * 4, 16) + size_t(kWaves) * group * (head_dim + 4) * 4 +
-         size_t(2) * head_dim * 4;
+  (void)group;
+  (void)head_dim;
+  return align_up(size_t(units + 1) * 4, 16);
 }
 
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s) {
