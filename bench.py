@@ -16,7 +16,6 @@ from __future__ import annotations
 
 import argparse
 import json
-import math
 import os
 import sys
 import time
@@ -56,6 +55,25 @@ def algorithmic_bytes(lens_before, lens_after, w, page):
     la = lens_after.astype(np.int64)
     per = 2 * d * s * lb + 2 * d * s + (2 * G + 2) * d * s + 16 + 4 * ((la + page - 1) // page)
     return int(per.sum())
+
+
+def profiled_traffic(workload):
+    """Calibrated HBM bytes per launch from the committed rocprofv3 counter
+    summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload}_counters.txt")
+    src = os.path.join(ROOT, "paper_2403_09636_amd", "csrc", "dmc_kernels.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha:
+        return None
+    return int(kv["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(w, lens_layers, seconds):
@@ -122,15 +140,8 @@ def main():
     t_setup = time.time()
 
     # ---- cache and its contents --------------------------------------------
-    if w.cache_kind == "precompressed":
-        lens_lh = W.precompressed_lengths(w)                      # [L, Hkv]
-    else:
-        lens_lh = None
     max_slots = w.prompt_len + total_steps
-    if lens_lh is not None:
-        pages = int(w.batch * np.ceil((lens_lh + total_steps) / P_SIZE).sum())
-    else:
-        pages = int(w.num_layers * w.batch * w.num_kv_heads * math.ceil(max_slots / P_SIZE))
+    pages = W.pool_pages(w, total_steps)
     cfg = P.make_config(w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim,
                         w.dtype, P_SIZE, max_slots, pages, 0.0, "lead", args.split_tile,
                         w.prompt_len if w.cache_kind == "prefill" else 0)
@@ -218,7 +229,8 @@ def main():
                    "global_cr": round(float(w.prompt_len * lens0.size / lens0.sum()), 3),
                    "split_tile": cache.cfg.split_tile, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": profiled_traffic(w.name),
                      "kernel": "dmc_decode_step (decode_kernel + combine_kernel)",
                      "alg_bytes_per_launch": int(alg_per_launch),
                      "avg_launch_us": round(avg_launch_ms * 1e3, 2)},

@@ -190,14 +190,25 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   // n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
   // unit's open slot (or, for an empty unit, the slot its first token opens).
   {
+    constexpr int kBatch = 8;     // coalesced loads in flight per thread
+    for (int i0 = 0; i0 < U; i0 += kThreads * kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int i = i0 + j * kThreads + tid;
+        v[j] = i < U ? p.len_in[i] : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int i = i0 + j * kThreads + tid;
+        if (i < U) s_off[i] = max(v[j], 1);
+      }
+    }
+    __syncthreads();
     const int per = (U + kThreads - 1) / kThreads;
     const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
     int sum = 0;
-    for (int i = i0; i < i1; ++i) {
-      const int n = max(p.len_in[i], 1);
-      s_off[i] = n;
-      sum += n;
-    }
+    for (int i = i0; i < i1; ++i) sum += s_off[i];
     int incl = sum;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -256,83 +267,26 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int e = 0; e < VN; ++e) qf[h][e] *= p.scale_log2;
       }
 
-      // Owner: Algorithm 1 for unit u.  ck/cv hold the current slot.
-      float ck[VN], cv[VN];
-      bool has_cur = false;
+      // Owner of the unit's last position: start the loads Algorithm 1 needs
+      // (new key/value, decision and importance neurons, z, the open slot) so
+      // they are in flight while the closed slots stream; the update itself
+      // runs after the loop.  The loop covers [start, n_u - 1) only; the open
+      // slot is attended to after the update, as merged or as it was.
+      uint4 k_raw = make_uint4(0, 0, 0, 0), v_raw = k_raw, ok_raw = k_raw, ov_raw = k_raw;
+      float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
+      int open_page = -1;
       if (owner) {
-        const float k0 = load_elem<ES>(p.k, int64_t(u) * D);
-        const int alpha = (l > 0 && k0 > p.c) ? 1 : 0;
-        end = alpha ? l - 1 : l;
-        float om;
-        if (p.omega_src == 0) {
-          om = sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D));
-        } else {
-          float s = 0.0f;
-          for (int h = 0; h < G; ++h)
-            s += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
-          om = fmaxf(s / G, 0x1p-100f);
-        }
-        V::unpack(ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES), ck);
-        V::unpack(ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES), cv);
-        if (part == 0) ck[0] = 0.0f;  // Algorithm 1: k_t[0] <- 0
-        int flag = 0, slot, page = -1;
-        float znew;
-        has_cur = true;
-        if (alpha) {
-          slot = l - 1;
-          page = p.ptab[pt + (slot >> p.log2p)];
-          const char *kr = p.pool + int64_t(page) * p.page_bytes +
-                           int64_t(slot & (P - 1)) * RB + part * 16;
-          float ok[VN], ov[VN];
-          V::unpack(ld16(kr), ok);
-          V::unpack(ld16(kr + int64_t(P) * RB), ov);
-          const float zold = p.z[u];
-          znew = zold + om;
-#pragma unroll
-          for (int e = 0; e < VN; ++e) {
-            ck[e] = (ok[e] * zold + ck[e] * om) / znew;
-            cv[e] = (ov[e] * zold + cv[e] * om) / znew;
-          }
-        } else {
-          slot = l;
-          znew = om;
-          if (l >= p.max_slots) {
-            has_cur = false;
-            flag = FLAG_SLOTS_EXHAUSTED;
-          } else if ((l & (P - 1)) == 0) {
-            int pg = 0;
-            if (lane == 0) {
-              const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
-              pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
-            }
-            pg = __shfl(pg, 0, 64);
-            if (pg < 0) {
-              has_cur = false;
-              flag = FLAG_POOL_EXHAUSTED;
-            } else {
-              page = pg;
-              if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
-            }
-          } else {
-            page = p.ptab[pt + (l >> p.log2p)];
-          }
-        }
-        if (has_cur) {
-          const uint4 kp = V::pack(ck), vp = V::pack(cv);   // ck, cv become the stored values
-          if (grp == 0) {
-            char *kr = p.pool + int64_t(page) * p.page_bytes + int64_t(slot & (P - 1)) * RB + part * 16;
-            st16(kr, kp);
-            st16(kr + int64_t(P) * RB, vp);
-          }
-        }
-        if (lane == 0) {
-          if (has_cur) p.z[u] = znew;
-          p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
-          if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
-          if (flag) atomicOr(&p.ctrl->flags, flag);
-          const int r0 = off / span;                  // range holding the unit's first slot
-          p.meta[2 * u] = r0 + u;                     // its first partial record
-          p.meta[2 * u + 1] = r - r0 + 1;             // number of pieces
+        k0 = load_elem<ES>(p.k, int64_t(u) * D);
+        q0 = load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D);
+        k_raw = ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES);
+        v_raw = ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES);
+        if (l > 0) {
+          zold = p.z[u];
+          open_page = p.ptab[pt + ((l - 1) >> p.log2p)];
+          const char *kr = p.pool + int64_t(open_page) * p.page_bytes +
+                           int64_t((l - 1) & (P - 1)) * RB + part * 16;
+          ok_raw = ld16(kr);
+          ov_raw = ld16(kr + int64_t(P) * RB);
         }
       }
 
@@ -346,15 +300,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int e = 0; e < VN; ++e) acc[h][e] = 0.0f;
       }
       if (end > start) {
+        // Chunks of <= CS rows inside one page; the next chunk's loads are in
+        // flight while the current one is consumed (two register buffers).
         const int c0 = start >> log2cs, c1 = (end - 1) >> log2cs;
-        for (int ch = c0; ch <= c1; ++ch) {
+        auto issue = [&](int ch, uint4 *kr, uint4 *vr) {
           const int row0 = ch << log2cs;
           const int rlo = max(start, row0) - row0, rhi = min(end, row0 + CS) - row0;
           const int page = p.ptab[pt + (row0 >> p.log2p)];
           const char *kb = p.pool + int64_t(page) * p.page_bytes + int64_t(row0 & (P - 1)) * RB +
                            part * 16;
           const char *vb = kb + int64_t(P) * RB;
-          uint4 kr[NI], vr[NI];
 #pragma unroll
           for (int i = 0; i < NI; ++i) {
             const int rr = min(max(i * RPI + grp, rlo), rhi - 1);
@@ -365,6 +320,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
             const int rr = min(max(i * RPI + grp, rlo), rhi - 1);
             vr[i] = ld16_stream(vb + rr * RB);
           }
+        };
+        auto consume = [&](int ch, const uint4 *kr, const uint4 *vr) {
+          const int row0 = ch << log2cs;
+          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + CS) - row0;
           float s[G][NI];
 #pragma unroll
           for (int i = 0; i < NI; ++i) {
@@ -412,10 +371,19 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
               for (int e = 0; e < VN; ++e) acc[h][e] = fmaf(s[h][i], vf[e], acc[h][e]);
             }
           }
+        };
+        uint4 ka[NI], va[NI], kb2[NI], vb2[NI];
+        issue(c0, ka, va);
+        for (int ch = c0; ch <= c1; ch += 2) {
+          if (ch + 1 <= c1) issue(ch + 1, kb2, vb2);
+          consume(ch, ka, va);
+          if (ch + 1 > c1) break;
+          if (ch + 2 <= c1) issue(ch + 2, ka, va);
+          consume(ch + 1, kb2, vb2);
         }
       }
 
-      // Merge the RPI row groups of the wave; add the current slot.
+      // Merge the RPI row groups of the wave.
 #pragma unroll
       for (int o = LPR; o < 64; o <<= 1) {
 #pragma unroll
@@ -427,14 +395,98 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
           merge_state<VN>(m[h], ls[h], acc[h], m2, l2, a2);
         }
       }
-      if (has_cur) {
+
+      if (owner) {
+        // Algorithm 1 for unit u: alpha from k[0] (the first token of an empty
+        // unit appends), omega from q[0]; k[0] <- 0; merge or append.
+        const int alpha = (l > 0 && k0 > p.c) ? 1 : 0;
+        float om;
+        if (p.omega_src == 0) {
+          om = sigmoid_floor(q0);
+        } else {
+          float sum = 0.0f;
+          for (int h = 0; h < G; ++h)
+            sum += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
+          om = fmaxf(sum / G, 0x1p-100f);
+        }
+        float ck[VN], cv[VN];
+        V::unpack(k_raw, ck);
+        V::unpack(v_raw, cv);
+        if (part == 0) ck[0] = 0.0f;
+        int flag = 0, slot, page = open_page;
+        bool has_cur = true;
+        float znew;
+        if (alpha) {
+          float ok[VN], ov[VN];
+          V::unpack(ok_raw, ok);
+          V::unpack(ov_raw, ov);
+          slot = l - 1;
+          znew = zold + om;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-          float d = 0.0f;
+          for (int e = 0; e < VN; ++e) {
+            ck[e] = (ok[e] * zold + ck[e] * om) / znew;
+            cv[e] = (ov[e] * zold + cv[e] * om) / znew;
+          }
+        } else {
+          if (l > 0) {   // the old open slot stays as it is: attend to it
+            float ok[VN], ov[VN];
+            V::unpack(ok_raw, ok);
+            V::unpack(ov_raw, ov);
 #pragma unroll
-          for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ck[e], d);
-          d = row_sum<LPR>(d);
-          merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, cv);
+            for (int h = 0; h < G; ++h) {
+              float d = 0.0f;
+#pragma unroll
+              for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ok[e], d);
+              d = row_sum<LPR>(d);
+              merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, ov);
+            }
+          }
+          slot = l;
+          znew = om;
+          if (l >= p.max_slots) {
+            has_cur = false;
+            flag = FLAG_SLOTS_EXHAUSTED;
+          } else if ((l & (P - 1)) == 0) {
+            int pg = 0;
+            if (lane == 0) {
+              const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
+              pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
+            }
+            pg = __shfl(pg, 0, 64);
+            if (pg < 0) {
+              has_cur = false;
+              flag = FLAG_POOL_EXHAUSTED;
+            } else {
+              page = pg;
+              if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
+            }
+          }
+          // otherwise slot l shares the open slot's page
+        }
+        if (has_cur) {
+          const uint4 kp = V::pack(ck), vp = V::pack(cv);   // ck, cv become the stored values
+          if (grp == 0) {
+            char *kr = p.pool + int64_t(page) * p.page_bytes + int64_t(slot & (P - 1)) * RB + part * 16;
+            st16(kr, kp);
+            st16(kr + int64_t(P) * RB, vp);
+          }
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            float d = 0.0f;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ck[e], d);
+            d = row_sum<LPR>(d);
+            merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, cv);
+          }
+        }
+        if (lane == 0) {
+          if (has_cur) p.z[u] = znew;
+          p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
+          if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
+          if (flag) atomicOr(&p.ctrl->flags, flag);
+          const int r0 = off / span;                  // range holding the unit's first slot
+          p.meta[2 * u] = r0 + u;                     // its first partial record
+          p.meta[2 * u + 1] = r - r0 + 1;             // number of pieces
         }
       }
 

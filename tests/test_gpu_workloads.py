@@ -1,0 +1,206 @@
+"""GPU parity at the full sizes of the benchmark workloads, in the launch
+configuration the benchmark times (default split, default grid).
+
+* one Llama-2-7B layer (batch 16, 4096-token prompt compressed in-kernel,
+  128 decode steps): every slot index, length, slot, z and output;
+* the Llama-2-7B stack, the Llama-2-13B skewed shape and the Llama-2-70B GQA
+  shape: slot indices and lengths of EVERY unit (bit-exact, against the
+  oracle's decision rule) and full content and output parity on a seeded
+  sample of >= 64 (layer, batch, kv-head) units followed by the oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from tests.gpu_helpers import assert_close, f64, log
+from workloads import (WORKLOADS, decode_inputs_torch, pool_pages, precompressed_torch,
+                       prompt_torch, sample_units)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2403_09636_amd  # noqa: F401
+    return torch
+
+
+def _cache_for(w, steps, pages):
+    import paper_2403_09636_amd as P
+    cfg = P.make_config(w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                        w.page_size, w.prompt_len + steps, pages, 0.0, "lead", 0,
+                        w.prompt_len if w.cache_kind == "prefill" else 0)
+    return P.DMCCache(cfg, device="cuda")
+
+
+@pytest.mark.timeout(600)
+def test_llama7b_layer_full(torch_cuda):
+    """Prefill 4096 tokens for 16 x 32 units at CR in {1, 2, 4, 8}, then 128
+    decode steps; everything compared with the oracle."""
+    torch = torch_cuda
+    w = WORKLOADS["llama7b_layer"]
+    log(f"case llama7b_layer: {w.notes}")
+    steps = w.decode_steps
+    cache = _cache_for(w, steps, pool_pages(w, steps))
+    k, v, q0 = prompt_torch(w, 0, "cuda")
+    slot = torch.empty((w.batch, w.num_kv_heads, w.prompt_len), dtype=torch.int32, device="cuda")
+    cache.prefill(0, k, v, q0, slot_index=slot)
+    orc = oracle.DMCOracle(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim,
+                           w.prompt_len + steps)
+    ref_slot = orc.prefill(0, f64(k), f64(v), f64(q0))
+    del k, v, q0
+    assert (slot.cpu().numpy() == ref_slot).all(), "prefill slot indices"
+    log(f"prefill ok: {int(orc.layers[0].l.sum())} slots")
+    _compare_layer(cache, orc, 0, w.dtype)
+    worst = 0.0
+    for s in range(steps):
+        q, kk, vv = decode_inputs_torch(w, s, 0, "cuda")
+        si = torch.empty((w.batch, w.num_kv_heads), dtype=torch.int32, device="cuda")
+        out = cache.decode_step(0, q, kk, vv, slot_index=si)
+        ref, ref_si = orc.decode_step(0, f64(q), f64(kk), f64(vv))
+        assert (si.cpu().numpy() == ref_si).all(), f"step {s} slot indices"
+        worst = max(worst, assert_close(f64(out), ref, w.dtype, f"step {s} output"))
+        if s % 32 == 31:
+            log(f"decode step {s + 1}/{steps}, max abs err {worst:.3e}")
+    _compare_layer(cache, orc, 0, w.dtype)
+    cache.check()
+
+
+def _compare_layer(cache, orc, layer, dtype):
+    K_ref, V_ref, l_ref, z_ref = orc.export(layer)
+    lens = cache.lengths(layer).cpu().numpy()
+    assert (lens == l_ref).all(), "lengths"
+    dense = int(l_ref.max())
+    K, V, z = cache.export(layer, dense_slots=dense)
+    mask = np.arange(dense)[None, None, :] < l_ref[:, :, None]
+    assert_close(f64(K)[mask], K_ref[:, :, :dense][mask], dtype, "keys")
+    assert_close(f64(V)[mask], V_ref[:, :, :dense][mask], dtype, "values")
+    assert np.allclose(f64(z), z_ref, rtol=1e-4, atol=1e-4), "z"
+
+
+class Sampled:
+    """Oracle units following a sample of (layer, b, g) of a big workload."""
+
+    def __init__(self, w, steps, count=64):
+        self.w = w
+        self.units = sample_units(w, count)
+        self.by_layer = {}
+        for (l, b, g) in self.units:
+            self.by_layer.setdefault(l, []).append((b, g))
+        self.orc = {}
+        self.cap = w.prompt_len + steps
+
+    def _new(self):
+        w = self.w
+        return oracle.DMCOracle(1, 1, w.group, 1, w.head_dim, self.cap)
+
+    def load(self, layer, K, V, lens, z):
+        for (b, g) in self.by_layer.get(layer, []):
+            o = self._new()
+            n = int(lens[b, g])
+            o.load(0, f64(K[b, g, :n])[None, None], f64(V[b, g, :n])[None, None],
+                   np.array([[n]]), np.array([[float(z[b, g])]]))
+            self.orc[(layer, b, g)] = o
+
+    def prefill(self, layer, k, v, q0):
+        G = self.w.group
+        for (b, g) in self.by_layer.get(layer, []):
+            o = self._new()
+            o.prefill(0, f64(k[b, :, g])[None, :, None], f64(v[b, :, g])[None, :, None],
+                      f64(q0[b, :, g * G:(g + 1) * G])[None])
+            self.orc[(layer, b, g)] = o
+
+    def step(self, layer, q, k, v, out):
+        G = self.w.group
+        worst = 0.0
+        for (b, g) in self.by_layer.get(layer, []):
+            o = self.orc[(layer, b, g)]
+            ref, ref_slot = o.decode_step(0, f64(q[b, g * G:(g + 1) * G])[None],
+                                          f64(k[b, g])[None, None], f64(v[b, g])[None, None])
+            worst = max(worst, assert_close(f64(out[b, g * G:(g + 1) * G]), ref[0], self.w.dtype,
+                                            f"unit {(layer, b, g)} output"))
+        return worst
+
+    def compare_cache(self, cache, layer):
+        units = self.by_layer.get(layer, [])
+        if not units:
+            return
+        lens = cache.lengths(layer).cpu().numpy()
+        dense = int(max(lens[b, g] for b, g in units))
+        K, V, z = cache.export(layer, dense_slots=dense)
+        for (b, g) in units:
+            Kr, Vr, lr, zr = self.orc[(layer, b, g)].export(0)
+            n = int(lr[0, 0])
+            assert lens[b, g] == n
+            assert_close(f64(K[b, g, :n]), Kr[0, 0, :n], self.w.dtype, f"unit {(layer, b, g)} keys")
+            assert_close(f64(V[b, g, :n]), Vr[0, 0, :n], self.w.dtype, f"unit {(layer, b, g)} values")
+            assert abs(float(z[b, g]) - zr[0, 0]) <= 1e-4 * max(1.0, abs(zr[0, 0])), "z"
+
+
+def _run_big(torch, w, steps):
+    """Set the whole cache up, run `steps` decode steps over every layer and
+    check every unit's slot index and the sampled units' outputs."""
+    smp = Sampled(w, steps)
+    cache = _cache_for(w, steps, pool_pages(w, steps))
+    for layer in range(w.num_layers):
+        if w.cache_kind == "precompressed":
+            K, V, lt, zt = precompressed_torch(w, layer, "cuda")
+            cache.import_(layer, K, V, lt, zt)
+            smp.load(layer, K, V, lt.cpu().numpy(), zt.cpu().numpy())
+            del K, V
+        else:
+            k, v, q0 = prompt_torch(w, layer, "cuda")
+            cache.prefill(layer, k, v, q0)
+            smp.prefill(layer, k, v, q0)
+            del k, v, q0
+        if layer % 16 == 15:
+            log(f"cache layer {layer + 1}/{w.num_layers} ready")
+    cache.check()
+    lens = [cache.lengths(layer).cpu().numpy() for layer in range(w.num_layers)]
+    for (l, b, g) in smp.units:
+        assert lens[l][b, g] == smp.orc[(l, b, g)].layers[0].l[0], f"prefill length {(l, b, g)}"
+    worst = 0.0
+    for s in range(steps):
+        for layer in range(w.num_layers):
+            q, k, v = decode_inputs_torch(w, s, layer, "cuda")
+            si = torch.empty((w.batch, w.num_kv_heads), dtype=torch.int32, device="cuda")
+            out = cache.decode_step(layer, q, k, v, slot_index=si)
+            # every unit: slot index from the oracle's decision rule
+            lp = lens[layer]
+            alpha = oracle.decision(f64(k[:, :, 0]), 0.0) * (lp > 0)
+            want = np.where(alpha == 1, lp - 1, lp)
+            assert (si.cpu().numpy() == want).all(), f"step {s} layer {layer} slot indices"
+            lens[layer] = lp + (1 - alpha)
+            worst = max(worst, smp.step(layer, q, k, v, out))
+        log(f"step {s + 1}/{steps} over {w.num_layers} layers, sampled max abs err {worst:.3e}")
+    for layer in range(w.num_layers):
+        assert (cache.lengths(layer).cpu().numpy() == lens[layer]).all(), f"lengths layer {layer}"
+        smp.compare_cache(cache, layer)
+    cache.check()
+    return smp
+
+
+@pytest.mark.timeout(600)
+def test_llama7b_stack_sampled(torch_cuda):
+    w = WORKLOADS["llama7b_stack"]
+    log(f"case llama7b_stack: {w.notes}")
+    smp = _run_big(torch_cuda, w, steps=3)
+    assert len(smp.units) >= 64
+
+
+@pytest.mark.timeout(900)
+def test_llama13b_skew_sampled(torch_cuda):
+    w = WORKLOADS["llama13b_skew"]
+    log(f"case llama13b_skew: {w.notes}")
+    smp = _run_big(torch_cuda, w, steps=2)
+    assert len(smp.units) >= 64
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_gqa_sampled(torch_cuda):
+    w = WORKLOADS["llama70b_gqa"]
+    log(f"case llama70b_gqa: {w.notes}")
+    smp = _run_big(torch_cuda, w, steps=2)
+    assert len(smp.units) >= 64

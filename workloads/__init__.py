@@ -2,4 +2,4 @@
 from .synthetic import (WORKLOADS, Workload, scaled, head_crs, effective_crs,  # noqa: F401
                         precompressed_lengths, decision_logits, decode_inputs_np,
                         prompt_np, decode_inputs_torch, prompt_torch,
-                        precompressed_torch, sample_units, seed_for)
+                        precompressed_torch, sample_units, seed_for, pool_pages)

@@ -175,6 +175,23 @@ def precompressed_lengths(w: Workload) -> np.ndarray:
     return lens
 
 
+def pool_pages(w: Workload, steps: int) -> int:
+    """Pages a cache for this workload needs after `steps` decode steps.
+
+    Pre-compressed caches: exact.  Prefilled caches: the expected slot count
+    1 + (n - 1) / CR of every (layer, kv head) plus six standard deviations of
+    the binomial append count, capped at n, plus one slot per decode step.
+    """
+    n, P = w.prompt_len, w.page_size
+    if w.cache_kind == "precompressed":
+        return int(w.batch * np.ceil((precompressed_lengths(w) + steps) / P).sum())
+    cr = head_crs(w)
+    pa = 1.0 / cr
+    expect = 1 + (n - 1) * pa + 6.0 * np.sqrt(n * pa * (1 - pa))
+    slots = np.minimum(np.ceil(expect), n) + steps
+    return int(w.batch * np.ceil(slots / P).sum())
+
+
 def effective_crs(w: Workload) -> np.ndarray:
     """[L, Hkv] CR that drives decode-step decisions."""
     if w.cache_kind == "precompressed":
@@ -280,6 +297,15 @@ def decode_inputs_torch(w: Workload, step: int, layer: int, device, bias: float 
     return q.to(dt), k.to(dt), v.to(dt)
 
 
+def _randn_rows(shape, g, device, dt):
+    """N(0, 1) of dtype dt, generated one leading row at a time (bounded fp32 temporaries)."""
+    import torch
+    out = torch.empty(shape, dtype=dt, device=device)
+    for i in range(shape[0]):
+        out[i] = torch.randn(shape[1:], generator=g, device=device)
+    return out
+
+
 def prompt_torch(w: Workload, layer: int, device, bias: float = 0.0, n: int | None = None):
     """Device twin of prompt_np: k, v [B, n, Hkv, d], q0 [B, n, Hq]."""
     import torch
@@ -287,8 +313,8 @@ def prompt_torch(w: Workload, layer: int, device, bias: float = 0.0, n: int | No
     n = w.prompt_len if n is None else n
     B, Hq, Hkv, d = w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim
     dt = _torch_dtype(w)
-    k = torch.randn((B, n, Hkv, d), generator=g, device=device).to(dt)
-    v = torch.randn((B, n, Hkv, d), generator=g, device=device).to(dt)
+    k = _randn_rows((B, n, Hkv, d), g, device, dt)
+    v = _randn_rows((B, n, Hkv, d), g, device, dt)
     q0 = torch.randn((B, n, Hq), generator=g, device=device).to(dt)
     u = torch.rand((B, n, Hkv), generator=g, device=device)
     k[..., 0] = _torch_logits(u, effective_crs(w)[layer][None, None, :], bias).to(dt)
@@ -308,8 +334,8 @@ def precompressed_torch(w: Workload, layer: int, device):
     lmax = int(lens_np.max())
     g = _gen(w, PROMPT_STREAM, layer, device)
     dt = _torch_dtype(w)
-    K = torch.randn((B, Hkv, lmax, d), generator=g, device=device).to(dt)
-    V = torch.randn((B, Hkv, lmax, d), generator=g, device=device).to(dt)
+    K = _randn_rows((B, Hkv, lmax, d), g, device, dt)
+    V = _randn_rows((B, Hkv, lmax, d), g, device, dt)
     K[..., 0] = 0
     lengths = torch.as_tensor(lens_np, dtype=torch.int32, device=device).repeat(B, 1)
     crs = w.prompt_len / lens_np.astype(np.float64)
