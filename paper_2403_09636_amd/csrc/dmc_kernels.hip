@@ -88,19 +88,31 @@ __device__ __forceinline__ uint4 ld16(const char *p) { return *reinterpret_cast<
 __device__ __forceinline__ void st16(char *p, const uint4 &v) { *reinterpret_cast<uint4 *>(p) = v; }
 
 // E consecutive elements (E = 1 or 2) <-> floats, for the prefill/combine paths.
+// (One memory access each; p is aligned to E * ES bytes.)
 template <int ES, int E>
 __device__ __forceinline__ void load_e(const char *p, float *f) {
-#pragma unroll
-  for (int e = 0; e < E; ++e) f[e] = load_elem<ES>(p, e);
+  if constexpr (ES == 2 && E == 2) {
+    const uint32_t w = *reinterpret_cast<const uint32_t *>(p);
+    f[0] = __uint_as_float(w << 16);
+    f[1] = __uint_as_float(w & 0xffff0000u);
+  } else if constexpr (ES == 4 && E == 2) {
+    const float2 w = *reinterpret_cast<const float2 *>(p);
+    f[0] = w.x;
+    f[1] = w.y;
+  } else {
+    f[0] = load_elem<ES>(p, 0);
+  }
 }
 template <int ES, int E>
 __device__ __forceinline__ void store_e(char *p, const float *f) {
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    if (ES == 2)
-      reinterpret_cast<uint16_t *>(p)[e] = static_cast<uint16_t>(bf16_bits(f[e]));
-    else
-      reinterpret_cast<float *>(p)[e] = f[e];
+  if constexpr (ES == 2 && E == 2) {
+    *reinterpret_cast<uint32_t *>(p) = bf16_bits(f[0]) | (bf16_bits(f[1]) << 16);
+  } else if constexpr (ES == 4 && E == 2) {
+    *reinterpret_cast<float2 *>(p) = make_float2(f[0], f[1]);
+  } else if constexpr (ES == 2) {
+    *reinterpret_cast<uint16_t *>(p) = static_cast<uint16_t>(bf16_bits(f[0]));
+  } else {
+    *reinterpret_cast<float *>(p) = f[0];
   }
 }
 
@@ -610,32 +622,49 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
   const int b = u / p.hkv, g = u - b * p.hkv, G = p.hq / p.hkv;
   const int nb = prompt_len(p, b, tid == 0);
   int total = 0;
-  for (int t0 = 0; t0 < p.n; t0 += kThreads) {
-    const int t = t0 + tid;
-    int start = 0;
-    if (t < p.n) {
-      const bool valid = t < nb;
-      const float k0 = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + g * p.ks[2]);
-      const int a = (t > 0 && k0 > p.c) ? 1 : 0;
-      float om;
-      if (p.omega_src == 0) {
-        om = sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G) * p.qs[2]));
-      } else {
-        float s = 0.0f;
-        for (int h = 0; h < G; ++h)
-          s += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G + h) * p.qs[2]));
-        om = fmaxf(s / G, 0x1p-100f);
+  constexpr int kBatch = 8;   // token rows whose decision neurons are in flight per thread
+  for (int t00 = 0; t00 < p.n; t00 += kThreads * kBatch) {
+    float k0[kBatch], q0[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int t = t00 + j * kThreads + tid;
+      k0[j] = 0.0f;
+      q0[j] = 0.0f;
+      if (t < p.n) {
+        k0[j] = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + g * p.ks[2]);
+        if (p.omega_src == 0)
+          q0[j] = load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G) * p.qs[2]);
       }
-      p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
-      p.omega[int64_t(u) * p.max_prompt + t] = om;
-      if (p.slot_index && !valid) p.slot_index[int64_t(u) * p.n + t] = -1;
-      start = (valid && !a) ? 1 : 0;
     }
-    const unsigned long long mask = __ballot(start);
-    const int chunk = (t0 >> 6) + wave;
-    if (lane == 0 && chunk * 64 < p.n) {
-      p.count[int64_t(u) * p.prompt_chunks + chunk] = __popcll(mask);
-      total += __popcll(mask);
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int t0 = t00 + j * kThreads;
+      if (t0 >= p.n) break;
+      const int t = t0 + tid;
+      int start = 0;
+      if (t < p.n) {
+        const bool valid = t < nb;
+        const int a = (t > 0 && k0[j] > p.c) ? 1 : 0;
+        float om;
+        if (p.omega_src == 0) {
+          om = sigmoid_floor(q0[j]);
+        } else {
+          float sum = 0.0f;
+          for (int h = 0; h < G; ++h)
+            sum += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G + h) * p.qs[2]));
+          om = fmaxf(sum / G, 0x1p-100f);
+        }
+        p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
+        p.omega[int64_t(u) * p.max_prompt + t] = om;
+        if (p.slot_index && !valid) p.slot_index[int64_t(u) * p.n + t] = -1;
+        start = (valid && !a) ? 1 : 0;
+      }
+      const unsigned long long mask = __ballot(start);
+      const int chunk = (t0 >> 6) + wave;
+      if (lane == 0 && chunk * 64 < p.n) {
+        p.count[int64_t(u) * p.prompt_chunks + chunk] = __popcll(mask);
+        total += __popcll(mask);
+      }
     }
   }
   if (lane == 0) s_tot[wave] = total;
@@ -649,6 +678,7 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
 
 // Pass 2 (also used by import), one workgroup: pages for every unit by an
 // exclusive scan of ceil(l / P), contiguous per unit, from the bump pointer.
+// The kernels that write the slots fill the page table.
 __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *z,
                                                            int32_t *ptab, int32_t *page_base,
                                                            Control *ctrl, int64_t num_pages,
@@ -700,9 +730,7 @@ __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *
       page_base[i] = -1;
       len[i] = 0;
     } else {
-      const int pb = static_cast<int>(base + run);
-      page_base[i] = pb;
-      for (int j = 0; j < np; ++j) ptab[int64_t(i) * maxpages + j] = pb + j;
+      page_base[i] = static_cast<int>(base + run);   // the slot writers fill the page table
     }
     run += np;
   }
@@ -718,12 +746,16 @@ __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *
 // Pass 3, one wave per (unit, 64-token chunk): every segment whose first
 // token lies in the chunk is reduced by this wave -- the omega-weighted sums
 // of its keys (element 0 zeroed) and values divided by its omega sum, which
-// equals the running mean of Algorithm 1 -- reading past the chunk end when
-// the segment continues.  Each token is therefore read exactly once.
+// equals the running mean of Algorithm 1 -- reading past the chunk end while
+// the last segment continues.  Each token is read exactly once.  Tokens are
+// streamed in fixed batches whatever the segment lengths; a segment is
+// flushed (slot written) when the next one starts.  The wave that writes
+// the first slot of a page also writes its page-table entry.
 template <int ES, int D>
 __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams p) {
   constexpr int E = D / 64;  // elements per lane
   constexpr int RB = D * ES;
+  constexpr int kRows = 8;   // token rows in flight per wave
   const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ch = blockIdx.x * kWaves + wave;
   const int tlo = ch * 64;
@@ -746,67 +778,76 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o, 64);
 
+  // Tokens [t0, t_stop): from the chunk's first segment start to the next
+  // start at or after the chunk end (or the prompt end).
+  const int t0 = tlo + __ffsll(static_cast<long long>(m0)) - 1;
+  int t_stop = nb;
+  for (int wb = tlo + 64; wb < nb; wb += 64) {
+    const unsigned long long mk = starts(wb);
+    if (mk) {
+      t_stop = wb + __ffsll(static_cast<long long>(mk)) - 1;
+      break;
+    }
+  }
+
   const int P = 1 << p.log2p;
   const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
   const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
   const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
   int s = before;
-  int t = tlo + __ffsll(static_cast<long long>(m0)) - 1;
-  while (true) {
-    // End of this segment: the next start after t, or the prompt end.
-    int wb = (t + 1) & ~63;
-    unsigned long long mk = (wb < nb) ? (starts(wb) & (~0ull << ((t + 1) - wb))) : 0ull;
-    while (mk == 0 && wb + 64 < nb) {
-      wb += 64;
-      mk = starts(wb);
-    }
-    const int te = mk ? wb + __ffsll(static_cast<long long>(mk)) - 1 : nb;
-
-    float ak[E], av[E], zs = 0.0f;
+  float ak[E], av[E], zs = 0.0f;
 #pragma unroll
-    for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
-    for (int t2 = t; t2 < te; t2 += 8) {
-      const int cnt = min(8, te - t2);
-      float kk[8][E], vv[8][E], ww[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int tj = t2 + min(j, cnt - 1);
-        load_e<ES, E>(kbase + tj * kst, kk[j]);
-        load_e<ES, E>(vbase + tj * vst, vv[j]);
-        ww[j] = om[tj];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (j < cnt) {
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const float kv = (lane * E + e == 0) ? 0.0f : kk[j][e];  // k_t[0] <- 0
-            ak[e] = fmaf(ww[j], kv, ak[e]);
-            av[e] = fmaf(ww[j], vv[j][e], av[e]);
-          }
-          zs += ww[j];
-        }
-      }
-      if (p.slot_index && lane < cnt) p.slot_index[int64_t(u) * p.n + t2 + lane] = s;
-    }
+  for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+  auto flush = [&]() {   // write slot s = sums / zs
     const float inv = 1.0f / zs;
+    float kq[E], vq[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      ak[e] = ak[e] * inv;
-      av[e] = av[e] * inv;
+      kq[e] = ak[e] * inv;
+      vq[e] = av[e] * inv;
     }
     char *row = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB +
                 lane * E * ES;
-    store_e<ES, E>(row, ak);
-    store_e<ES, E>(row + int64_t(P) * RB, av);
-    if (te >= nb) {
-      if (lane == 0) p.z[u] = zs;
-      break;
+    store_e<ES, E>(row, kq);
+    store_e<ES, E>(row + int64_t(P) * RB, vq);
+    if (lane == 0 && (s & (P - 1)) == 0)
+      p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)] = pb + (s >> p.log2p);
+  };
+  for (int t2 = t0; t2 < t_stop; t2 += kRows) {
+    const int cnt = min(kRows, t_stop - t2);
+    float kk[kRows][E], vv[kRows][E], ww[kRows];
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      const int tj = t2 + min(j, cnt - 1);
+      load_e<ES, E>(kbase + tj * kst, kk[j]);
+      load_e<ES, E>(vbase + tj * vst, vv[j]);
+      ww[j] = om[tj];
     }
-    if (te >= tlo + 64) break;  // the next segment starts in the next chunk
-    t = te;
-    ++s;
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      if (j < cnt) {
+        const int tj = t2 + j;
+        const int rel = tj - tlo;
+        if (tj != t0 && rel < 64 && ((m0 >> rel) & 1ull)) {   // a new segment opens
+          flush();
+          ++s;
+          zs = 0.0f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float kv = (lane * E + e == 0) ? 0.0f : kk[j][e];  // k_t[0] <- 0
+          ak[e] = fmaf(ww[j], kv, ak[e]);
+          av[e] = fmaf(ww[j], vv[j][e], av[e]);
+        }
+        zs += ww[j];
+        if (p.slot_index && lane == 0) p.slot_index[int64_t(u) * p.n + tj] = s;
+      }
+    }
   }
+  flush();
+  if (t_stop >= nb && lane == 0) p.z[u] = zs;   // the unit's last segment
 }
 
 // ---------------------------------------------------------------------------
@@ -828,6 +869,7 @@ __global__ __launch_bounds__(kThreads) void import_kernel(DenseParams p) {
     if (s >= l) continue;
     const int64_t src = (int64_t(u) * p.dense_slots + s) * RB + c * 16;
     char *dst = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB + c * 16;
+    if (c == 0 && (s & (P - 1)) == 0) p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)] = pb + (s >> p.log2p);
     st16(dst, ld16(static_cast<const char *>(p.kd) + src));
     st16(dst + int64_t(P) * RB, ld16(static_cast<const char *>(p.vd) + src));
   }
