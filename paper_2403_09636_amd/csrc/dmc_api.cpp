@@ -121,6 +121,8 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.max_prompt = c.max_prompt_len > 0 ? c.max_prompt_len : c.max_slots_per_seq;
   L.prompt_chunks = (L.max_prompt + 63) / 64;
   L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
+  // Grouped-query caches decode on matrix cores with value pages transposed.
+  L.v_trans = c.dtype == DMC_BF16 && L.group >= 4 && c.page_size == 32;
   const size_t U = size_t(L.units), NL = size_t(c.num_layers);
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -294,7 +296,7 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   const int grid = static_cast<int>(grid64);
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, p, grid,
+  hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, L.v_trans, p, grid,
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   cache->parity[layer] = static_cast<uint8_t>(par ^ 1);
@@ -360,7 +362,8 @@ dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
   p.prompt_chunks = L.prompt_chunks;
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, p, static_cast<hipStream_t>(stream));
+  hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, L.v_trans, p,
+                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return DMC_OK;
 }
@@ -412,7 +415,7 @@ dmc_status dmc_cache_export(const dmc_cache *cache, int32_t layer, void *k_dense
   p.z_out = z;
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_export(elem_bytes(cache->cfg), cache->cfg.head_dim, p,
+  hipError_t e = dmc::launch_export(elem_bytes(cache->cfg), cache->cfg.head_dim, cache->lay.v_trans, p,
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "export launch");
   return DMC_OK;
@@ -435,7 +438,7 @@ dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense
   p.z_in = z;
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_import(elem_bytes(cache->cfg), cache->cfg.head_dim, p,
+  hipError_t e = dmc::launch_import(elem_bytes(cache->cfg), cache->cfg.head_dim, cache->lay.v_trans, p,
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "import launch");
   return DMC_OK;

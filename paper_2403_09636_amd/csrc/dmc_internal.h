@@ -21,8 +21,10 @@ enum : int32_t {
 // Control block at the start of the control section.
 struct Control {
   unsigned long long pages_used;  // bump allocator of the page pool
+  long long alloc_base;           // first page of the last prefill / import allocation
+  long long alloc_count;          // pages in it (0 after a failed allocation)
   int32_t flags;
-  int32_t pad[13];
+  int32_t pad[9];
 };
 
 // Byte offsets of the workspace sections (all 256-byte aligned).
@@ -37,6 +39,7 @@ struct Layout {
   int64_t max_records;    // decode partial records: ranges + units
   int32_t max_prompt;     // prefill staging capacity (tokens)
   int32_t prompt_chunks;  // ceil(max_prompt / 64)
+  bool v_trans;           // value pages stored transposed (matrix-core decode)
 };
 
 // Everything the decode kernel needs for one layer.
@@ -99,11 +102,14 @@ struct DenseParams {
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s);
 hipError_t launch_fill_u8(void *p, size_t bytes, hipStream_t s);
 hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, size_t count, hipStream_t s);
-hipError_t launch_decode(int elem_bytes, int head_dim, int group, const DecodeParams &p,
+// vt: value pages stored transposed ([d][32] per page; bf16, G >= 4, P == 32),
+// decoded on matrix cores.
+hipError_t launch_decode(int elem_bytes, int head_dim, int group, bool vt, const DecodeParams &p,
                          int grid, hipStream_t s);
-hipError_t launch_prefill(int elem_bytes, int head_dim, const PrefillParams &p, hipStream_t s);
-hipError_t launch_import(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s);
-hipError_t launch_export(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s);
+hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillParams &p,
+                          hipStream_t s);
+hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
+hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 
 // Dynamic LDS bytes of the decode kernel for a unit count / group / head dim.
 size_t decode_lds_bytes(int units, int group, int head_dim);

@@ -177,6 +177,65 @@ __device__ __forceinline__ uint4 ld16_stream(const char *p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Slot space of a layer: unit u owns positions [off_u, off_u + n_u) with
+// n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
+// unit's open slot (or, for an empty unit, the slot its first token opens).
+// Every workgroup builds the exclusive prefix s_off[0..U] in LDS and gets S.
+__device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_off, int *s_wsum) {
+  const int U = p.units;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kBatch = 8;     // coalesced loads in flight per thread
+  for (int i0 = 0; i0 < U; i0 += kThreads * kBatch) {
+    int v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = i0 + j * kThreads + tid;
+      v[j] = i < U ? p.len_in[i] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = i0 + j * kThreads + tid;
+      if (i < U) s_off[i] = max(v[j], 1);
+    }
+  }
+  __syncthreads();
+  const int per = (U + kThreads - 1) / kThreads;
+  const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
+  int sum = 0;
+  for (int i = i0; i < i1; ++i) sum += s_off[i];
+  int incl = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) s_wsum[wave] = incl;
+  __syncthreads();
+  int run = incl - sum, total = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    if (w < wave) run += s_wsum[w];
+    total += s_wsum[w];
+  }
+  for (int i = i0; i < i1; ++i) {
+    const int n = s_off[i];
+    s_off[i] = run;
+    run += n;
+  }
+  if (tid == 0) s_off[U] = total;
+  __syncthreads();
+  return s_off[U];
+}
+
+// Unit holding slot-space position pos (s_off[u] <= pos < s_off[u + 1]).
+__device__ __forceinline__ int unit_at(const int *s_off, int U, int pos) {
+  int lo = 0, hi = U - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s_off[mid] <= pos) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
 template <int ES, int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   using V = V16<ES>;
@@ -198,51 +257,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int CS = P < kChunk ? P : kChunk;
   const int log2cs = p.log2p < 5 ? p.log2p : 5;
 
-  // Slot space of the layer: unit u owns positions [off_u, off_u + n_u) with
-  // n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
-  // unit's open slot (or, for an empty unit, the slot its first token opens).
-  {
-    constexpr int kBatch = 8;     // coalesced loads in flight per thread
-    for (int i0 = 0; i0 < U; i0 += kThreads * kBatch) {
-      int v[kBatch];
-#pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const int i = i0 + j * kThreads + tid;
-        v[j] = i < U ? p.len_in[i] : 0;
-      }
-#pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const int i = i0 + j * kThreads + tid;
-        if (i < U) s_off[i] = max(v[j], 1);
-      }
-    }
-    __syncthreads();
-    const int per = (U + kThreads - 1) / kThreads;
-    const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
-    int sum = 0;
-    for (int i = i0; i < i1; ++i) sum += s_off[i];
-    int incl = sum;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += t;
-    }
-    if (lane == 63) s_wsum[wave] = incl;
-    __syncthreads();
-    int run = incl - sum, total = 0;
-    for (int w = 0; w < kWaves; ++w) {
-      if (w < wave) run += s_wsum[w];
-      total += s_wsum[w];
-    }
-    for (int i = i0; i < i1; ++i) {
-      const int n = s_off[i];
-      s_off[i] = run;
-      run += n;
-    }
-    if (tid == 0) s_off[U] = total;
-    __syncthreads();
-  }
-  const int S = s_off[U];
+  const int S = build_slot_space(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
   int span = (S + nwaves - 1) / nwaves;          // equal share of actual slots per range
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
@@ -251,12 +266,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
     int pos = r * span;
     const int pos_end = min(pos + span, S);
-    int lo = 0, hi = U - 1;                       // unit holding position pos
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_off[mid] <= pos) lo = mid; else hi = mid - 1;
-    }
-    for (int u = lo; pos < pos_end; ++u) {
+    for (int u = unit_at(s_off, U, pos); pos < pos_end; ++u) {
       const int off = s_off[u], n_u = s_off[u + 1] - off;
       const int start = pos - off;
       const int stop = min(pos_end, off + n_u) - off;   // this piece: [start, stop)
@@ -530,6 +540,330 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Grouped-query decode on matrix cores (bf16, G >= 4, pages of 32 slots).
+//
+// Same slot-space split, owner rule and partial records as decode_kernel;
+// only the per-chunk arithmetic differs.  With G query heads per kv head the
+// chunk work is G dot products and G weighted sums per cached row, too much
+// for the vector ALUs at HBM speed, so both products run on
+// v_mfma_f32_16x16x32_bf16 (query heads padded to 16):
+//   scores  S^T[row][head] = K[row][:] . Q[head][:]   (A = K, B = Q^T)
+//   values  O^T[dim][head] += V^T[dim][row] P^T[row][head]   (A = V^T, B = P^T)
+// Key rows are assigned to the two 16-row score tiles interleaved (tile t,
+// tile row m -> chunk row 8(m/4) + 4t + m%4) so that each lane ends up with
+// the 8 consecutive rows 8q..8q+7 of one head -- exactly its slice of the
+// P^T operand of the value product.  Value pages of such caches are stored
+// transposed (V^T: d rows of page_size slots) so that slice of V^T is one
+// 16-byte load.  P enters the value product rounded to bf16; its row sum is
+// taken over the same rounded values.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4_t mfma_16x16x32(const uint4 &a, const uint4 &b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+  return bf16_bits(lo) | (bf16_bits(hi) << 16);
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
+  constexpr int KS = D / 32;      // k-steps of the score product
+  constexpr int NT = D / 16;      // 16-dim tiles of the value product
+  constexpr int RB = D * 2;       // bytes per key row
+  constexpr int REC = D + 4;      // partial record: m, l, -, -, acc[D]
+  static_assert(G >= 4 && G <= 16, "query group");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_wsum[kWaves];
+  const int U = p.units;
+  int *s_off = reinterpret_cast<int *>(smem);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, q = lane >> 4;      // MFMA column (head or dim) and k-group
+  const int P = 1 << p.log2p;
+  const int krow = 8 * (n >> 2) + (n & 3);     // this lane's key row in score tile 0 (+4 in tile 1)
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+
+  const int S = build_slot_space(p, s_off, s_wsum);
+  const int nwaves = gridDim.x * kWaves;
+  int span = (S + nwaves - 1) / nwaves;
+  if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
+  const int nranges = (S + span - 1) / span;
+
+  for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
+    int pos = r * span;
+    const int pos_end = min(pos + span, S);
+    for (int u = unit_at(s_off, U, pos); pos < pos_end; ++u) {
+      const int off = s_off[u], n_u = s_off[u + 1] - off;
+      const int start = pos - off;
+      const int stop = min(pos_end, off + n_u) - off;
+      pos = off + stop;
+      const bool owner = stop == n_u;
+      const int l = p.len_in[u];
+      const int b = u / p.hkv, g = u - b * p.hkv;
+      const int64_t pt = int64_t(u) * p.maxpages;
+      const int end = owner ? n_u - 1 : stop;          // closed slots [start, end)
+
+      // Q^T operand: lane (n, q) holds Q[head n][32 ks + 8q .. +8]; heads >= G are 0.
+      uint4 qb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qb[ks] = n < G ? ld16(static_cast<const char *>(p.q) +
+                              (int64_t(b * p.hq + g * G + n) * D + ks * 32 + 8 * q) * 2)
+                       : zero4;
+      if (q == 0) qb[0].x &= 0xffff0000u;              // Algorithm 1: q_t[0] <- 0
+
+      float m = neg_inf(), ls = 0.0f;
+      f32x4_t acc[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+      // One chunk of <= 32 rows: rows whose bit is set in vbits are valid.
+      auto consume = [&](const uint4 (&ka)[2][KS], uint4 (&va)[NT], uint32_t vbits) {
+        f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          s0 = mfma_16x16x32(ka[0][ks], qb[ks], s0);
+          s1 = mfma_16x16x32(ka[1][ks], qb[ks], s1);
+        }
+        const uint32_t mine = (vbits >> (8 * q)) & 0xffu;   // rows 8q .. 8q+7
+        float sv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          sv[i] = ((mine >> i) & 1u) ? s0[i] * p.scale_log2 : neg_inf();
+          sv[4 + i] = ((mine >> (4 + i)) & 1u) ? s1[i] * p.scale_log2 : neg_inf();
+        }
+        float mc = sv[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) mc = fmaxf(mc, sv[j]);
+        mc = fmaxf(mc, __shfl_xor(mc, 16, 64));
+        mc = fmaxf(mc, __shfl_xor(mc, 32, 64));
+        const float mn = fmaxf(m, mc);
+        if (vbits == 0u) return;
+        const float f = fast_exp2(m - mn);
+        ls *= f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[nt] *= f;
+        m = mn;
+        uint32_t pw[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          pw[w] = bf16_pair(fast_exp2(sv[2 * w] - mn), fast_exp2(sv[2 * w + 1] - mn));
+          ls += __uint_as_float(pw[w] << 16) + __uint_as_float(pw[w] & 0xffff0000u);
+        }
+        const uint4 pb = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+        // Rows past the unit's length hold unwritten page memory: clear them in V^T.
+        uint32_t keep[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          keep[w] = (((mine >> (2 * w)) & 1u) ? 0x0000ffffu : 0u) |
+                    (((mine >> (2 * w + 1)) & 1u) ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          va[nt].x &= keep[0];
+          va[nt].y &= keep[1];
+          va[nt].z &= keep[2];
+          va[nt].w &= keep[3];
+          acc[nt] = mfma_16x16x32(va[nt], pb, acc[nt]);
+        }
+      };
+
+      if (end > start) {
+        const int c0 = start >> 5, c1 = (end - 1) >> 5;
+        auto issue = [&](int ch, uint4 (&ka)[2][KS], uint4 (&va)[NT]) {
+          const int row0 = ch << 5;
+          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + 32) - row0;
+          const int page = p.ptab[pt + (row0 >> p.log2p)];
+          const char *pg = p.pool + int64_t(page) * p.page_bytes;
+          const int ro = row0 & (P - 1);
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const int rr = min(max(krow + 4 * t, rlo), rhi - 1);
+            const char *kr = pg + int64_t(ro + rr) * RB + q * 16;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) ka[t][ks] = ld16_stream(kr + ks * 64);
+          }
+          const char *vtp = pg + int64_t(P) * RB + (ro + 8 * q) * 2;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) va[nt] = ld16_stream(vtp + int64_t(16 * nt + n) * P * 2);
+        };
+        auto bits = [&](int ch) -> uint32_t {
+          const int row0 = ch << 5;
+          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + 32) - row0;
+          const uint32_t hi_mask = rhi >= 32 ? 0xffffffffu : ((1u << rhi) - 1u);
+          return hi_mask & ~((1u << rlo) - 1u);
+        };
+        // One buffer: at 2 waves per SIMD the other wave's loads cover this
+        // one's products (a second buffer would cost that occupancy).
+        uint4 ka_a[2][KS], va_a[NT];
+        for (int ch = c0; ch <= c1; ++ch) {
+          issue(ch, ka_a, va_a);
+          consume(ka_a, va_a, bits(ch));
+        }
+      }
+
+      // Owner: Algorithm 1 loads (issued after the stream to keep registers free).
+      float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
+      int open_page = -1;
+      uint4 kt[KS], ko[KS];
+      uint16_t vt[NT], vo[NT];
+      if (owner) {
+        k0 = load_elem<2>(p.k, int64_t(u) * D);
+        q0 = load_elem<2>(p.q, int64_t(b * p.hq + g * G) * D);
+        const char *kp = static_cast<const char *>(p.k) + int64_t(u) * RB;
+        const uint16_t *vp = static_cast<const uint16_t *>(p.v) + int64_t(u) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kt[ks] = ld16(kp + ks * 64 + q * 16);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) vt[nt] = vp[16 * nt + n];
+        if (l > 0) {
+          zold = p.z[u];
+          open_page = p.ptab[pt + ((l - 1) >> p.log2p)];
+          const char *pg = p.pool + int64_t(open_page) * p.page_bytes;
+          const int so = (l - 1) & (P - 1);
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) ko[ks] = ld16(pg + int64_t(so) * RB + ks * 64 + q * 16);
+          const uint16_t *vtp = reinterpret_cast<const uint16_t *>(pg + int64_t(P) * RB);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) vo[nt] = vtp[(16 * nt + n) * P + so];
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) ko[ks] = zero4;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) vo[nt] = 0;
+        }
+      }
+
+      if (owner) {
+        // Algorithm 1 for unit u (decision, importance, merge or append).
+        const int alpha = (l > 0 && k0 > p.c) ? 1 : 0;
+        float om;
+        if (p.omega_src == 0) {
+          om = sigmoid_floor(q0);
+        } else {
+          float sum = 0.0f;
+          for (int h = 0; h < G; ++h)
+            sum += sigmoid_floor(load_elem<2>(p.q, int64_t(b * p.hq + g * G + h) * D));
+          om = fmaxf(sum / G, 0x1p-100f);
+        }
+        int flag = 0, slot, page = open_page;
+        bool has_cur = true;
+        float znew;
+        if (alpha) {
+          slot = l - 1;
+          znew = zold + om;
+        } else {
+          slot = l;
+          znew = om;
+          if (l >= p.max_slots) {
+            has_cur = false;
+            flag = FLAG_SLOTS_EXHAUSTED;
+          } else if ((l & (P - 1)) == 0) {
+            int pg = 0;
+            if (lane == 0) {
+              const unsigned long long x = atomicAdd(&p.ctrl->pages_used, 1ull);
+              pg = x < static_cast<unsigned long long>(p.num_pages) ? static_cast<int>(x) : -1;
+            }
+            pg = __shfl(pg, 0, 64);
+            if (pg < 0) {
+              has_cur = false;
+              flag = FLAG_POOL_EXHAUSTED;
+            } else {
+              page = pg;
+              if (lane == 0) p.ptab[pt + (l >> p.log2p)] = pg;
+            }
+          }
+        }
+        // Current key (lanes hold dims 32 ks + 8q .. +8) and value (dims 16 nt + n).
+        uint4 kc[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          float kf[8], of[8];
+          V16<2>::unpack(kt[ks], kf);
+          V16<2>::unpack(ko[ks], of);
+          if (ks == 0 && q == 0) kf[0] = 0.0f;            // Algorithm 1: k_t[0] <- 0
+          if (alpha) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kf[e] = (of[e] * zold + kf[e] * om) / znew;
+          }
+          kc[ks] = V16<2>::pack(kf);
+        }
+        uint16_t vc[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          float vf = __uint_as_float(uint32_t(vt[nt]) << 16);
+          if (alpha) vf = (__uint_as_float(uint32_t(vo[nt]) << 16) * zold + vf * om) / znew;
+          vc[nt] = static_cast<uint16_t>(bf16_bits(vf));
+        }
+        if (has_cur) {
+          char *pg = p.pool + int64_t(page) * p.page_bytes;
+          const int so = slot & (P - 1);
+          if (n == 0) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) st16(pg + int64_t(so) * RB + ks * 64 + q * 16, kc[ks]);
+          }
+          if (q == 0) {
+            uint16_t *vtp = reinterpret_cast<uint16_t *>(pg + int64_t(P) * RB);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) vtp[(16 * nt + n) * P + so] = vc[nt];
+          }
+        }
+        // Attend to the old open slot (kept on append) and the current slot:
+        // a pseudo-chunk with them as rows 0 and 1.
+        const bool old_valid = !alpha && l > 0;
+        uint4 ka[2][KS], va[NT];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          ka[0][ks] = n == 0 ? ko[ks] : (n == 1 ? kc[ks] : zero4);
+          ka[1][ks] = zero4;
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          va[nt] = q == 0 ? make_uint4(uint32_t(vo[nt]) | (uint32_t(vc[nt]) << 16), 0, 0, 0) : zero4;
+        consume(ka, va, (old_valid ? 1u : 0u) | (has_cur ? 2u : 0u));
+        if (lane == 0) {
+          if (has_cur) p.z[u] = znew;
+          p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
+          if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
+          if (flag) atomicOr(&p.ctrl->flags, flag);
+          const int r0 = off / span;
+          p.meta[2 * u] = r0 + u;
+          p.meta[2 * u + 1] = r - r0 + 1;
+        }
+      }
+
+      ls += __shfl_xor(ls, 16, 64);
+      ls += __shfl_xor(ls, 32, 64);
+      if (n < G) {
+        if (start == 0 && owner) {     // the whole unit in one piece: final output
+          const float inv = ls > 0.0f ? 1.0f / ls : 0.0f;
+          uint16_t *op = static_cast<uint16_t *>(p.out) + int64_t(b * p.hq + g * G + n) * D + 4 * q;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const uint2 w = make_uint2(bf16_pair(acc[nt][0] * inv, acc[nt][1] * inv),
+                                       bf16_pair(acc[nt][2] * inv, acc[nt][3] * inv));
+            *reinterpret_cast<uint2 *>(op + 16 * nt) = w;
+          }
+        } else {                       // partial record r + u for the combine launch
+          float *rec = p.partials + (int64_t(r + u) * G + n) * REC;
+          if (q == 0) {
+            rec[0] = m;
+            rec[1] = ls;
+          }
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            *reinterpret_cast<float4 *>(rec + 4 + 16 * nt + 4 * q) =
+                make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
+        }
+      }
+    }
+  }
+}
+
 // Combine the split-K partial records of units with more than one tile:
 // o = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i.  One wave per
 // (b, query head); lane i fetches record i's max and sum, then every lane
@@ -736,10 +1070,14 @@ __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *
   }
   __syncthreads();
   if (tid == 0) {
-    if (fail)
+    if (fail) {
       atomicOr(&ctrl->flags, FLAG_POOL_EXHAUSTED);
-    else
+      ctrl->alloc_count = 0;
+    } else {
       ctrl->pages_used = static_cast<unsigned long long>(base + total);
+      ctrl->alloc_base = base;
+      ctrl->alloc_count = total;
+    }
   }
 }
 
@@ -875,7 +1213,7 @@ __global__ __launch_bounds__(kThreads) void import_kernel(DenseParams p) {
   }
 }
 
-template <int ES, int D>
+template <int ES, int D, bool VT>
 __global__ __launch_bounds__(kThreads) void export_kernel(DenseParams p) {
   constexpr int RB = D * ES, CPR = RB / 16;
   const int u = blockIdx.y;
@@ -892,10 +1230,67 @@ __global__ __launch_bounds__(kThreads) void export_kernel(DenseParams p) {
       const int page = p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)];
       const char *src = p.pool + int64_t(page) * p.page_bytes + int64_t(s & (P - 1)) * RB + c * 16;
       kv = ld16(src);
-      vv = ld16(src + int64_t(P) * RB);
+      if constexpr (VT) {
+        const uint16_t *vt = reinterpret_cast<const uint16_t *>(p.pool + int64_t(page) * p.page_bytes +
+                                                                int64_t(P) * RB);
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          w[j] = uint32_t(vt[(c * 8 + 2 * j) * P + (s & (P - 1))]) |
+                 (uint32_t(vt[(c * 8 + 2 * j + 1) * P + (s & (P - 1))]) << 16);
+        vv = make_uint4(w[0], w[1], w[2], w[3]);
+      } else {
+        vv = ld16(src + int64_t(P) * RB);
+      }
     }
     st16(static_cast<char *>(p.kd) + dst, kv);
     st16(static_cast<char *>(p.vd) + dst, vv);
+  }
+}
+
+// Value pages of matrix-core caches (32-slot pages) are stored transposed
+// ([d][32] bf16).  Prefill and import write rows ([32][d]); this pass turns
+// the pages the last allocation handed out into the transposed form, one
+// page per workgroup iteration: the whole page is read into LDS (row stride
+// padded against bank conflicts) before any of it is overwritten.
+template <int D>
+__global__ __launch_bounds__(kThreads) void transpose_v_pages_kernel(char *pool, int64_t page_bytes,
+                                                                     const Control *ctrl) {
+  constexpr int RB = D * 2;
+  constexpr int LDW = D + 2;                  // padded LDS row, in bf16 elements
+  constexpr int CHUNKS = 32 * RB / 16;        // 16-byte pieces of a page's value rows
+  constexpr int PER = (CHUNKS + kThreads - 1) / kThreads;
+  __shared__ uint16_t tile[32 * LDW];
+  const long long base = ctrl->alloc_base, count = ctrl->alloc_count;
+  for (long long job = blockIdx.x; job < count; job += gridDim.x) {
+    char *vreg = pool + (base + job) * page_bytes + 32 * RB;
+    uint4 rows[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = k * kThreads + threadIdx.x;
+      if (idx < CHUNKS) rows[k] = ld16(vreg + int64_t(idx) * 16);
+    }
+    __syncthreads();   // every reader of the previous page's tile is done
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = k * kThreads + threadIdx.x;
+      if (idx < CHUNKS) {
+        const int r = idx / (RB / 16), c = (idx % (RB / 16)) * 8;
+        const uint32_t w[4] = {rows[k].x, rows[k].y, rows[k].z, rows[k].w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) tile[r * LDW + c + j] = static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
+      }
+    }
+    __syncthreads();   // the page is fully in LDS before it is overwritten
+    // V^T[dim][8g .. 8g+7] for every dim and 8-row group g: 16-byte stores
+    for (int idx = threadIdx.x; idx < D * 4; idx += kThreads) {
+      const int dim = idx >> 2, g8 = (idx & 3) * 8;
+      uint32_t w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = uint32_t(tile[(g8 + 2 * j) * LDW + dim]) | (uint32_t(tile[(g8 + 2 * j + 1) * LDW + dim]) << 16);
+      st16(vreg + (int64_t(dim) * 32 + g8) * 2, make_uint4(w[0], w[1], w[2], w[3]));
+    }
   }
 }
 
@@ -919,10 +1314,25 @@ int grid_for(size_t n) {
   return static_cast<int>(g < 4096 ? (g > 0 ? g : 1) : 4096);
 }
 
+template <int D>
+hipError_t launch_transpose(char *pool, int64_t page_bytes, const Control *ctrl, hipStream_t s) {
+  hipLaunchKernelGGL((transpose_v_pages_kernel<D>), dim3(2048), dim3(kThreads), 0, s, pool,
+                     page_bytes, ctrl);
+  return hipGetLastError();
+}
+
 template <int ES, int D, int G>
-hipError_t decode_impl(const DecodeParams &p, int grid, hipStream_t s) {
+hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) {
   const size_t lds = decode_lds_bytes(p.units, G, D);
-  hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
+  if constexpr (ES == 2 && G >= 4) {
+    if (vt)
+      hipLaunchKernelGGL((decode_mfma_kernel<D, G>), dim3(grid), dim3(kThreads), lds, s, p);
+    else
+      hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
+  } else {
+    if (vt) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int batch = p.units / p.hkv;
@@ -932,18 +1342,18 @@ hipError_t decode_impl(const DecodeParams &p, int grid, hipStream_t s) {
 }
 
 template <int ES, int D>
-hipError_t decode_by_group(int group, const DecodeParams &p, int grid, hipStream_t s) {
+hipError_t decode_by_group(int group, const DecodeParams &p, int grid, bool vt, hipStream_t s) {
   switch (group) {
-    case 1: return decode_impl<ES, D, 1>(p, grid, s);
-    case 2: return decode_impl<ES, D, 2>(p, grid, s);
-    case 4: return decode_impl<ES, D, 4>(p, grid, s);
-    case 8: return decode_impl<ES, D, 8>(p, grid, s);
+    case 1: return decode_impl<ES, D, 1>(p, grid, vt, s);
+    case 2: return decode_impl<ES, D, 2>(p, grid, vt, s);
+    case 4: return decode_impl<ES, D, 4>(p, grid, vt, s);
+    case 8: return decode_impl<ES, D, 8>(p, grid, vt, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int ES, int D>
-hipError_t prefill_impl(const PrefillParams &p, hipStream_t s) {
+hipError_t prefill_impl(const PrefillParams &p, bool vt, hipStream_t s) {
   if (p.n > 0) {
     hipLaunchKernelGGL((prefill_decide_kernel<ES>), dim3(p.units), dim3(kThreads), 0, s, p);
   } else {
@@ -960,11 +1370,13 @@ hipError_t prefill_impl(const PrefillParams &p, hipStream_t s) {
   const int nch = (p.n + 63) / 64;
   hipLaunchKernelGGL((prefill_reduce_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
                      dim3(kThreads), 0, s, p);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !vt) return e;
+  return launch_transpose<D>(p.pool, p.page_bytes, p.ctrl, s);
 }
 
 template <int ES, int D>
-hipError_t import_impl(const DenseParams &p, hipStream_t s) {
+hipError_t import_impl(const DenseParams &p, bool vt, hipStream_t s) {
   const int limit = p.dense_slots < p.max_slots ? p.dense_slots : p.max_slots;
   hipLaunchKernelGGL(alloc_pages_kernel, dim3(1), dim3(1024), 0, s, p.len, p.z, p.ptab,
                      p.page_base, p.ctrl, p.num_pages, p.lengths_in, p.z_in, limit, p.units,
@@ -974,13 +1386,18 @@ hipError_t import_impl(const DenseParams &p, hipStream_t s) {
   hipLaunchKernelGGL((import_kernel<ES, D>),
                      dim3((p.dense_slots + kDenseRows - 1) / kDenseRows, p.units), dim3(kThreads), 0,
                      s, p);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !vt) return e;
+  return launch_transpose<D>(p.pool, p.page_bytes, p.ctrl, s);
 }
 
 template <int ES, int D>
-hipError_t export_impl(const DenseParams &p, hipStream_t s) {
+hipError_t export_impl(const DenseParams &p, bool vt, hipStream_t s) {
   const int bx = p.dense_slots > 0 ? (p.dense_slots + kDenseRows - 1) / kDenseRows : 1;
-  hipLaunchKernelGGL((export_kernel<ES, D>), dim3(bx, p.units), dim3(kThreads), 0, s, p);
+  if (vt)
+    hipLaunchKernelGGL((export_kernel<ES, D, true>), dim3(bx, p.units), dim3(kThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL((export_kernel<ES, D, false>), dim3(bx, p.units), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
@@ -1015,21 +1432,22 @@ hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, size_t count, hipSt
   ((es) == 2 ? ((d) == 128 ? fn<2, 128>(__VA_ARGS__) : fn<2, 64>(__VA_ARGS__)) \
              : ((d) == 128 ? fn<4, 128>(__VA_ARGS__) : fn<4, 64>(__VA_ARGS__)))
 
-hipError_t launch_decode(int elem_bytes, int head_dim, int group, const DecodeParams &p, int grid,
-                         hipStream_t s) {
-  return DMC_DISPATCH_ES_D(decode_by_group, elem_bytes, head_dim, group, p, grid, s);
+hipError_t launch_decode(int elem_bytes, int head_dim, int group, bool vt, const DecodeParams &p,
+                         int grid, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(decode_by_group, elem_bytes, head_dim, group, p, grid, vt, s);
 }
 
-hipError_t launch_prefill(int elem_bytes, int head_dim, const PrefillParams &p, hipStream_t s) {
-  return DMC_DISPATCH_ES_D(prefill_impl, elem_bytes, head_dim, p, s);
+hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillParams &p,
+                          hipStream_t s) {
+  return DMC_DISPATCH_ES_D(prefill_impl, elem_bytes, head_dim, p, vt, s);
 }
 
-hipError_t launch_import(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s) {
-  return DMC_DISPATCH_ES_D(import_impl, elem_bytes, head_dim, p, s);
+hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(import_impl, elem_bytes, head_dim, p, vt, s);
 }
 
-hipError_t launch_export(int elem_bytes, int head_dim, const DenseParams &p, hipStream_t s) {
-  return DMC_DISPATCH_ES_D(export_impl, elem_bytes, head_dim, p, s);
+hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s) {
+  return DMC_DISPATCH_ES_D(export_impl, elem_bytes, head_dim, p, vt, s);
 }
 
 }  // namespace dmc

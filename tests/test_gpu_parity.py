@@ -53,6 +53,11 @@ VARIANTS = [
     ("fp32", 64, 4, 32, 0, "group_mean", -0.5),
     ("fp32", 128, 8, 64, 64, "lead", 0.0),
     ("fp32", 64, 1, 256, 7, "lead", 0.0),
+    # grouped-query caches on matrix cores (bf16, G >= 4, 32-slot pages)
+    ("bf16", 128, 4, 32, 0, "lead", 0.0),
+    ("bf16", 64, 8, 32, 0, "group_mean", 0.0),
+    ("bf16", 64, 4, 32, 16, "lead", -0.3),
+    ("bf16", 128, 8, 32, 5, "group_mean", 0.0),
 ]
 
 
@@ -178,14 +183,16 @@ def test_empty_prompt_then_decode(torch_cuda):
     pr.ok()
 
 
-def test_import_export_roundtrip(torch_cuda):
+@pytest.mark.parametrize("G,d", [(1, 128), (4, 128), (8, 64)])
+def test_import_export_roundtrip(torch_cuda, G, d):
     """Importing a dense cache and exporting it is the identity on the
-    valid slots (bit-exact) and zero elsewhere; then decode on top of it."""
+    valid slots (bit-exact) and zero elsewhere; then decode on top of it.
+    G >= 4 exercises the transposed value pages of matrix-core caches."""
     import torch
-    log("case import/export")
-    B, Hkv, d, dense = 3, 2, 128, 70
+    log(f"case import/export G={G} d={d}")
+    B, Hkv, dense = 3, 2, 70
     lens = np.array([[0, 1], [31, 32], [33, 70]], dtype=np.int32)
-    pr = Pair(1, B, Hkv, Hkv, d, "bf16", max_slots=80, split_tile=32)
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=80, split_tile=32)
     K = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
     V = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
     z = torch.rand((B, Hkv)).cuda() * 3 + 0.1
@@ -199,7 +206,7 @@ def test_import_export_roundtrip(torch_cuda):
     assert torch.equal(z2[lt > 0], z[lt > 0])
     rng = np.random.default_rng(9)
     for _ in range(10):
-        pr.decode(0, *random_step(rng, B, Hkv, Hkv, d, np.array([1.5, 3.0]), "bf16", "cuda"))
+        pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, np.array([1.5, 3.0]), "bf16", "cuda"))
     pr.compare_cache(0)
     pr.ok()
 
