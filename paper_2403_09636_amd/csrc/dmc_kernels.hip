@@ -571,7 +571,7 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
   constexpr int NT = D / 16;      // 16-dim tiles of the value product
   constexpr int RB = D * 2;       // bytes per key row
@@ -622,21 +622,26 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-      // One chunk of <= 32 rows: rows whose bit is set in vbits are valid.
-      auto consume = [&](const uint4 (&ka)[2][KS], uint4 (&va)[NT], uint32_t vbits) {
+      // Score product of one chunk: lane (n, q) gets rows 8q .. 8q+7 of head n.
+      auto scores = [&](const uint4 (&ka)[2][KS], float (&sv)[8]) {
         f32x4_t s0 = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           s0 = mfma_16x16x32(ka[0][ks], qb[ks], s0);
           s1 = mfma_16x16x32(ka[1][ks], qb[ks], s1);
         }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          sv[i] = s0[i];
+          sv[4 + i] = s1[i];
+        }
+      };
+      // Online softmax + value product of one chunk (rows with a bit set in vbits are valid).
+      auto values = [&](const float (&sraw)[8], uint4 (&va)[NT], uint32_t vbits) {
         const uint32_t mine = (vbits >> (8 * q)) & 0xffu;   // rows 8q .. 8q+7
         float sv[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          sv[i] = ((mine >> i) & 1u) ? s0[i] * p.scale_log2 : neg_inf();
-          sv[4 + i] = ((mine >> (4 + i)) & 1u) ? s1[i] * p.scale_log2 : neg_inf();
-        }
+        for (int j = 0; j < 8; ++j) sv[j] = ((mine >> j) & 1u) ? sraw[j] * p.scale_log2 : neg_inf();
         float mc = sv[0];
 #pragma unroll
         for (int j = 1; j < 8; ++j) mc = fmaxf(mc, sv[j]);
@@ -674,35 +679,46 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
 
       if (end > start) {
         const int c0 = start >> 5, c1 = (end - 1) >> 5;
-        auto issue = [&](int ch, uint4 (&ka)[2][KS], uint4 (&va)[NT]) {
+        auto range_of = [&](int ch, int &rlo, int &rhi) {
           const int row0 = ch << 5;
-          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + 32) - row0;
-          const int page = p.ptab[pt + (row0 >> p.log2p)];
-          const char *pg = p.pool + int64_t(page) * p.page_bytes;
-          const int ro = row0 & (P - 1);
+          rlo = max(start, row0) - row0;
+          rhi = min(end, row0 + 32) - row0;
+        };
+        auto issue_k = [&](int ch, uint4 (&ka)[2][KS]) {
+          int rlo, rhi;
+          range_of(ch, rlo, rhi);
+          const char *pg = p.pool + int64_t(p.ptab[pt + ((ch << 5) >> p.log2p)]) * p.page_bytes;
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             const int rr = min(max(krow + 4 * t, rlo), rhi - 1);
-            const char *kr = pg + int64_t(ro + rr) * RB + q * 16;
+            const char *kr = pg + int64_t(rr) * RB + q * 16;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) ka[t][ks] = ld16_stream(kr + ks * 64);
           }
-          const char *vtp = pg + int64_t(P) * RB + (ro + 8 * q) * 2;
+        };
+        auto issue_v = [&](int ch, uint4 (&va)[NT]) {
+          const char *pg = p.pool + int64_t(p.ptab[pt + ((ch << 5) >> p.log2p)]) * p.page_bytes;
+          const char *vtp = pg + int64_t(P) * RB + (8 * q) * 2;
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) va[nt] = ld16_stream(vtp + int64_t(16 * nt + n) * P * 2);
         };
         auto bits = [&](int ch) -> uint32_t {
-          const int row0 = ch << 5;
-          const int rlo = max(start, row0) - row0, rhi = min(end, row0 + 32) - row0;
+          int rlo, rhi;
+          range_of(ch, rlo, rhi);
           const uint32_t hi_mask = rhi >= 32 ? 0xffffffffu : ((1u << rhi) - 1u);
           return hi_mask & ~((1u << rlo) - 1u);
         };
-        // One buffer: at 2 waves per SIMD the other wave's loads cover this
-        // one's products (a second buffer would cost that occupancy).
-        uint4 ka_a[2][KS], va_a[NT];
+        // One operand set; the next chunk's keys load during this chunk's
+        // softmax and value product, its values during the next score product.
+        uint4 ka[2][KS], va[NT];
+        issue_k(c0, ka);
+        issue_v(c0, va);
         for (int ch = c0; ch <= c1; ++ch) {
-          issue(ch, ka_a, va_a);
-          consume(ka_a, va_a, bits(ch));
+          float sraw[8];
+          scores(ka, sraw);
+          if (ch < c1) issue_k(ch + 1, ka);
+          values(sraw, va, bits(ch));
+          if (ch < c1) issue_v(ch + 1, va);
         }
       }
 
@@ -824,7 +840,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
           va[nt] = q == 0 ? make_uint4(uint32_t(vo[nt]) | (uint32_t(vc[nt]) << 16), 0, 0, 0) : zero4;
-        consume(ka, va, (old_valid ? 1u : 0u) | (has_cur ? 2u : 0u));
+        float sraw[8];
+        scores(ka, sraw);
+        values(sraw, va, (old_valid ? 1u : 0u) | (has_cur ? 2u : 0u));
         if (lane == 0) {
           if (has_cur) p.z[u] = znew;
           p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
