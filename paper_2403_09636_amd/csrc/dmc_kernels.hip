@@ -24,7 +24,15 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kChunk = 32;  // max rows a wave streams per chunk
+constexpr int kChunk = 32;  // max rows of a matrix-core chunk
+#ifndef DMC_VALU_CHUNK
+#define DMC_VALU_CHUNK 16
+#endif
+#ifndef DMC_VALU_BUFFERS
+#define DMC_VALU_BUFFERS 3
+#endif
+constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
+constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
 
@@ -81,6 +89,50 @@ struct V16<4> {
   __device__ static __forceinline__ uint4 pack(float *f) {
     return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
                       __float_as_uint(f[3]));
+  }
+};
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// One lane's slice of a query head (16 bytes of it) with q[0] zeroed, and
+// its dot product with the matching 16-byte slice of a key row.  bf16 keeps
+// the query packed and uses v_dot2_f32_bf16 (products exact in fp32, fp32
+// accumulation); fp32 uses plain FMAs.
+template <int ES>
+struct QSlice;
+template <>
+struct QSlice<2> {
+  uint4 w;
+  __device__ __forceinline__ void load(const char *p, bool first) {
+    w = *reinterpret_cast<const uint4 *>(p);
+    if (first) w.x &= 0xffff0000u;
+  }
+  __device__ __forceinline__ float dot(const uint4 &k) const {
+    float d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.x),
+                                              __builtin_bit_cast(bf16x2_t, k.x), 0.0f, false);
+    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.y),
+                                        __builtin_bit_cast(bf16x2_t, k.y), d, false);
+    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.z),
+                                        __builtin_bit_cast(bf16x2_t, k.z), d, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.w),
+                                           __builtin_bit_cast(bf16x2_t, k.w), d, false);
+  }
+};
+template <>
+struct QSlice<4> {
+  float f[4];
+  __device__ __forceinline__ void load(const char *p, bool first) {
+    const uint4 r = *reinterpret_cast<const uint4 *>(p);
+    V16<4>::unpack(r, f);
+    if (first) f[0] = 0.0f;
+  }
+  __device__ __forceinline__ float dot(const uint4 &k) const {
+    float kf[4];
+    V16<4>::unpack(k, kf);
+    float d = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) d = fmaf(f[e], kf[e], d);
+    return d;
   }
 };
 
@@ -242,9 +294,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   constexpr int VN = V::N;        // elements per 16-byte lane chunk
   constexpr int LPR = D / VN;     // lanes per cache row
   constexpr int RPI = 64 / LPR;   // rows per wave-wide load
-  constexpr int NI = kChunk / RPI;
+  constexpr int NI = kValuChunk / RPI;
   constexpr int REC = D + 4;      // partial record: m, l, -, -, acc[D]
   constexpr int RB = D * ES;      // bytes per row
+  constexpr int kLog2Chunk = kValuChunk == 8 ? 3 : kValuChunk == 16 ? 4 : 5;
+  static_assert(kValuChunk == (1 << kLog2Chunk) && NI >= 1, "chunk rows");
 
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_wsum[kWaves];
@@ -254,8 +308,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane / LPR, part = lane % LPR;
   const int P = 1 << p.log2p;
-  const int CS = P < kChunk ? P : kChunk;
-  const int log2cs = p.log2p < 5 ? p.log2p : 5;
+  const int CS = P < kValuChunk ? P : kValuChunk;
+  const int log2cs = p.log2p < kLog2Chunk ? p.log2p : kLog2Chunk;
 
   const int S = build_slot_space(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
@@ -277,17 +331,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       const int64_t pt = int64_t(u) * p.maxpages;
       int end = owner ? n_u - 1 : stop;                 // closed slots [start, end)
 
-      // The unit's query heads, element 0 zeroed, pre-scaled by log2(e)/sqrt(d).
-      float qf[G][VN];
+      // The unit's query heads (this lane's slice), element 0 zeroed.  Scores
+      // are scaled by log2(e)/sqrt(d) after the row sum.
+      QSlice<ES> qs[G];
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const char *qp = static_cast<const char *>(p.q) +
-                         (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES;
-        V::unpack(ld16(qp), qf[h]);
-        if (part == 0) qf[h][0] = 0.0f;
-#pragma unroll
-        for (int e = 0; e < VN; ++e) qf[h][e] *= p.scale_log2;
-      }
+      for (int h = 0; h < G; ++h)
+        qs[h].load(static_cast<const char *>(p.q) +
+                       (int64_t(b * p.hq + g * G + h) * D + part * VN) * ES,
+                   part == 0);
 
       // Owner of the unit's last position: start the loads Algorithm 1 needs
       // (new key/value, decision and importance neurons, z, the open slot) so
@@ -322,8 +373,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int e = 0; e < VN; ++e) acc[h][e] = 0.0f;
       }
       if (end > start) {
-        // Chunks of <= CS rows inside one page; the next chunk's loads are in
-        // flight while the current one is consumed (two register buffers).
+        // Chunks of <= CS rows inside one page, kBuf register buffers in a
+        // ring: kBuf - 1 chunks are in flight while one is consumed.
         const int c0 = start >> log2cs, c1 = (end - 1) >> log2cs;
         auto issue = [&](int ch, uint4 *kr, uint4 *vr) {
           const int row0 = ch << log2cs;
@@ -349,16 +400,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
           float s[G][NI];
 #pragma unroll
           for (int i = 0; i < NI; ++i) {
-            float kf[VN];
-            V::unpack(kr[i], kf);
             const int rr = i * RPI + grp;
             const bool valid = rr >= rlo && rr < rhi;
 #pragma unroll
             for (int h = 0; h < G; ++h) {
-              float d = 0.0f;
-#pragma unroll
-              for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], kf[e], d);
-              d = row_sum<LPR>(d);
+              const float d = row_sum<LPR>(qs[h].dot(kr[i])) * p.scale_log2;
               s[h][i] = valid ? d : neg_inf();
             }
           }
@@ -394,14 +440,18 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
             }
           }
         };
-        uint4 ka[NI], va[NI], kb2[NI], vb2[NI];
-        issue(c0, ka, va);
-        for (int ch = c0; ch <= c1; ch += 2) {
-          if (ch + 1 <= c1) issue(ch + 1, kb2, vb2);
-          consume(ch, ka, va);
-          if (ch + 1 > c1) break;
-          if (ch + 2 <= c1) issue(ch + 2, ka, va);
-          consume(ch + 1, kb2, vb2);
+        uint4 kbuf[kBuf][NI], vbuf[kBuf][NI];
+#pragma unroll
+        for (int j = 0; j < kBuf - 1; ++j)
+          if (c0 + j <= c1) issue(c0 + j, kbuf[j], vbuf[j]);
+        for (int ch = c0; ch <= c1; ch += kBuf) {
+#pragma unroll
+          for (int j = 0; j < kBuf; ++j) {
+            if (ch + j > c1) break;
+            if (ch + j + kBuf - 1 <= c1)
+              issue(ch + j + kBuf - 1, kbuf[(j + kBuf - 1) % kBuf], vbuf[(j + kBuf - 1) % kBuf]);
+            consume(ch + j, kbuf[j], vbuf[j]);
+          }
         }
       }
 
@@ -451,15 +501,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
           }
         } else {
           if (l > 0) {   // the old open slot stays as it is: attend to it
-            float ok[VN], ov[VN];
-            V::unpack(ok_raw, ok);
+            float ov[VN];
             V::unpack(ov_raw, ov);
 #pragma unroll
             for (int h = 0; h < G; ++h) {
-              float d = 0.0f;
-#pragma unroll
-              for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ok[e], d);
-              d = row_sum<LPR>(d);
+              const float d = row_sum<LPR>(qs[h].dot(ok_raw)) * p.scale_log2;
               merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, ov);
             }
           }
@@ -494,10 +540,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
           }
 #pragma unroll
           for (int h = 0; h < G; ++h) {
-            float d = 0.0f;
-#pragma unroll
-            for (int e = 0; e < VN; ++e) d = fmaf(qf[h][e], ck[e], d);
-            d = row_sum<LPR>(d);
+            const float d = row_sum<LPR>(qs[h].dot(kp)) * p.scale_log2;
             merge_state<VN>(m[h], ls[h], acc[h], d, 1.0f, cv);
           }
         }
