@@ -58,6 +58,8 @@ VARIANTS = [
     ("bf16", 64, 8, 32, 0, "group_mean", 0.0),
     ("bf16", 64, 4, 32, 16, "lead", -0.3),
     ("bf16", 128, 8, 32, 5, "group_mean", 0.0),
+    # one slot per range: units split into up to 75 pieces (> 64 records in the combine)
+    ("fp32", 64, 1, 32, 1, "lead", 0.0),
 ]
 
 
@@ -251,3 +253,27 @@ def test_bad_import_length_sets_flag(torch_cuda):
                    torch.ones((1, 2), device="cuda"))
     assert pr.gpu.status() == P.binding.DMC_ERR_INVALID_ARG
     assert pr.gpu.lengths(0).cpu().numpy().tolist() == [[3, 0]]
+
+
+def test_largest_unit_table(torch_cuda):
+    """batch * kv heads near the decode kernel's LDS slot-table limit (64 KB):
+    16000 units of one query head each, a few steps from empty, against the
+    oracle on a sample of units (slot indices of all units bit-exact)."""
+    import torch
+    import oracle
+    import paper_2403_09636_amd as P
+    log("case largest unit table")
+    B, H, d, steps = 1000, 16, 64, 3
+    cfg = P.make_config(1, B, H, H, d, "bf16", 32, 8)
+    cache = P.DMCCache(cfg, device="cuda")
+    orc = oracle.DMCOracle(1, B, H, H, d, 8)
+    rng = np.random.default_rng(77)
+    for _ in range(steps):
+        q, k, v = random_step(rng, B, H, H, d, np.full(H, 2.0), "bf16", "cuda")
+        si = torch.empty((B, H), dtype=torch.int32, device="cuda")
+        out = cache.decode_step(0, q, k, v, slot_index=si)
+        ref, ref_si = orc.decode_step(0, f64(q), f64(k), f64(v))
+        assert (si.cpu().numpy() == ref_si).all()
+        err = np.abs(f64(out) - ref)
+        assert (err <= 2e-2 + 1e-2 * np.abs(ref)).all(), err.max()
+    cache.check()
