@@ -82,7 +82,8 @@ typedef struct dmc_cache_config {
   int32_t split_tile;        /* cap on slots per split-K range; 0 = no cap: each wave of
                                 a decode launch gets an equal share of the layer's actual
                                 (compressed) slots */
-  int32_t max_prompt_len;    /* largest n for dmc_prefill_compress; 0 = max_slots_per_seq */
+  int32_t max_prompt_len;    /* largest n for dmc_prefill_compress / dmc_prefill_attend;
+                                0 = max_slots_per_seq */
 } dmc_cache_config;
 
 typedef struct dmc_cache dmc_cache; /* opaque host handle */
@@ -131,6 +132,34 @@ dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer,
                                 const void *q_dev, const int64_t q_strides[3],
                                 int32_t n, const int32_t *prompt_lens_dev,
                                 int32_t *slot_index_dev, dmc_stream_t stream);
+
+/* Prompt phase of one layer with attention outputs: the compaction of
+ * dmc_prefill_compress (same cache result, same slot_index), and for every
+ * prompt token t the softmax attention of its G query heads over the cache
+ * as it stands right after token t's own update -- the per-position form of
+ * the inference rule of Sec. 3.1 (Sec. 3.2 states the same set as a mask
+ * over the unrolled intermediate states): the final state of every segment
+ * that closed before t (slots 0 .. slot(t)-1), plus the running omega-
+ * weighted mean of t's own segment over its tokens up to t.  Scale
+ * 1/sqrt(d), q[0] treated as 0, as in decode.
+ *   k_dev, v_dev, k_strides, v_strides, n, prompt_lens_dev, slot_index_dev:
+ *     as for dmc_prefill_compress.
+ *   q_dev: logical [B, n, Hq, d] with q_strides for B, n, Hq (d contiguous);
+ *     every element is read; 16-byte aligned, strides multiples of 8.
+ *   out_dev: logical [B, n, Hq, d], config dtype, out_strides for B, n, Hq
+ *     (d contiguous), 16-byte aligned, strides multiples of 8.  Rows of
+ *     tokens t >= prompt_lens[b] are written as zeros.  out must not overlap
+ *     q, k or v.
+ * bf16 runs on the matrix cores (v_mfma_f32_16x16x32_bf16, fp32
+ * accumulation), fp32 on the vector ALUs.  Uses the staging area sized by
+ * max_prompt_len, including the per-32-token running-sum records. */
+dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer,
+                              const void *k_dev, const int64_t k_strides[3],
+                              const void *v_dev, const int64_t v_strides[3],
+                              const void *q_dev, const int64_t q_strides[3],
+                              int32_t n, const int32_t *prompt_lens_dev,
+                              void *out_dev, const int64_t out_strides[3],
+                              int32_t *slot_index_dev, dmc_stream_t stream);
 
 /* One auto-regressive decode step of one layer: for every unit, the DMC
  * update of Algorithm 1 with the new token (alpha from the unit's own k[0];

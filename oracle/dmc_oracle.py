@@ -263,6 +263,39 @@ class DMCOracle:
             slots[:, t] = slot
         return slots.reshape(self.B, self.Hkv, n)
 
+    def prefill_attend(self, layer, q, k, v, prompt_lens=None):
+        """Prompt phase with attention: for every prompt token in order, the
+        Algorithm 1 update and then the attention of its query heads over the
+        updated cache -- the inference semantics of Sec. 3.1 applied to each
+        prompt position (equivalently the training-time view of Sec. 3.2 with
+        discrete decisions).
+
+        q: [B, n, Hq, d]; k, v: [B, n, Hkv, d].  The layer's cache must be
+        empty.  Returns out [B, n, Hq, d] (zeros for tokens past a row's
+        prompt length) and slot_index [B, Hkv, n].
+        """
+        lc = self.layers[layer]
+        assert not lc.l.any(), "prefill expects an empty layer cache"
+        q = np.asarray(q, dtype=np.float64)
+        k = np.asarray(k, dtype=np.float64)
+        v = np.asarray(v, dtype=np.float64)
+        B, n = k.shape[:2]
+        lens = np.full(B, n) if prompt_lens is None else np.asarray(prompt_lens)
+        U = self.B * self.Hkv
+        out = np.zeros((self.B, n, self.Hq, self.d))
+        slots = np.full((U, n), -1, dtype=np.int64)
+        for t in range(n):
+            active = np.repeat(lens > t, self.Hkv)
+            _, slot = lc.update(k[:, t].reshape(U, self.d), v[:, t].reshape(U, self.d),
+                                self._q0_groups(q[:, t, :, 0]), active=active,
+                                c=self.c, omega_src=self.omega_src)
+            slots[:, t] = slot
+            qg = q[:, t].reshape(U, self.G, self.d)
+            for u in np.nonzero(active)[0]:
+                b, g = divmod(u, self.Hkv)
+                out[b, t, g * self.G:(g + 1) * self.G] = lc.attend(u, qg[u])
+        return out, slots.reshape(self.B, self.Hkv, n)
+
     def export(self, layer):
         """Dense copy of one layer: K, V [B, Hkv, cap, d], lengths, z [B, Hkv]."""
         lc = self.layers[layer]

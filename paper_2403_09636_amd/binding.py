@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "DMC_OK", 1: "DMC_ERR_INVALID_ARG", 2: "DMC_ERR_UNSUPPORTED",
 
 #: Every entry point declared in include/dmc.h.
 EXPORTS = ("dmc_cache_workspace_bytes", "dmc_cache_alloc", "dmc_cache_free", "dmc_cache_reset",
-           "dmc_prefill_compress", "dmc_decode_step", "dmc_cache_lengths", "dmc_cache_export",
+           "dmc_prefill_compress", "dmc_prefill_attend", "dmc_decode_step", "dmc_cache_lengths", "dmc_cache_export",
            "dmc_cache_import", "dmc_cache_check", "dmc_cache_pages_used", "dmc_last_error")
 
 
@@ -55,6 +55,9 @@ def _load():
     lib.dmc_cache_reset.argtypes = [c_void_p, c_void_p]
     lib.dmc_prefill_compress.argtypes = [c_void_p, c_int32, c_void_p, i64p, c_void_p, i64p,
                                          c_void_p, i64p, c_int32, c_void_p, c_void_p, c_void_p]
+    lib.dmc_prefill_attend.argtypes = [c_void_p, c_int32, c_void_p, i64p, c_void_p, i64p,
+                                       c_void_p, i64p, c_int32, c_void_p, c_void_p, i64p,
+                                       c_void_p, c_void_p]
     lib.dmc_decode_step.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                     c_void_p, c_void_p]
     lib.dmc_cache_lengths.argtypes = [c_void_p, c_int32, c_void_p, c_void_p]
@@ -167,6 +170,24 @@ class DMCCache:
         qs = (c_int64 * 3)(q.stride(0), q.stride(1), q.stride(2))
         check(lib.dmc_prefill_compress(self.handle, layer, _ptr(k), ks, _ptr(v), vs, _ptr(q), qs,
                                        n, _ptr(prompt_lens), _ptr(slot_index), _stream(stream)))
+
+    def prefill_attend(self, layer, k, v, q, out=None, n=None, prompt_lens=None, slot_index=None,
+                       stream=None):
+        """Compress a prompt and attend every prompt query: k, v [B, n, Hkv, d],
+        q [B, n, Hq, d] (strided, d contiguous); returns out [B, n, Hq, d]."""
+        n = k.shape[1] if n is None else n
+        if out is None:
+            import torch
+            out = torch.empty((q.shape[0], n, q.shape[2], q.shape[3]), dtype=q.dtype,
+                              device=q.device)
+        ks = (c_int64 * 3)(k.stride(0), k.stride(1), k.stride(2))
+        vs = (c_int64 * 3)(v.stride(0), v.stride(1), v.stride(2))
+        qs = (c_int64 * 3)(q.stride(0), q.stride(1), q.stride(2))
+        os_ = (c_int64 * 3)(out.stride(0), out.stride(1), out.stride(2))
+        check(lib.dmc_prefill_attend(self.handle, layer, _ptr(k), ks, _ptr(v), vs, _ptr(q), qs, n,
+                                     _ptr(prompt_lens), _ptr(out), os_, _ptr(slot_index),
+                                     _stream(stream)))
+        return out
 
     # -- accessors --------------------------------------------------------------
     def lengths(self, layer, stream=None):

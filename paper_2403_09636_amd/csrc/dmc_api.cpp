@@ -120,6 +120,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   }
   L.max_prompt = c.max_prompt_len > 0 ? c.max_prompt_len : c.max_slots_per_seq;
   L.prompt_chunks = (L.max_prompt + 63) / 64;
+  L.carry_blocks = (L.max_prompt + 31) / 32;
   L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
   // Grouped-query caches decode on matrix cores with value pages transposed.
   L.v_trans = c.dtype == DMC_BF16 && L.group >= 4 && c.page_size == 32;
@@ -141,6 +142,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.pf_omega = take(U * size_t(L.max_prompt) * 4);
   L.pf_count = take(U * size_t(L.prompt_chunks) * 4);
   L.pf_pagebase = take(U * 4);
+  L.pf_carry = take(U * size_t(L.carry_blocks) * dmc::carry_stride(c.head_dim) * 4);
   L.total = off;
   return L;
 }
@@ -303,12 +305,13 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   return DMC_OK;
 }
 
-dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
-                                const int64_t k_strides[3], const void *v,
-                                const int64_t v_strides[3], const void *q,
-                                const int64_t q_strides[3], int32_t n,
-                                const int32_t *prompt_lens, int32_t *slot_index,
-                                dmc_stream_t stream) {
+namespace {
+
+// Shared argument checks and parameter set-up of the two prompt entry points.
+dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const int64_t k_strides[3],
+                          const void *v, const int64_t v_strides[3], const void *q,
+                          const int64_t q_strides[3], int32_t n, const int32_t *prompt_lens,
+                          int32_t *slot_index, bool full_q, dmc::PrefillParams *out) {
   dmc_status st = check_layer(cache, layer);
   if (st != DMC_OK) return st;
   const dmc_cache_config &c = cache->cfg;
@@ -321,14 +324,18 @@ dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
       return fail(DMC_ERR_INVALID_ARG, "stride arrays must be non-NULL");
     if (!aligned16(k) || !aligned16(v))
       return fail(DMC_ERR_INVALID_ARG, "k and v must be 16-byte aligned");
+    if (full_q && !aligned16(q)) return fail(DMC_ERR_INVALID_ARG, "q must be 16-byte aligned");
     for (int i = 0; i < 3; ++i) {
       if (k_strides[i] < 0 || v_strides[i] < 0 || q_strides[i] < 0)
         return fail(DMC_ERR_INVALID_ARG, "strides must be non-negative");
       if (k_strides[i] % 8 || v_strides[i] % 8)
         return fail(DMC_ERR_INVALID_ARG, "k and v strides must be multiples of 8 elements");
+      if (full_q && q_strides[i] % 8)
+        return fail(DMC_ERR_INVALID_ARG, "q strides must be multiples of 8 elements");
     }
   }
-  dmc::PrefillParams p{};
+  dmc::PrefillParams &p = *out;
+  p = dmc::PrefillParams{};
   p.pool = cache->ws + L.pool;
   p.page_bytes = L.page_bytes;
   p.num_pages = c.num_pages;
@@ -350,6 +357,7 @@ dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
   p.omega = at<float>(cache, L.pf_omega);
   p.count = at<int32_t>(cache, L.pf_count);
   p.page_base = at<int32_t>(cache, L.pf_pagebase);
+  p.carry = nullptr;
   p.c = c.decision_bias;
   p.n = n;
   p.units = L.units;
@@ -360,11 +368,88 @@ dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
   p.omega_src = c.omega_src;
   p.max_prompt = L.max_prompt;
   p.prompt_chunks = L.prompt_chunks;
+  p.carry_blocks = L.carry_blocks;
+  return DMC_OK;
+}
+
+}  // namespace
+
+dmc_status dmc_prefill_compress(dmc_cache *cache, int32_t layer, const void *k,
+                                const int64_t k_strides[3], const void *v,
+                                const int64_t v_strides[3], const void *q,
+                                const int64_t q_strides[3], int32_t n,
+                                const int32_t *prompt_lens, int32_t *slot_index,
+                                dmc_stream_t stream) {
+  dmc::PrefillParams p;
+  dmc_status st = prefill_params(cache, layer, k, k_strides, v, v_strides, q, q_strides, n,
+                                 prompt_lens, slot_index, false, &p);
+  if (st != DMC_OK) return st;
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, L.v_trans, p,
-                                     static_cast<hipStream_t>(stream));
+  hipError_t e = dmc::launch_prefill(elem_bytes(cache->cfg), cache->cfg.head_dim, cache->lay.v_trans,
+                                     p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  return DMC_OK;
+}
+
+dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer, const void *k,
+                              const int64_t k_strides[3], const void *v,
+                              const int64_t v_strides[3], const void *q,
+                              const int64_t q_strides[3], int32_t n,
+                              const int32_t *prompt_lens, void *out,
+                              const int64_t out_strides[3], int32_t *slot_index,
+                              dmc_stream_t stream) {
+  dmc::PrefillParams p;
+  dmc_status st = prefill_params(cache, layer, k, k_strides, v, v_strides, q, q_strides, n,
+                                 prompt_lens, slot_index, true, &p);
+  if (st != DMC_OK) return st;
+  if (n > 0) {
+    if (!out || !out_strides) return fail(DMC_ERR_INVALID_ARG, "out and out_strides must be non-NULL");
+    if (!aligned16(out)) return fail(DMC_ERR_INVALID_ARG, "out must be 16-byte aligned");
+    for (int i = 0; i < 3; ++i)
+      if (out_strides[i] < 0 || out_strides[i] % 8)
+        return fail(DMC_ERR_INVALID_ARG, "out strides must be non-negative multiples of 8");
+  }
+  const dmc_cache_config &c = cache->cfg;
+  const dmc::Layout &L = cache->lay;
+  p.carry = at<float>(cache, L.pf_carry);
+  dmc::PromptParams a{};
+  a.pool = p.pool;
+  a.page_bytes = p.page_bytes;
+  a.ptab = p.ptab;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  for (int i = 0; i < 3; ++i) {
+    a.qs[i] = p.qs[i];
+    a.ks[i] = p.ks[i];
+    a.vs[i] = p.vs[i];
+    a.os[i] = n > 0 ? out_strides[i] : 0;
+  }
+  a.out = out;
+  a.prompt_lens = prompt_lens;
+  a.alpha = p.alpha;
+  a.omega = p.omega;
+  a.count = p.count;
+  a.page_base = p.page_base;
+  a.carry = p.carry;
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(c.head_dim)));
+  a.n = n;
+  a.units = L.units;
+  a.hkv = c.num_kv_heads;
+  a.hq = c.num_q_heads;
+  a.maxpages = L.maxpages;
+  a.log2p = p.log2p;
+  a.max_prompt = L.max_prompt;
+  a.prompt_chunks = L.prompt_chunks;
+  a.carry_blocks = L.carry_blocks;
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, L.v_trans, p, s);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  e = dmc::launch_prompt_attend(elem_bytes(c), c.head_dim, L.group, L.v_trans, a, s);
+  if (e != hipSuccess) return hip_fail(e, "prompt attention launch");
   return DMC_OK;
 }
 

@@ -29,7 +29,8 @@ struct Control {
 
 // Byte offsets of the workspace sections (all 256-byte aligned).
 struct Layout {
-  size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_pagebase;
+  size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_pagebase,
+      pf_carry;
   size_t total;
   int64_t page_bytes;     // 2 * P * d * elem_bytes (K rows, then V rows)
   int32_t units;          // B * Hkv per layer
@@ -39,6 +40,7 @@ struct Layout {
   int64_t max_records;    // decode partial records: ranges + units
   int32_t max_prompt;     // prefill staging capacity (tokens)
   int32_t prompt_chunks;  // ceil(max_prompt / 64)
+  int32_t carry_blocks;   // ceil(max_prompt / 32)
   bool v_trans;           // value pages stored transposed (matrix-core decode)
 };
 
@@ -78,8 +80,35 @@ struct PrefillParams {
   float *omega;            // [U, max_prompt]
   int32_t *count;          // [U, prompt_chunks]
   int32_t *page_base;      // [U]
+  float *carry;            // optional [U, carry_blocks, carry_stride]: open-segment sums at
+                           // every 32-token boundary inside a segment (prompt attention)
   float c;
-  int32_t n, units, hkv, hq, maxpages, log2p, omega_src, max_prompt, prompt_chunks;
+  int32_t n, units, hkv, hq, maxpages, log2p, omega_src, max_prompt, prompt_chunks,
+      carry_blocks;
+};
+
+// Floats per carry record: sum of omega * k (d), sum of omega * v (d), sum of
+// omega, padding to 16 bytes.
+__host__ __device__ constexpr inline int carry_stride(int head_dim) { return 2 * head_dim + 4; }
+
+// Prompt-phase attention over a freshly compacted layer (after the prefill
+// passes have run with carry records enabled).
+struct PromptParams {
+  const char *pool;
+  int64_t page_bytes;
+  const int32_t *ptab;     // [U, maxpages] of this layer
+  const void *q, *k, *v;
+  int64_t qs[3], ks[3], vs[3];   // element strides of (batch, token, head); d contiguous
+  void *out;
+  int64_t os[3];
+  const int32_t *prompt_lens;
+  const uint8_t *alpha;    // [U, max_prompt] decisions (1 = accumulate; 1 past the prompt)
+  const float *omega;      // [U, max_prompt]
+  const int32_t *count;    // [U, prompt_chunks] segment starts per 64-token chunk
+  const int32_t *page_base;  // [U]; < 0 when the layer's allocation failed
+  const float *carry;      // [U, carry_blocks, carry_stride(d)]
+  float scale_log2;        // log2(e) / sqrt(d)
+  int32_t n, units, hkv, hq, maxpages, log2p, max_prompt, prompt_chunks, carry_blocks;
 };
 
 struct DenseParams {
@@ -110,6 +139,10 @@ hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillPa
                           hipStream_t s);
 hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
+
+// Prompt-phase attention; bf16 runs on matrix cores, fp32 on the vector ALUs.
+hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
+                                const PromptParams &p, hipStream_t s);
 
 // Dynamic LDS bytes of the decode kernel for a unit count / group / head dim.
 size_t decode_lds_bytes(int units, int group, int head_dim);

@@ -17,13 +17,11 @@
 // Decode = one fused launch per layer (Algorithm 1 update + split-K
 // attention, balanced by actual compressed length) plus a small combine
 // launch for units split over several pieces.
-#include "dmc_internal.h"
+#include "dmc_device.h"
 
 namespace dmc {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 32;  // max rows of a matrix-core chunk
 #ifndef DMC_VALU_CHUNK
 #define DMC_VALU_CHUNK 16
@@ -33,145 +31,6 @@ constexpr int kChunk = 32;  // max rows of a matrix-core chunk
 #endif
 constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
 constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
-
-__device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// fp32 -> bf16 bits, round to nearest even (quiet NaN preserved).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) | 0x40u) & 0xffffu;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
-template <int ES>
-__device__ __forceinline__ float load_elem(const void *base, int64_t idx);
-template <>
-__device__ __forceinline__ float load_elem<2>(const void *base, int64_t idx) {
-  return __uint_as_float(uint32_t(static_cast<const uint16_t *>(base)[idx]) << 16);
-}
-template <>
-__device__ __forceinline__ float load_elem<4>(const void *base, int64_t idx) {
-  return static_cast<const float *>(base)[idx];
-}
-
-// 16-byte vector <-> floats.
-template <int ES>
-struct V16;
-template <>
-struct V16<2> {
-  static constexpr int N = 8;
-  __device__ static __forceinline__ void unpack(const uint4 &r, float *f) {
-    f[0] = bf16_lo(r.x); f[1] = bf16_hi(r.x); f[2] = bf16_lo(r.y); f[3] = bf16_hi(r.y);
-    f[4] = bf16_lo(r.z); f[5] = bf16_hi(r.z); f[6] = bf16_lo(r.w); f[7] = bf16_hi(r.w);
-  }
-  // Round to storage; f is replaced by the widened stored values.
-  __device__ static __forceinline__ uint4 pack(float *f) {
-    uint32_t h[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      h[i] = bf16_bits(f[i]);
-      f[i] = __uint_as_float(h[i] << 16);
-    }
-    return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                      h[6] | (h[7] << 16));
-  }
-};
-template <>
-struct V16<4> {
-  static constexpr int N = 4;
-  __device__ static __forceinline__ void unpack(const uint4 &r, float *f) {
-    f[0] = __uint_as_float(r.x); f[1] = __uint_as_float(r.y);
-    f[2] = __uint_as_float(r.z); f[3] = __uint_as_float(r.w);
-  }
-  __device__ static __forceinline__ uint4 pack(float *f) {
-    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
-                      __float_as_uint(f[3]));
-  }
-};
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-
-// One lane's slice of a query head (16 bytes of it) with q[0] zeroed, and
-// its dot product with the matching 16-byte slice of a key row.  bf16 keeps
-// the query packed and uses v_dot2_f32_bf16 (products exact in fp32, fp32
-// accumulation); fp32 uses plain FMAs.
-template <int ES>
-struct QSlice;
-template <>
-struct QSlice<2> {
-  uint4 w;
-  __device__ __forceinline__ void load(const char *p, bool first) {
-    w = *reinterpret_cast<const uint4 *>(p);
-    if (first) w.x &= 0xffff0000u;
-  }
-  __device__ __forceinline__ float dot(const uint4 &k) const {
-    float d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.x),
-                                              __builtin_bit_cast(bf16x2_t, k.x), 0.0f, false);
-    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.y),
-                                        __builtin_bit_cast(bf16x2_t, k.y), d, false);
-    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.z),
-                                        __builtin_bit_cast(bf16x2_t, k.z), d, false);
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w.w),
-                                           __builtin_bit_cast(bf16x2_t, k.w), d, false);
-  }
-};
-template <>
-struct QSlice<4> {
-  float f[4];
-  __device__ __forceinline__ void load(const char *p, bool first) {
-    const uint4 r = *reinterpret_cast<const uint4 *>(p);
-    V16<4>::unpack(r, f);
-    if (first) f[0] = 0.0f;
-  }
-  __device__ __forceinline__ float dot(const uint4 &k) const {
-    float kf[4];
-    V16<4>::unpack(k, kf);
-    float d = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) d = fmaf(f[e], kf[e], d);
-    return d;
-  }
-};
-
-__device__ __forceinline__ uint4 ld16(const char *p) { return *reinterpret_cast<const uint4 *>(p); }
-__device__ __forceinline__ void st16(char *p, const uint4 &v) { *reinterpret_cast<uint4 *>(p) = v; }
-
-// E consecutive elements (E = 1 or 2) <-> floats, for the prefill/combine paths.
-// (One memory access each; p is aligned to E * ES bytes.)
-template <int ES, int E>
-__device__ __forceinline__ void load_e(const char *p, float *f) {
-  if constexpr (ES == 2 && E == 2) {
-    const uint32_t w = *reinterpret_cast<const uint32_t *>(p);
-    f[0] = __uint_as_float(w << 16);
-    f[1] = __uint_as_float(w & 0xffff0000u);
-  } else if constexpr (ES == 4 && E == 2) {
-    const float2 w = *reinterpret_cast<const float2 *>(p);
-    f[0] = w.x;
-    f[1] = w.y;
-  } else {
-    f[0] = load_elem<ES>(p, 0);
-  }
-}
-template <int ES, int E>
-__device__ __forceinline__ void store_e(char *p, const float *f) {
-  if constexpr (ES == 2 && E == 2) {
-    *reinterpret_cast<uint32_t *>(p) = bf16_bits(f[0]) | (bf16_bits(f[1]) << 16);
-  } else if constexpr (ES == 4 && E == 2) {
-    *reinterpret_cast<float2 *>(p) = make_float2(f[0], f[1]);
-  } else if constexpr (ES == 2) {
-    *reinterpret_cast<uint16_t *>(p) = static_cast<uint16_t>(bf16_bits(f[0]));
-  } else {
-    *reinterpret_cast<float *>(p) = f[0];
-  }
-}
-
-__device__ __forceinline__ float sigmoid_floor(float x) {
-  // omega = sigmoid(x), floored at 2^-100 so a running sum never reaches 0.
-  return fmaxf(1.0f / (1.0f + expf(-x)), 0x1p-100f);
-}
 
 
 
@@ -192,21 +51,6 @@ __device__ __forceinline__ float sigmoid_floor(float x) {
 // built (the page allocator's bump counter aside).
 // ---------------------------------------------------------------------------
 
-// Reduction over the LPR lanes of a row group (lanes are grouped in runs of
-// LPR); every lane of the group receives the sum.
-template <int LPR>
-__device__ __forceinline__ float row_sum(float x) {
-  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "row width");
-  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
-  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
-  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x141, 0xF, 0xF, false));  // row_half_mirror
-  if (LPR >= 16)
-    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x140, 0xF, 0xF, false));  // row_mirror
-  if (LPR >= 32) x += __shfl_xor(x, 16, 64);
-  return x;
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Merge (m2, l2, a2) into (m, l, a); scores are in the log2 domain.
 template <int N>
@@ -221,13 +65,6 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float *a, float 
   m = mn;
 }
 
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-// Streaming 16-byte load of cache data that is read once per step.
-__device__ __forceinline__ uint4 ld16_stream(const char *p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
 
 // Slot space of a layer: unit u owns positions [off_u, off_u + n_u) with
 // n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
@@ -601,18 +438,6 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
 // 16-byte load.  P enters the value product rounded to bf16; its row sum is
 // taken over the same rounded values.
 // ---------------------------------------------------------------------------
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f32x4_t mfma_16x16x32(const uint4 &a, const uint4 &b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-}
-
-__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
-  return bf16_bits(lo) | (bf16_bits(hi) << 16);
-}
-
 template <int D, int G>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
@@ -1149,7 +974,10 @@ __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *
 // the last segment continues.  Each token is read exactly once.  Tokens are
 // streamed in fixed batches whatever the segment lengths; a segment is
 // flushed (slot written) when the next one starts.  The wave that writes
-// the first slot of a page also writes its page-table entry.
+// the first slot of a page also writes its page-table entry.  With carry
+// records enabled, the running sums of a segment that crosses a 32-token
+// boundary t (t not a segment start) are stored as they stand before t:
+// the prompt-attention pass resumes a segment's running mean from there.
 template <int ES, int D>
 __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams p) {
   constexpr int E = D / 64;  // elements per lane
@@ -1227,12 +1055,21 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
       if (j < cnt) {
         const int tj = t2 + j;
         const int rel = tj - tlo;
-        if (tj != t0 && rel < 64 && ((m0 >> rel) & 1ull)) {   // a new segment opens
+        const bool opens = tj != t0 && rel < 64 && ((m0 >> rel) & 1ull);
+        if (opens) {   // a new segment opens
           flush();
           ++s;
           zs = 0.0f;
 #pragma unroll
           for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+        } else if (p.carry && tj != t0 && (tj & 31) == 0) {
+          float *cr = p.carry + (int64_t(u) * p.carry_blocks + (tj >> 5)) * carry_stride(D);
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            cr[lane * E + e] = ak[e];
+            cr[D + lane * E + e] = av[e];
+          }
+          if (lane == 0) cr[2 * D] = zs;
         }
 #pragma unroll
         for (int e = 0; e < E; ++e) {

@@ -25,3 +25,13 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    """torch with a visible GPU and the built HIP library (fails loudly if
+    libdmc.so is missing)."""
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2403_09636_amd  # noqa: F401
+    return torch

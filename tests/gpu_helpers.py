@@ -88,6 +88,21 @@ class Pair:
         got = slot.cpu().numpy()
         assert (got == s_ref).all(), "prefill slot index mismatch"
 
+    def prefill_attend(self, layer, k, v, q, prompt_lens=None, out=None):
+        """Prompt attention on both sides: slot indices bit-exact, outputs
+        (zeros past each row's prompt length) within tolerance."""
+        import torch
+        B, n = k.shape[:2]
+        slot = torch.full((B, self.Hkv, n), -7, dtype=torch.int32, device=k.device)
+        lens_t = None if prompt_lens is None else torch.as_tensor(
+            prompt_lens, dtype=torch.int32, device=k.device)
+        out = self.gpu.prefill_attend(layer, k, v, q, out=out, prompt_lens=lens_t, slot_index=slot)
+        o_ref, s_ref = self.orc.prefill_attend(layer, f64(q), f64(k), f64(v),
+                                               prompt_lens=prompt_lens)
+        got = slot.cpu().numpy()
+        assert (got == s_ref).all(), "prompt slot index mismatch"
+        return assert_close(f64(out), o_ref, self.dtype, "prompt attention output")
+
     def compare_cache(self, layer):
         """Lengths bit-exact; slots and z within tolerance."""
         K_ref, V_ref, l_ref, z_ref = self.orc.export(layer)

@@ -366,7 +366,37 @@ def check_prefill_matches_decode(O):
             _close(V2[b, g, :l2[b, g]], V1[0, 0, :l1[0, 0]], tol=0.0, what="prefill V")
 
 
+def check_prefill_attend(O):
+    """Prompt-phase attention equals token-by-token decode steps and the
+    unrolled states with the additive mask of Sec. 3.2, per unit; ragged
+    prompt lengths leave zero outputs past each row's end."""
+    rng = np.random.default_rng(37)
+    B, Hkv, G, d, n = 3, 2, 2, 4, 9
+    Hq = Hkv * G
+    q = rng.standard_normal((B, n, Hq, d))
+    k = rng.standard_normal((B, n, Hkv, d))
+    v = rng.standard_normal((B, n, Hkv, d))
+    lens = np.array([9, 4, 0])
+    orc = O.DMCOracle(1, B, Hq, Hkv, d, max_slots=n)
+    out, slots = orc.prefill_attend(0, q, k, v, prompt_lens=lens)
+    for b in range(B):
+        assert (out[b, lens[b]:] == 0).all()
+        for g in range(Hkv):
+            m = lens[b]
+            if m == 0:
+                assert (slots[b, g] == -1).all()
+                continue
+            kk = k[b, :m, g].copy()
+            alpha = (kk[:, 0] > 0).astype(int)
+            alpha[0] = 0
+            kk[:, 0] = 0.0
+            omega = 1.0 / (1.0 + np.exp(-q[b, :m, g * G, 0]))
+            ref = unrolled_attention(kk, v[b, :m, g], omega, alpha, q[b, :m, g * G:(g + 1) * G])
+            _close(out[b, :m, g * G:(g + 1) * G], ref, tol=1e-10, what=f"prefill attend {(b, g)}")
+            assert slots[b, g, :m].tolist() == (np.cumsum(1 - alpha) - 1).tolist()
+
+
 ALL_CHECKS = [check_worked_example, check_sigmoid_c5, check_exact_decisions,
               check_all_append_vanilla, check_all_accumulate, check_segments,
               check_avg_pool, check_bruteforce_unrolled, check_gqa_omega,
-              check_permutation, check_prefill_matches_decode]
+              check_permutation, check_prefill_matches_decode, check_prefill_attend]

@@ -105,6 +105,8 @@ def test_entry_points_reject_null_cache(P):
         "dmc_decode_step": lambda: lib.dmc_decode_step(None, 0, None, None, None, None, None, None),
         "dmc_prefill_compress": lambda: lib.dmc_prefill_compress(None, 0, None, s, None, s, None,
                                                                  s, 0, None, None, None),
+        "dmc_prefill_attend": lambda: lib.dmc_prefill_attend(None, 0, None, s, None, s, None, s,
+                                                             0, None, None, s, None, None),
         "dmc_cache_lengths": lambda: lib.dmc_cache_lengths(None, 0, None, None),
         "dmc_cache_export": lambda: lib.dmc_cache_export(None, 0, None, None, 0, None, None),
         "dmc_cache_import": lambda: lib.dmc_cache_import(None, 0, None, None, 0, None, None, None),

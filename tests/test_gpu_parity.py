@@ -14,12 +14,6 @@ from workloads import WORKLOADS, decision_logits, decode_inputs_np
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch_cuda():
-    import torch
-    assert torch.cuda.is_available()
-    import paper_2403_09636_amd  # noqa: F401  (fails loudly if libdmc.so is missing)
-    return torch
 
 
 def test_tiny_workload_full(torch_cuda):

@@ -1,0 +1,165 @@
+"""Prompt-phase attention (every prompt query attends to the closed
+segments' final states and its own segment's running mean) on the GPU
+against the float64 oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.gpu_helpers import Pair, assert_close, f64, log, random_step
+from workloads import decision_logits
+
+pytestmark = pytest.mark.gpu
+
+LENS = [0, 1, 31, 32, 33, 64, 65, 127, 128, 129, 200]
+
+
+def _inputs(rng, B, n, Hkv, G, d, crs, dtype, bias=0.0):
+    import torch
+    k = rng.standard_normal((B, n, Hkv, d), dtype=np.float32)
+    v = rng.standard_normal((B, n, Hkv, d), dtype=np.float32)
+    q = rng.standard_normal((B, n, Hkv * G, d), dtype=np.float32)
+    k[..., 0] = decision_logits(rng.uniform(size=(B, n, Hkv)), np.asarray(crs)[None, None], bias)
+    dt = torch.float32 if dtype == "fp32" else torch.bfloat16
+    return tuple(torch.from_numpy(x).to(dt).cuda() for x in (k, v, q))
+
+
+@pytest.mark.parametrize("dtype,d,G,page", [
+    ("bf16", 128, 1, 32), ("bf16", 128, 2, 32), ("bf16", 128, 4, 32), ("bf16", 128, 8, 32),
+    ("bf16", 64, 1, 16), ("bf16", 64, 8, 64), ("bf16", 128, 4, 8), ("bf16", 128, 1, 128),
+    ("fp32", 64, 1, 32), ("fp32", 128, 2, 16), ("fp32", 64, 8, 32),
+])
+def test_prompt_attend_ragged(torch_cuda, dtype, d, G, page):
+    """Ragged prompt lengths around the 32/64/128-token boundaries, per-head
+    CR from always-append to (almost) never-append, then decode on the
+    resulting cache."""
+    log(f"case prompt dtype={dtype} d={d} G={G} page={page}")
+    n, Hkv = 200, 4
+    crs = [1.0, 3.0, 12.0, 1e9]
+    B = len(LENS)
+    rng = np.random.default_rng(100 + d + 10 * G + page)
+    pr = Pair(1, B, Hkv * G, Hkv, d, dtype, page_size=page, max_slots=n + 24, max_prompt_len=n)
+    k, v, q = _inputs(rng, B, n, Hkv, G, d, crs, dtype)
+    err = pr.prefill_attend(0, k, v, q, prompt_lens=LENS)
+    log(f"  max abs err {err:.3e}")
+    pr.compare_cache(0)
+    for _ in range(6):
+        pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, np.array(crs), dtype, "cuda"))
+    pr.compare_cache(0)
+    pr.ok()
+
+
+def test_prompt_attend_segments_across_tiles(torch_cuda):
+    """One unit never appends after token 0 (one open segment across every
+    32-token boundary), one always appends (plain causal attention), one
+    alternates in long runs; bias c = 1.5; group-mean omega."""
+    import torch
+    log("case prompt long segments")
+    B, n, Hkv, G, d = 2, 300, 3, 2, 128
+    rng = np.random.default_rng(77)
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=n, max_prompt_len=n, bias=1.5,
+              omega_src="group_mean")
+    k, v, q = _inputs(rng, B, n, Hkv, G, d, [1e12, 1.0, 1.0], "bf16", bias=1.5)
+    runs = (np.arange(n) // 45) % 2 == 0          # unit 2: 45-token runs of accumulate / append
+    k0 = np.where(runs, 4.0, -4.0).astype(np.float32)
+    k[:, :, 2, 0] = torch.from_numpy(k0).to(k.dtype).cuda()[None]
+    err = pr.prefill_attend(0, k, v, q)
+    log(f"  max abs err {err:.3e}")
+    assert pr.gpu.lengths(0).cpu().numpy()[:, 0].tolist() == [1, 1]
+    pr.compare_cache(0)
+    pr.ok()
+
+
+def test_prompt_attend_all_append_is_causal_attention(torch_cuda):
+    """With every token appending, prompt attention is ordinary causal
+    attention over dims 1..d-1 (checked against torch on the CPU in float32)."""
+    import torch
+    import torch.nn.functional as F
+    log("case prompt all-append")
+    B, n, Hkv, G, d = 2, 150, 2, 4, 64
+    rng = np.random.default_rng(9)
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=n, max_prompt_len=n)
+    k, v, q = _inputs(rng, B, n, Hkv, G, d, [1.0, 1.0], "bf16")
+    out = pr.gpu.prefill_attend(0, k, v, q)
+    kk = f64(k)[..., 1:].repeat(G, axis=2).transpose(0, 2, 1, 3)   # [B, Hq, n, d-1]
+    vv = f64(v).repeat(G, axis=2).transpose(0, 2, 1, 3)
+    qq = f64(q)[..., 1:].transpose(0, 2, 1, 3)
+    ref = F.scaled_dot_product_attention(torch.from_numpy(qq).float(), torch.from_numpy(kk).float(),
+                                         torch.from_numpy(vv).float(), is_causal=True,
+                                         scale=1.0 / np.sqrt(d))
+    assert_close(f64(out), ref.numpy().transpose(0, 2, 1, 3), "bf16", "causal attention")
+    pr.ok()
+
+
+def test_prompt_attend_strided(torch_cuda):
+    """k, v, q and out through non-contiguous (B, n, H) strides; out rows of
+    other heads untouched."""
+    import torch
+    log("case prompt strided")
+    B, n, Hkv, G, d = 2, 96, 2, 2, 128
+    rng = np.random.default_rng(21)
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=n, max_prompt_len=n)
+    k, v, q = _inputs(rng, B, n, Hkv, G, d, [2.0, 5.0], "bf16")
+    ks = k.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    vs = torch.empty((n, B, Hkv, d), dtype=v.dtype, device="cuda")
+    vs.copy_(v.permute(1, 0, 2, 3))
+    vs = vs.permute(1, 0, 2, 3)
+    qs = torch.empty((B, Hkv * G, n, d), dtype=q.dtype, device="cuda")
+    qs.copy_(q.permute(0, 2, 1, 3))
+    qs = qs.permute(0, 2, 1, 3)
+    big = torch.full((B, n, 2 * Hkv * G, d), 7.0, dtype=q.dtype, device="cuda")
+    out = big[:, :, ::2]                                   # head stride 2 * d
+    err = pr.prefill_attend(0, ks, vs, qs, out=out)
+    log(f"  max abs err {err:.3e}")
+    assert (big[:, :, 1::2] == 7.0).all()
+    pr.ok()
+
+
+def test_prompt_attend_empty_and_single(torch_cuda):
+    """n = 0 writes nothing; n = 1 returns each token's own value."""
+    import torch
+    log("case prompt empty / single")
+    pr = Pair(1, 2, 4, 2, 64, "bf16", max_slots=16, max_prompt_len=8)
+    z = torch.empty((2, 0, 2, 64), dtype=torch.bfloat16, device="cuda")
+    zq = torch.empty((2, 0, 4, 64), dtype=torch.bfloat16, device="cuda")
+    pr.gpu.prefill_attend(0, z, z, zq, n=0)
+    assert (pr.gpu.lengths(0).cpu().numpy() == 0).all()
+    rng = np.random.default_rng(4)
+    k, v, q = _inputs(rng, 2, 1, 2, 2, 64, [2.0, 2.0], "bf16")
+    pr.gpu.reset()
+    out = pr.gpu.prefill_attend(0, k, v, q)
+    want = f64(v).repeat(2, axis=2)
+    assert_close(f64(out), want, "bf16", "single token")
+    pr.ok()
+
+
+def test_prompt_attend_sampled_7b_layer(torch_cuda):
+    """Llama-2-7B layer shape (B=2, n=4096, 32 heads, d=128, CR per head in
+    {1, 2, 4, 8}) -- every output row of 6 sampled units against a per-unit
+    oracle, and every unit's slot indices against the oracle's decisions."""
+    import torch
+    import workloads as W
+    log("case prompt 7b layer sampled")
+    w = W.scaled(W.WORKLOADS["llama7b_layer"], batch=2)
+    k, v, q = W.prompt_full_torch(w, 0, "cuda")
+    import paper_2403_09636_amd as P
+    cfg = P.make_config(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                        w.page_size, w.prompt_len + 8, max_prompt_len=w.prompt_len)
+    cache = P.DMCCache(cfg, device="cuda")
+    n = w.prompt_len
+    slot = torch.empty((w.batch, w.num_kv_heads, n), dtype=torch.int32, device="cuda")
+    out = cache.prefill_attend(0, k, v, q, slot_index=slot)
+    torch.cuda.synchronize()
+    cache.check()
+    k0 = f64(k[..., 0])                                   # [B, n, Hkv]
+    alpha = oracle.decision(k0, 0.0)
+    alpha[:, 0] = 0
+    want_slots = np.cumsum(1 - alpha, axis=1) - 1
+    assert (slot.cpu().numpy() == want_slots.transpose(0, 2, 1)).all()
+    rng = np.random.default_rng(0)
+    units = [(0, 0), (1, 31)] + [(int(rng.integers(2)), int(rng.integers(32))) for _ in range(4)]
+    for b, g in units:
+        orc = oracle.DMCOracle(1, 1, 1, 1, w.head_dim, max_slots=n)
+        o_ref, _ = orc.prefill_attend(0, f64(q[b:b + 1, :, g:g + 1]), f64(k[b:b + 1, :, g:g + 1]),
+                                      f64(v[b:b + 1, :, g:g + 1]))
+        err = assert_close(f64(out[b, :, g]), o_ref[0, :, 0], "bf16", f"unit {(b, g)}")
+        log(f"  unit {(b, g)} max abs err {err:.3e}")

@@ -19,14 +19,6 @@ from workloads import (WORKLOADS, decode_inputs_torch, pool_pages, precompressed
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch_cuda():
-    import torch
-    assert torch.cuda.is_available()
-    import paper_2403_09636_amd  # noqa: F401
-    return torch
-
-
 def _cache_for(w, steps, pages):
     import paper_2403_09636_amd as P
     cfg = P.make_config(w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,

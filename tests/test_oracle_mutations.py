@@ -34,6 +34,8 @@ MUTATIONS = {
                               "slot = np.where(active, self.l, -1)"),
     "prefill_ignores_lens": ("active = np.repeat(t < lens, self.Hkv)",
                              "active = np.repeat(t < n, self.Hkv)"),
+    "prefill_attend_ignores_lens": ("active = np.repeat(lens > t, self.Hkv)",
+                                    "active = np.repeat(n > t, self.Hkv)"),
 }
 
 

@@ -321,6 +321,23 @@ def prompt_torch(w: Workload, layer: int, device, bias: float = 0.0, n: int | No
     return k, v, q0
 
 
+def prompt_full_torch(w: Workload, layer: int, device, bias: float = 0.0, n: int | None = None):
+    """Prompt inputs with whole query rows (for prompt-phase attention):
+    k, v [B, n, Hkv, d] and q [B, n, Hq, d], all N(0, 1), k[..., 0] from the
+    decision logits of each (layer, kv head)."""
+    g = _gen(w, PROMPT_STREAM, layer, device)
+    import torch
+    n = w.prompt_len if n is None else n
+    B, Hq, Hkv, d = w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim
+    dt = _torch_dtype(w)
+    k = _randn_rows((B, n, Hkv, d), g, device, dt)
+    v = _randn_rows((B, n, Hkv, d), g, device, dt)
+    q = _randn_rows((B, n, Hq, d), g, device, dt)
+    u = torch.rand((B, n, Hkv), generator=g, device=device)
+    k[..., 0] = _torch_logits(u, effective_crs(w)[layer][None, None, :], bias).to(dt)
+    return k, v, q
+
+
 def precompressed_torch(w: Workload, layer: int, device):
     """A pre-compressed cache for one layer (inputs to the cache import).
 
