@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--split-tile", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--prompt", action="store_true",
+                    help="measure prompt-phase attention (dmc_prefill_attend) instead of decode")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
     ap.add_argument("--calib-copy", action="store_true",
                     help="finish with plain 1 GiB device copies (counter calibration)")
     return ap.parse_args()
@@ -118,6 +121,80 @@ def cpu_baseline(w, lens_layers, seconds):
                       f"1 / (mean unit-step time x {L} layers x {H} kv heads)"}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_prompt(args):
+    """Prompt phase of one layer with attention outputs (dmc_prefill_attend):
+    compaction passes + the prompt-attention kernel, timed per call with HIP
+    events on the launch stream (the cache is emptied between calls, outside
+    the timed region).  Algorithmic flops: 4 d per (query head, visible
+    state), visible states of token t = slot(t) closed slots + its open one."""
+    import torch
+
+    import paper_2403_09636_amd as P
+    import workloads as W
+
+    w = W.WORKLOADS[args.workload if args.workload != "llama7b_stack" else "llama7b_layer"]
+    if args.batch:
+        w = W.scaled(w, batch=args.batch)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n = w.prompt_len
+    cfg = P.make_config(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                        w.page_size, n, None, 0.0, "lead", 0, n)
+    cache = P.DMCCache(cfg, device=dev)
+    k, v, q = W.prompt_full_torch(w, 0, dev)
+    out = torch.empty_like(q)
+    slot = torch.empty((w.batch, w.num_kv_heads, n), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        ms = []
+        for _ in range(reps):
+            cache.reset()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return ms
+
+    attend = lambda: cache.prefill_attend(0, k, v, q, out=out, slot_index=slot)  # noqa: E731
+    compress = lambda: cache.prefill(0, k, v, q)  # noqa: E731
+    timed(attend, args.warmup)
+    ms_attend = timed(attend, args.steps)
+    timed(compress, 2)
+    ms_compress = timed(compress, args.steps)
+    cache.check()
+    seg = slot.to(torch.int64)
+    visible = int((seg + 1).sum().item())              # per kv unit, summed over tokens
+    flops = 4.0 * w.head_dim * w.group * visible
+    t_att = float(np.median(ms_attend))
+    t_cmp = float(np.median(ms_compress))
+    t_kernel = max(t_att - t_cmp, 1e-6)
+    lens = cache.lengths(0).cpu().numpy()
+    res = {
+        "metric": f"prompt tokens/s (DMC prefill with attention), {w.name}",
+        "value": round(w.batch * n / (t_att * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_att, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": 1, "batch": w.batch, "q_heads": w.num_q_heads,
+                   "kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "prompt": n,
+                   "page_size": w.page_size,
+                   "global_cr": round(float(n * lens.size / lens.sum()), 3)},
+        "roofline": {"bound": "mfma", "achieved": round(flops / (t_kernel * 1e-3) / 1e12, 1),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(flops / (t_kernel * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": "prompt_mfma_kernel (attend - compress time)",
+                     "alg_flops_per_launch": int(flops), "avg_launch_us": round(t_kernel * 1e3, 1)},
+        "compress_ms": round(t_cmp, 4),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -125,6 +202,9 @@ def main():
               "the decode path shards by kv head or by sequence, see the design notes",
               file=sys.stderr)
         sys.exit(2)
+    if args.prompt:
+        bench_prompt(args)
+        return
 
     import torch
 

@@ -412,6 +412,9 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer, const void *k,
   }
   const dmc_cache_config &c = cache->cfg;
   const dmc::Layout &L = cache->lay;
+  if (c.dtype == DMC_BF16 && (int64_t(n) + c.page_size - 1) / c.page_size > dmc::kPromptMaxPages)
+    return fail(DMC_ERR_UNSUPPORTED, "prompt of %d tokens exceeds %d pages per unit", n,
+                dmc::kPromptMaxPages);
   p.carry = at<float>(cache, L.pf_carry);
   dmc::PromptParams a{};
   a.pool = p.pool;
@@ -448,7 +451,7 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer, const void *k,
   const hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = dmc::launch_prefill(elem_bytes(c), c.head_dim, L.v_trans, p, s);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
-  e = dmc::launch_prompt_attend(elem_bytes(c), c.head_dim, L.group, L.v_trans, a, s);
+  e = dmc::launch_prompt_attend(elem_bytes(c), c.head_dim, L.group, L.v_trans, a, p.ctrl, s);
   if (e != hipSuccess) return hip_fail(e, "prompt attention launch");
   return DMC_OK;
 }

@@ -140,9 +140,15 @@ hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillPa
 hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 
-// Prompt-phase attention; bf16 runs on matrix cores, fp32 on the vector ALUs.
+// Largest prompt, in pages per unit, of the matrix-core prompt attention
+// (its page-table slice is held in LDS).
+constexpr int kPromptMaxPages = 1024;
+
+// Prompt-phase attention; bf16 runs on matrix cores (value pages of caches
+// stored as rows are transposed in place around it, over the pages of the
+// last allocation named in ctrl), fp32 on the vector ALUs.
 hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
-                                const PromptParams &p, hipStream_t s);
+                                const PromptParams &p, const Control *ctrl, hipStream_t s);
 
 // Dynamic LDS bytes of the decode kernel for a unit count / group / head dim.
 size_t decode_lds_bytes(int units, int group, int head_dim);

@@ -130,35 +130,95 @@ __device__ __forceinline__ void walk_open_state(const PromptParams &p, int u, in
 // bf16 on matrix cores.  One workgroup = 4 waves = one unit's 128 query
 // columns (token-major: column c is token c / G, head c % G of the group);
 // each wave owns 32 columns, T = 32 / G tokens.  The unit's closed slots
-// stream through LDS in blocks of 32 (keys row-major, values transposed),
-// shared by the 4 waves; per block and wave
+// stream through LDS in blocks of 32, shared by the 4 waves; per block and
+// wave
 //   S^T[slot][col]  = K[slot][:] . Q[col][:]          (A = K, B = Q^T)
 //   O^T[dim][col]  += V^T[dim][slot] P^T[slot][col]    (A = V^T, B = P^T)
 // on v_mfma_f32_16x16x32_bf16, with the interleaved key-row assignment of
 // the decode kernel (score tile sb, row m -> block slot 8(m/4) + 4 sb + m%4)
 // so that the score tile's output registers are already the P^T operand.
-// Workgroups are mapped so that all tiles of a unit run on one XCD (sharing
-// its L2), latest tiles (most slots) first.  P enters the value product
-// rounded to bf16 and its sum is taken over the rounded values.
+//
+// Blocks arrive by direct global -> LDS transfers (16 bytes per lane, no
+// registers) into a ring of kStages buffers, kStages - 1 blocks ahead of the
+// one being multiplied.  Key rows land XOR-swizzled in 16-byte units so that
+// each 16-lane group's operand loads hit distinct banks.  Value rows are
+// read transposed by ds_read_b64_tr_b16 (a 16-lane group pointing at four
+// 8-byte row pieces each of 4 rows receives, per lane, one column's 4
+// consecutive rows); caches that store value pages transposed ([d][P]) are
+// read as V^T rows directly.  Workgroups are mapped so that all tiles of a
+// unit run on one XCD (sharing its L2), latest tiles (most slots) first.  P
+// enters the value product rounded to bf16 and its sum is taken over the
+// rounded values.
 // ---------------------------------------------------------------------------
+#ifndef DMC_PROMPT_STAGES
+#define DMC_PROMPT_STAGES 3
+#endif
+constexpr int kStages = DMC_PROMPT_STAGES;
+constexpr int kPtabLds = kPromptMaxPages;   // page-table entries of a unit cached in LDS
+
+template <int CPR>
+__device__ __forceinline__ int k_swizzle(int row) {   // physical 16-byte chunk = logical ^ this
+  return ((row & 3) | (((row >> 3) & 3) << 2)) & (CPR - 1);
+}
+template <int CPR>
+__device__ __forceinline__ int v_swizzle(int row) { return (2 * (row & 3)) & (CPR - 1); }
+__device__ __forceinline__ int vt_swizzle(int dim) { return (dim >> 2) & 3; }
+
+__device__ __forceinline__ uint32_t lds_offset(const void *p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char *)p));
+}
+
+// 16 bytes per lane from global memory straight into LDS at
+// lds_base + 16 * lane (lds_base wave-uniform).  Issued as inline assembly so
+// that the compiler neither waits for it nor reorders LDS accesses around it;
+// completion is awaited with wait_vmcnt before the workgroup barrier.
+__device__ __forceinline__ void dma16(uint32_t lds_base, const void *g) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory");
+}
+
+// s_waitcnt with only the vector-memory count (at most N outstanding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+
+__device__ __forceinline__ uint2 ds_read_tr16(const void *p) {
+  const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4_t *)((__attribute__((address_space(3))) char *)p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// Two floats -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  typedef float f2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2_t{lo, hi}, b2_t));
+}
+
 template <int D, int G, bool VT>
 __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p, int ntiles) {
   constexpr int T = 32 / G;            // tokens per wave
   constexpr int TW = kWaves * T;       // tokens per workgroup
   constexpr int KS = D / 32, NT = D / 16, RB = D * 2;
-  constexpr int KRS = D + 8;           // LDS key row stride (bf16 elements)
-  constexpr int VTS = 40;              // LDS V^T row stride: 32 slots + 8 pad
-  constexpr int KBUF = 32 * KRS, VBUF = D * VTS;
-  constexpr int CPR = D / 8;           // 16-byte chunks per cache row
-  constexpr int CPT = 32 * CPR / kThreads;   // chunks per thread per block (keys or values)
-  constexpr int SBYTES = (2 * KBUF + 2 * VBUF) * 2;
+  constexpr int CPR = D / 8;           // 16-byte chunks per row
+  constexpr int BLK = 32 * RB;         // bytes of one block's keys (and of its values)
+  constexpr int DPW = BLK / 16 / kThreads;   // transfers per thread per block half
+  constexpr int SBYTES = kStages * 2 * BLK;
   constexpr int STAGE = 8 * 2 * D;     // floats per wave: 8 tokens x (key mean, value mean)
-  static_assert(kWaves * STAGE * 4 <= SBYTES, "open-state staging fits the block buffers");
-  static_assert(CPT >= 1 && (32 * CPR) % kThreads == 0, "block split");
+  static_assert(kWaves * STAGE * 4 <= SBYTES, "open-state staging fits the block ring");
+  static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
+  static_assert(kStages >= 2 && kStages <= 4, "ring depth");
   __shared__ __align__(16) unsigned char smem[SBYTES];
   __shared__ int s_hi[kWaves];
-  uint16_t *s_k = reinterpret_cast<uint16_t *>(smem);   // [2][32][KRS]
-  uint16_t *s_v = s_k + 2 * KBUF;                       // [2][D][VTS]
+  __shared__ int s_pt[kPtabLds];
 
   const int bid = blockIdx.x;
   const int xcd = bid & 7, r = bid >> 3;
@@ -166,7 +226,8 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   const int u = ul * 8 + xcd;
   if (u >= p.units) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n16 = lane & 15, q4 = lane >> 4;
   const int b = u / p.hkv, g = u - b * p.hkv;
   const int nb = clamp_prompt_len(p.prompt_lens, p.n, b);
@@ -206,9 +267,9 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
     for (int nt = 0; nt < NT; ++nt) acc[qb][nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
   // Open state of each column's token.  The walk stages key and value means
-  // of 8 tokens at a time (fp32, this wave's part of the block buffers);
-  // then every lane takes its columns' score (dot with its Q^T slice, summed
-  // over the 4 lane groups) and its slice of the value mean.
+  // of 8 tokens at a time (fp32, this wave's part of the block ring); then
+  // every lane takes its columns' score (dot with its Q^T slice, summed over
+  // the 4 lane groups) and its slice of the value mean.
   if (cnt > 0) {
     float *stage = reinterpret_cast<float *>(smem) + wave * STAGE;
     constexpr int E = D / 64;
@@ -281,134 +342,136 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   const int nblk = (s_top + 31) >> 5;
   const int P = 1 << p.log2p;
   const int64_t pt = int64_t(u) * p.maxpages;
-
-  // Block staging: keys row-major, values transposed, slots >= s_top zero.
-  uint4 rk[CPT], rv[CPT];
-  auto fetch = [&](int kb) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * kThreads;
-      const int row = c / CPR, c16 = c - row * CPR;
-      const int s = kb * 32 + row;
-      if (s < s_top) {
-        const char *pg = p.pool + int64_t(p.ptab[pt + (s >> p.log2p)]) * p.page_bytes;
-        rk[i] = ld16(pg + int64_t(s & (P - 1)) * RB + c16 * 16);
-        if (!VT) rv[i] = ld16(pg + int64_t(P) * RB + int64_t(s & (P - 1)) * RB + c16 * 16);
-      } else {
-        rk[i] = zero4;
-        if (!VT) rv[i] = zero4;
-      }
-      if (VT) {   // value page is [D][32]: chunk c = (dim, 8 slots)
-        const int dim = c >> 2, s8 = c & 3;
-        const int s0 = kb * 32 + 8 * s8;
-        if (s0 < s_top) {
-          const char *pg = p.pool + int64_t(p.ptab[pt + kb]) * p.page_bytes;
-          uint4 x = ld16(pg + int64_t(P) * RB + int64_t(dim) * 64 + s8 * 16);
-          const int keep = s_top - s0;   // slots s0 .. s0 + keep - 1 are valid
-          if (keep < 8) {
-            uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const uint32_t lo = 2 * e < keep ? 0x0000ffffu : 0u;
-              const uint32_t hi = 2 * e + 1 < keep ? 0xffff0000u : 0u;
-              w[e] &= lo | hi;
-            }
-            x = make_uint4(w[0], w[1], w[2], w[3]);
-          }
-          rv[i] = x;
-        } else {
-          rv[i] = zero4;
-        }
-      }
-    }
-  };
-  auto stash = [&](int buf) {
-    uint16_t *kd = s_k + buf * KBUF;
-    uint16_t *vd = s_v + buf * VBUF;
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * kThreads;
-      const int row = c / CPR, c16 = c - row * CPR;
-      *reinterpret_cast<uint4 *>(kd + row * KRS + c16 * 8) = rk[i];
-      if (VT) {
-        const int dim = c >> 2, s8 = c & 3;
-        *reinterpret_cast<uint4 *>(vd + dim * VTS + s8 * 8) = rv[i];
-      } else {
-        const uint32_t w[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          vd[(c16 * 8 + 2 * e) * VTS + row] = static_cast<uint16_t>(w[e] & 0xffffu);
-          vd[(c16 * 8 + 2 * e + 1) * VTS + row] = static_cast<uint16_t>(w[e] >> 16);
-        }
-      }
-    }
-  };
-
-  if (nblk > 0) {
-    fetch(0);
-    stash(0);
-  }
+  const int npg = min((s_top + P - 1) >> p.log2p, kPtabLds);
+  for (int i = tid; i < npg; i += kThreads) s_pt[i] = p.ptab[pt + i];
   __syncthreads();
+  // The host limits this kernel to prompts of at most kPtabLds pages per unit.
+  auto page_of = [&](int s) -> const char * {
+    return p.pool + int64_t(s_pt[s >> p.log2p]) * p.page_bytes;
+  };
+
+  // Transfers of block kb into ring slot st; rows past the closed slots read
+  // the last closed one (in bounds; masked or zeroed when used).
+  const uint32_t ring = lds_offset(smem);
+  auto issue = [&](int kb, int st) {
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const int run = i * kWaves + wave;   // 1 KB run of the block written by this instruction
+      const int c = run * 64 + lane;       // 16-byte chunk of the block
+      const uint32_t kdst = __builtin_amdgcn_readfirstlane(ring + st * 2 * BLK + run * 1024);
+      const int row = c / CPR, pc = c - row * CPR;
+      const int s = min(kb * 32 + row, s_top - 1);
+      const char *krow = page_of(s) + int64_t(s & (P - 1)) * RB;
+      dma16(kdst, krow + (pc ^ k_swizzle<CPR>(row)) * 16);
+      const char *gv;
+      if (VT) {   // value page [D][P]: chunk = (dim, 8 slots)
+        const int dim = c >> 2, lc = (c & 3) ^ vt_swizzle(dim);
+        const int s0 = min(kb * 32 + 8 * lc, (s_top - 1) & ~7);
+        gv = page_of(s0) + int64_t(P) * RB + (int64_t(dim) * P + (s0 & (P - 1))) * 2;
+      } else {
+        gv = krow + int64_t(P) * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
+      }
+      dma16(kdst + BLK, gv);
+    }
+  };
+
+  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
   const int krow0 = 8 * (n16 >> 2) + (n16 & 3);   // score tile 0 row of this lane (+4 in tile 1)
   for (int kb = 0; kb < nblk; ++kb) {
-    const int cur = kb & 1;
-    if (kb + 1 < nblk) fetch(kb + 1);
-    if (kb * 32 < wave_hi) {
-      const uint16_t *kd = s_k + cur * KBUF;
-      const uint16_t *vd = s_v + cur * VBUF;
-      f32x4_t sc[2][2];
+    // blocks issued after kb: min(nblk - 1 - kb, kStages - 2)
+    const int after = min(nblk - 1 - kb, kStages - 2);
+    if (after >= 2) wait_vmcnt<4 * DPW>();
+    else if (after == 1) wait_vmcnt<2 * DPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();   // block kb is in LDS for every wave; the ring slot of kb - 1 is free
+    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (kb + kStages - 1) % kStages);
+    if (kb * 32 >= wave_hi) continue;
+    const int st = kb % kStages;
+    const char *kd = reinterpret_cast<const char *>(smem) + st * 2 * BLK;
+    const char *vd = kd + BLK;
+    f32x4_t sc[2][2];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      uint4 ka[2];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        const int row = krow0 + 4 * sb;
+        ka[sb] = *reinterpret_cast<const uint4 *>(kd + row * RB +
+                                                  (((4 * ks + q4) ^ k_swizzle<CPR>(row)) * 16));
+      }
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = mfma_16x16x32(ka[sb], qop[qb][ks], sc[sb][qb]);
+    }
+    // V^T operands of the value product: lane (n16, q4) = dim 16 nt + n16, slots 8 q4 .. +8.
+    uint4 va[NT];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        uint4 ka[2];
+    for (int nt = 0; nt < NT; ++nt) {
+      if (VT) {
+        const int dim = 16 * nt + n16;
+        va[nt] = *reinterpret_cast<const uint4 *>(vd + dim * 64 + ((q4 ^ vt_swizzle(dim)) * 16));
+      } else {
+        uint2 h[2];
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-          ka[sb] = *reinterpret_cast<const uint4 *>(kd + (krow0 + 4 * sb) * KRS + ks * 32 + q4 * 8);
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = mfma_16x16x32(ka[sb], qop[qb][ks], sc[sb][qb]);
-      }
-      uint4 pb[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        float x[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int s = kb * 32 + 8 * q4 + j;
-          x[j] = s < lim[qb] ? sc[j >> 2][qb][j & 3] * p.scale_log2 : neg_inf();
+        for (int hh = 0; hh < 2; ++hh) {
+          const int row = 8 * q4 + 4 * hh + (n16 >> 2);
+          const int lc = 2 * nt + ((n16 & 3) >> 1);
+          h[hh] = ds_read_tr16(vd + row * RB + ((lc ^ v_swizzle<CPR>(row)) * 16) + (n16 & 1) * 8);
         }
-        float mx = x[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) mx = fmaxf(mx, x[j]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mn = fmaxf(m[qb], mx);
-        const float f = fast_exp2(m[qb] - mn);
-        m[qb] = mn;
-        ls[qb] *= f;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[qb][nt] *= f;
-        uint32_t pw[4];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          pw[w] = bf16_pair(fast_exp2(x[2 * w] - mn), fast_exp2(x[2 * w + 1] - mn));
-          ls[qb] += __uint_as_float(pw[w] << 16) + __uint_as_float(pw[w] & 0xffff0000u);
-        }
-        pb[qb] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
-      }
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const uint4 va = *reinterpret_cast<const uint4 *>(vd + (16 * nt + n16) * VTS + 8 * q4);
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) acc[qb][nt] = mfma_16x16x32(va, pb[qb], acc[qb][nt]);
+        va[nt] = make_uint4(h[0].x, h[0].y, h[1].x, h[1].y);
       }
     }
-    if (kb + 1 < nblk) stash(cur ^ 1);
-    __syncthreads();
+    const int keep = s_top - (kb * 32 + 8 * q4);   // this lane's slots below s_top
+    if (keep < 8) {
+      uint32_t msk[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        msk[w] = (2 * w < keep ? 0x0000ffffu : 0u) | (2 * w + 1 < keep ? 0xffff0000u : 0u);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        va[nt].x &= msk[0];
+        va[nt].y &= msk[1];
+        va[nt].z &= msk[2];
+        va[nt].w &= msk[3];
+      }
+    }
+    uint4 pb[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int s = kb * 32 + 8 * q4 + j;
+        x[j] = s < lim[qb] ? sc[j >> 2][qb][j & 3] * p.scale_log2 : neg_inf();
+      }
+      float mx = x[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) mx = fmaxf(mx, x[j]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(m[qb], mx);
+      const float f = fast_exp2(m[qb] - mn);
+      m[qb] = mn;
+      ls[qb] *= f;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[qb][nt] *= f;
+      uint32_t pw[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        pw[w] = cvt_pk_bf16(fast_exp2(x[2 * w] - mn), fast_exp2(x[2 * w + 1] - mn));
+        ls[qb] += __uint_as_float(pw[w] << 16) + __uint_as_float(pw[w] & 0xffff0000u);
+      }
+      pb[qb] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) acc[qb][nt] = mfma_16x16x32(va[nt], pb[qb], acc[qb][nt]);
   }
 
   // Normalise and store: lane holds dims 16 nt + 4 q4 .. +4 of its columns.
@@ -426,8 +489,8 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
                  (b * p.os[0] + int64_t(t) * p.os[1] + (g * G + h) * p.os[2]) * 2;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint32_t lo = bf16_pair(acc[qb][nt][0] * inv, acc[qb][nt][1] * inv);
-      const uint32_t hi = bf16_pair(acc[qb][nt][2] * inv, acc[qb][nt][3] * inv);
+      const uint32_t lo = cvt_pk_bf16(acc[qb][nt][0] * inv, acc[qb][nt][1] * inv);
+      const uint32_t hi = cvt_pk_bf16(acc[qb][nt][2] * inv, acc[qb][nt][3] * inv);
       *reinterpret_cast<uint2 *>(orow + (16 * nt + 4 * q4) * 2) = make_uint2(lo, hi);
     }
   }
@@ -580,7 +643,9 @@ hipError_t prompt_valu(const PromptParams &p, hipStream_t s) {
 }
 
 template <int ES, int D>
-hipError_t prompt_by_group(int group, bool vt, const PromptParams &p, hipStream_t s) {
+hipError_t prompt_by_group(int group, bool vt, const PromptParams &p, const Control *ctrl,
+                           hipStream_t s) {
+  (void)ctrl;
   if constexpr (ES == 2) {
     switch (group) {
       case 1: return prompt_mfma<D, 1>(p, vt, s);
@@ -604,13 +669,13 @@ hipError_t prompt_by_group(int group, bool vt, const PromptParams &p, hipStream_
 }  // namespace
 
 hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
-                                const PromptParams &p, hipStream_t s) {
+                                const PromptParams &p, const Control *ctrl, hipStream_t s) {
   if (p.n == 0) return hipSuccess;
   if (elem_bytes == 2)
-    return head_dim == 128 ? prompt_by_group<2, 128>(group, vt, p, s)
-                           : prompt_by_group<2, 64>(group, vt, p, s);
-  return head_dim == 128 ? prompt_by_group<4, 128>(group, vt, p, s)
-                         : prompt_by_group<4, 64>(group, vt, p, s);
+    return head_dim == 128 ? prompt_by_group<2, 128>(group, vt, p, ctrl, s)
+                           : prompt_by_group<2, 64>(group, vt, p, ctrl, s);
+  return head_dim == 128 ? prompt_by_group<4, 128>(group, vt, p, ctrl, s)
+                         : prompt_by_group<4, 64>(group, vt, p, ctrl, s);
 }
 
 }  // namespace dmc
