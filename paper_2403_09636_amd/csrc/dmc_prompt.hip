@@ -21,6 +21,8 @@
 // its score, sum = 1, accumulator = its value mean); the closed slots then
 // stream through with a per-query limit seg(i) (a staircase mask in slot
 // space).
+#include <type_traits>
+
 #include "dmc_device.h"
 
 namespace dmc {
@@ -131,38 +133,44 @@ __device__ __forceinline__ void walk_open_state(const PromptParams &p, int u, in
 // columns (token-major: column c is token c / G, head c % G of the group);
 // each wave owns 32 columns, T = 32 / G tokens.  The unit's closed slots
 // stream through LDS in blocks of 32, shared by the 4 waves; per block and
-// wave
+// wave, on v_mfma_f32_32x32x16_bf16 (lane l: column l % 32, half l / 32),
 //   S^T[slot][col]  = K[slot][:] . Q[col][:]          (A = K, B = Q^T)
 //   O^T[dim][col]  += V^T[dim][slot] P^T[slot][col]    (A = V^T, B = P^T)
-// on v_mfma_f32_16x16x32_bf16, with the interleaved key-row assignment of
-// the decode kernel (score tile sb, row m -> block slot 8(m/4) + 4 sb + m%4)
-// so that the score tile's output registers are already the P^T operand.
+// Score row m of a block is key slot pi(m) (bits 2 and 3 of m swapped):
+// then a lane's score registers 8 kk .. 8 kk + 7 are exactly its P^T
+// operand for value k-step kk (slots 16 kk + 8 half .. + 8).
 //
 // Blocks arrive by direct global -> LDS transfers (16 bytes per lane, no
 // registers) into a ring of kStages buffers, kStages - 1 blocks ahead of the
-// one being multiplied.  Key rows land XOR-swizzled in 16-byte units so that
-// each 16-lane group's operand loads hit distinct banks.  Value rows are
+// one being multiplied.  Rows land XOR-swizzled in 16-byte units so that the
+// operand loads of each 16-lane group hit distinct banks.  Value rows are
 // read transposed by ds_read_b64_tr_b16 (a 16-lane group pointing at four
-// 8-byte row pieces each of 4 rows receives, per lane, one column's 4
+// 8-byte row pieces of each of 4 rows receives, per lane, one column's 4
 // consecutive rows); caches that store value pages transposed ([d][P]) are
-// read as V^T rows directly.  Workgroups are mapped so that all tiles of a
-// unit run on one XCD (sharing its L2), latest tiles (most slots) first.  P
-// enters the value product rounded to bf16 and its sum is taken over the
-// rounded values.
+// read as V^T rows directly.  The softmax rescales the accumulators only
+// when some column's running maximum grows by more than 2^8 (probabilities
+// stay below 256, exact enough in bf16 and fp32).  Workgroups are mapped so
+// that all tiles of a unit run on one XCD (sharing its L2), latest tiles
+// (most slots) first.  P enters the value product rounded to bf16 and its
+// sum is taken over the rounded values.
 // ---------------------------------------------------------------------------
 #ifndef DMC_PROMPT_STAGES
 #define DMC_PROMPT_STAGES 3
 #endif
 constexpr int kStages = DMC_PROMPT_STAGES;
 constexpr int kPtabLds = kPromptMaxPages;   // page-table entries of a unit cached in LDS
+constexpr float kLazyRescale = 8.0f;        // log2 of the largest unnormalised probability
 
 template <int CPR>
-__device__ __forceinline__ int k_swizzle(int row) {   // physical 16-byte chunk = logical ^ this
-  return ((row & 3) | (((row >> 3) & 3) << 2)) & (CPR - 1);
-}
+__device__ __forceinline__ int k_swizzle(int row) { return row & (CPR - 1); }
 template <int CPR>
-__device__ __forceinline__ int v_swizzle(int row) { return (2 * (row & 3)) & (CPR - 1); }
+__device__ __forceinline__ int v_swizzle(int row) {
+  return CPR == 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
+}
 __device__ __forceinline__ int vt_swizzle(int dim) { return (dim >> 2) & 3; }
+__device__ __forceinline__ int score_slot(int m) {   // pi(m): bits 2 and 3 swapped
+  return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
 
 __device__ __forceinline__ uint32_t lds_offset(const void *p) {
   return static_cast<uint32_t>(
@@ -180,6 +188,14 @@ __device__ __forceinline__ void dma16(uint32_t lds_base, const void *g) {
                : "memory");
 }
 
+// Same, with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane offset.
+__device__ __forceinline__ void dma16_s(uint32_t lds_base, const char *sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory");
+}
+
 // s_waitcnt with only the vector-memory count (at most N outstanding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -189,11 +205,26 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ uint2 ds_read_tr16(const void *p) {
   const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
       (lds_bf16x4_t *)((__attribute__((address_space(3))) char *)p));
   return __builtin_bit_cast(uint2, v);
+}
+
+__device__ __forceinline__ f32x16_t mfma_32x32x16(const uint4 &a, const uint4 &b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Maximum of x over lanes l and l ^ 32 (v_permlane32_swap of x with itself
+// leaves each lane's value and its partner's in the two results).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                  __builtin_bit_cast(unsigned, x), false, false);
+  return fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
+               __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
 }
 
 // Two floats -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
@@ -203,11 +234,19 @@ __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2_t{lo, hi}, b2_t));
 }
 
+// Sum of a packed bf16 pair added to acc (exact products by 1, fp32 sum).
+__device__ __forceinline__ float add_pair(uint32_t pair, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pair),
+                                         __builtin_bit_cast(bf16x2_t, 0x3f803f80u), acc, false);
+}
+
 template <int D, int G, bool VT>
 __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p, int ntiles) {
   constexpr int T = 32 / G;            // tokens per wave
   constexpr int TW = kWaves * T;       // tokens per workgroup
-  constexpr int KS = D / 32, NT = D / 16, RB = D * 2;
+  constexpr int KS = D / 16;           // 16-dim k-steps of the score product
+  constexpr int NTL = D / 32;          // 32-dim tiles of the value product
+  constexpr int RB = D * 2;
   constexpr int CPR = D / 8;           // 16-byte chunks per row
   constexpr int BLK = 32 * RB;         // bytes of one block's keys (and of its values)
   constexpr int DPW = BLK / 16 / kThreads;   // transfers per thread per block half
@@ -228,7 +267,7 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n16 = lane & 15, q4 = lane >> 4;
+  const int col = lane & 31, hb = lane >> 5;   // MFMA column and half
   const int b = u / p.hkv, g = u - b * p.hkv;
   const int nb = clamp_prompt_len(p.prompt_lens, p.n, b);
   const bool ok = p.page_base[u] >= 0;
@@ -237,39 +276,33 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
   const int seg = cnt > 0 ? token_slots(p, u, a, cnt) : -1;
-  int lim[2], tok[2];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    tok[qb] = (16 * qb + n16) / G;
-    const int sj = __shfl(seg, tok[qb], 64);
-    lim[qb] = tok[qb] < cnt ? sj : 0;
-  }
-  const int wave_hi = cnt > 0 ? __shfl(seg, cnt - 1, 64) : 0;
+  const int tok = col / G, head = col - tok * G;
+  const bool colv = tok < cnt;
+  const int lim = colv ? __shfl(seg, tok, 64) : 0;
+  const int wave_hi = __builtin_amdgcn_readfirstlane(cnt > 0 ? __shfl(seg, cnt - 1, 64) : 0);
+  // every column of the wave sees slots < wave_lo (0 when some column is empty)
+  const int wave_lo = __builtin_amdgcn_readfirstlane(cnt == T ? __shfl(seg, 0, 64) : 0);
   if (lane == 0) s_hi[wave] = wave_hi;
 
-  // Q^T operand: lane (n16, q4) holds Q[col 16 qb + n16][32 ks + 8 q4 .. +8].
-  uint4 qop[2][KS];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int j = tok[qb], h = 16 * qb + n16 - j * G;
+  // Q^T operand: lane holds Q[col][16 ks + 8 hb .. + 8] (q[0] is not part of the score).
+  uint4 qop[KS];
+  {
     const char *qr = static_cast<const char *>(p.q) +
-                     (b * p.qs[0] + int64_t(a + j) * p.qs[1] + (g * G + h) * p.qs[2]) * 2;
+                     (b * p.qs[0] + int64_t(a + tok) * p.qs[1] + (g * G + head) * p.qs[2]) * 2;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qop[qb][ks] = j < cnt ? ld16(qr + ks * 64 + q4 * 16) : zero4;
-    if (q4 == 0) qop[qb][0].x &= 0xffff0000u;   // q[0] is not part of the score
+    for (int ks = 0; ks < KS; ++ks) qop[ks] = colv ? ld16(qr + ks * 32 + hb * 16) : zero4;
+    if (hb == 0) qop[0].x &= 0xffff0000u;
   }
 
-  float m[2] = {0.0f, 0.0f}, ls[2] = {0.0f, 0.0f};
-  f32x4_t acc[2][NT];
+  float m = 0.0f, ls = 0.0f;
+  f32x16_t acc[NTL];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[qb][nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int t = 0; t < NTL; ++t) acc[t] = f32x16_t{};
 
   // Open state of each column's token.  The walk stages key and value means
   // of 8 tokens at a time (fp32, this wave's part of the block ring); then
-  // every lane takes its columns' score (dot with its Q^T slice, summed over
-  // the 4 lane groups) and its slice of the value mean.
+  // every lane takes its column's score (dot with its Q^T slice, summed over
+  // the two halves) and its slice of the value mean.
   if (cnt > 0) {
     float *stage = reinterpret_cast<float *>(smem) + wave * STAGE;
     constexpr int E = D / 64;
@@ -287,49 +320,42 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
         [&](int t0) {
           if (t0 + 8 <= a) return;   // nothing staged in this batch
           wave_lds_sync();
-          float part[2];
-          bool here[2];
+          const int t = a + tok;
+          const bool here = colv && t >= t0 && t < t0 + 8;
+          float part = 0.0f;
+          if (here) {
+            const float *kp = stage + (t & 7) * 2 * D;
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            const int t = a + tok[qb];
-            here[qb] = tok[qb] < cnt && t >= t0 && t < t0 + 8;
-            part[qb] = 0.0f;
-            if (here[qb]) {
-              const float *kp = stage + (t & 7) * 2 * D;
-#pragma unroll
-              for (int ks = 0; ks < KS; ++ks) {
-                float qf[8];
-                V16<2>::unpack(qop[qb][ks], qf);
-                const float4 k0 = *reinterpret_cast<const float4 *>(kp + 32 * ks + 8 * q4);
-                const float4 k1 = *reinterpret_cast<const float4 *>(kp + 32 * ks + 8 * q4 + 4);
-                part[qb] = fmaf(qf[0], k0.x, part[qb]);
-                part[qb] = fmaf(qf[1], k0.y, part[qb]);
-                part[qb] = fmaf(qf[2], k0.z, part[qb]);
-                part[qb] = fmaf(qf[3], k0.w, part[qb]);
-                part[qb] = fmaf(qf[4], k1.x, part[qb]);
-                part[qb] = fmaf(qf[5], k1.y, part[qb]);
-                part[qb] = fmaf(qf[6], k1.z, part[qb]);
-                part[qb] = fmaf(qf[7], k1.w, part[qb]);
-              }
+            for (int ks = 0; ks < KS; ++ks) {
+              float qf[8];
+              V16<2>::unpack(qop[ks], qf);
+              const float4 k0 = *reinterpret_cast<const float4 *>(kp + 16 * ks + 8 * hb);
+              const float4 k1 = *reinterpret_cast<const float4 *>(kp + 16 * ks + 8 * hb + 4);
+              part = fmaf(qf[0], k0.x, part);
+              part = fmaf(qf[1], k0.y, part);
+              part = fmaf(qf[2], k0.z, part);
+              part = fmaf(qf[3], k0.w, part);
+              part = fmaf(qf[4], k1.x, part);
+              part = fmaf(qf[5], k1.y, part);
+              part = fmaf(qf[6], k1.z, part);
+              part = fmaf(qf[7], k1.w, part);
             }
           }
+          part += __shfl_xor(part, 32, 64);
+          if (here) {
+            const float *vp = stage + (t & 7) * 2 * D + D;
+            m = part * p.scale_log2;
+            ls = hb == 0 ? 1.0f : 0.0f;   // the open state's weight, counted once per column
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            part[qb] += __shfl_xor(part[qb], 16, 64);
-            part[qb] += __shfl_xor(part[qb], 32, 64);
-          }
+            for (int tt = 0; tt < NTL; ++tt)
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            if (here[qb]) {
-              const float *vp = stage + ((a + tok[qb]) & 7) * 2 * D + D;
-              m[qb] = part[qb] * p.scale_log2;
-              ls[qb] = q4 == 0 ? 1.0f : 0.0f;   // the open state's weight, counted once
-#pragma unroll
-              for (int nt = 0; nt < NT; ++nt) {
-                const float4 x = *reinterpret_cast<const float4 *>(vp + 16 * nt + 4 * q4);
-                acc[qb][nt] = f32x4_t{x.x, x.y, x.z, x.w};
+              for (int i = 0; i < 4; ++i) {
+                const float4 x = *reinterpret_cast<const float4 *>(vp + 32 * tt + 8 * i + 4 * hb);
+                acc[tt][4 * i + 0] = x.x;
+                acc[tt][4 * i + 1] = x.y;
+                acc[tt][4 * i + 2] = x.z;
+                acc[tt][4 * i + 3] = x.w;
               }
-            }
           }
           wave_lds_sync();
         });
@@ -339,160 +365,204 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   int s_top = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) s_top = max(s_top, s_hi[w]);
+  s_top = __builtin_amdgcn_readfirstlane(s_top);
   const int nblk = (s_top + 31) >> 5;
   const int P = 1 << p.log2p;
   const int64_t pt = int64_t(u) * p.maxpages;
   const int npg = min((s_top + P - 1) >> p.log2p, kPtabLds);
   for (int i = tid; i < npg; i += kThreads) s_pt[i] = p.ptab[pt + i];
   __syncthreads();
-  // The host limits this kernel to prompts of at most kPtabLds pages per unit.
-  auto page_of = [&](int s) -> const char * {
-    return p.pool + int64_t(s_pt[s >> p.log2p]) * p.page_bytes;
-  };
 
-  // Transfers of block kb into ring slot st; rows past the closed slots read
-  // the last closed one (in bounds; masked or zeroed when used).
+  // Transfers of block kb into ring slot st.  This thread's chunks and their
+  // byte offsets within a 32-row block (rows XOR-swizzled; LDS position =
+  // chunk index).  Pages of >= 32 slots hold a block in one page: one
+  // wave-uniform base plus fixed per-lane offsets.  Smaller pages are looked
+  // up per row, rows past the closed slots reading the last closed one (in
+  // bounds; masked or zeroed when used).
   const uint32_t ring = lds_offset(smem);
-  auto issue = [&](int kb, int st) {
+  uint32_t koff[DPW], voff[DPW];
+  int krow_of[DPW];
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int run = i * kWaves + wave;   // 1 KB run of the block written by this instruction
-      const int c = run * 64 + lane;       // 16-byte chunk of the block
-      const uint32_t kdst = __builtin_amdgcn_readfirstlane(ring + st * 2 * BLK + run * 1024);
-      const int row = c / CPR, pc = c - row * CPR;
-      const int s = min(kb * 32 + row, s_top - 1);
-      const char *krow = page_of(s) + int64_t(s & (P - 1)) * RB;
-      dma16(kdst, krow + (pc ^ k_swizzle<CPR>(row)) * 16);
-      const char *gv;
-      if (VT) {   // value page [D][P]: chunk = (dim, 8 slots)
-        const int dim = c >> 2, lc = (c & 3) ^ vt_swizzle(dim);
-        const int s0 = min(kb * 32 + 8 * lc, (s_top - 1) & ~7);
-        gv = page_of(s0) + int64_t(P) * RB + (int64_t(dim) * P + (s0 & (P - 1))) * 2;
-      } else {
-        gv = krow + int64_t(P) * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
+  for (int i = 0; i < DPW; ++i) {
+    const int c = (i * kWaves + wave) * 64 + lane;
+    const int row = c / CPR, pc = c - row * CPR;
+    krow_of[i] = row;
+    koff[i] = row * RB + (pc ^ k_swizzle<CPR>(row)) * 16;
+    if (VT) {
+      const int dim = c >> 2, lc = (c & 3) ^ vt_swizzle(dim);
+      voff[i] = dim * 64 + lc * 16;   // value page [D][32]
+    } else {
+      voff[i] = row * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
+    }
+  }
+  const bool big_pages = p.log2p >= 5;
+  auto issue = [&](int kb, int st) {
+    if (big_pages) {
+      const int s0 = kb * 32;
+      const int pg = __builtin_amdgcn_readfirstlane(s_pt[s0 >> p.log2p]);
+      const char *page = p.pool + int64_t(pg) * p.page_bytes;
+      const char *kb_base = page + int64_t(s0 & (P - 1)) * RB;
+      const char *vb_base = VT ? page + int64_t(P) * RB : kb_base + int64_t(P) * RB;
+#pragma unroll
+      for (int i = 0; i < DPW; ++i) {
+        const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
+        dma16_s(kdst, kb_base, koff[i]);
+        dma16_s(kdst + BLK, vb_base, voff[i]);
       }
-      dma16(kdst + BLK, gv);
+    } else {
+#pragma unroll
+      for (int i = 0; i < DPW; ++i) {
+        const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
+        const int s = min(kb * 32 + krow_of[i], s_top - 1);
+        const char *pg = p.pool + int64_t(s_pt[s >> p.log2p]) * p.page_bytes +
+                         int64_t((s & (P - 1)) - krow_of[i]) * RB;
+        dma16(kdst, pg + koff[i]);
+        dma16(kdst + BLK, pg + int64_t(P) * RB + voff[i]);
+      }
     }
   };
 
-  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
-  const int krow0 = 8 * (n16 >> 2) + (n16 & 3);   // score tile 0 row of this lane (+4 in tile 1)
-  for (int kb = 0; kb < nblk; ++kb) {
+  // Loop-invariant LDS read offsets (within a ring slot).  Keys: row
+  // pi(col), chunk (2 ks + hb) ^ swizzle -> 8 offsets.  Values (rows, read
+  // transposed): row 16 kk + 8 hb + 4 hf + (lane & 15) / 4 has swizzle
+  // 4 * ((lane >> 2) & 3) independent of kk and hf, so the 16 reads need one
+  // offset per tile t (kk, hf as immediates).  V^T rows: one offset per kk.
+  const int krow = score_slot(col);
+  uint32_t kaddr[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) kaddr[ks] = krow * RB + (((2 * ks + hb) ^ k_swizzle<CPR>(krow)) * 16);
+  uint32_t vaddr[VT ? 2 : NTL];
+  if (VT) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) vaddr[kk] = col * 64 + (((2 * kk + hb) ^ vt_swizzle(col)) * 16);
+  } else {
+    const int g16 = lane >> 4, r16 = lane & 15;
+    const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
+#pragma unroll
+    for (int t = 0; t < NTL; ++t) {
+      const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+      vaddr[t] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+    }
+  }
+
+  const float sl2 = p.scale_log2;
+  auto step = [&](auto stage_c, int kb) {
+    constexpr int ST = decltype(stage_c)::value;
     // blocks issued after kb: min(nblk - 1 - kb, kStages - 2)
     const int after = min(nblk - 1 - kb, kStages - 2);
     if (after >= 2) wait_vmcnt<4 * DPW>();
     else if (after == 1) wait_vmcnt<2 * DPW>();
     else wait_vmcnt<0>();
     __syncthreads();   // block kb is in LDS for every wave; the ring slot of kb - 1 is free
-    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (kb + kStages - 1) % kStages);
-    if (kb * 32 >= wave_hi) continue;
-    const int st = kb % kStages;
-    const char *kd = reinterpret_cast<const char *>(smem) + st * 2 * BLK;
+    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (ST + kStages - 1) % kStages);
+    if (kb * 32 >= wave_hi) return;
+    const char *kd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
     const char *vd = kd + BLK;
-    f32x4_t sc[2][2];
+
+    f32x16_t sc = f32x16_t{};
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+    for (int ks = 0; ks < KS; ++ks)
+      sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(kd + kaddr[ks]), qop[ks], sc);
+
+    // Raw scores; slots past this column's limit are masked only in blocks
+    // that reach the staircase.
+    float sv[16];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int rr = 0; rr < 16; ++rr) sv[rr] = sc[rr];
+    if (kb * 32 + 32 > wave_lo) {   // the block reaches the staircase
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      uint4 ka[2];
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const int row = krow0 + 4 * sb;
-        ka[sb] = *reinterpret_cast<const uint4 *>(kd + row * RB +
-                                                  (((4 * ks + q4) ^ k_swizzle<CPR>(row)) * 16));
-      }
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) sc[sb][qb] = mfma_16x16x32(ka[sb], qop[qb][ks], sc[sb][qb]);
-    }
-    // V^T operands of the value product: lane (n16, q4) = dim 16 nt + n16, slots 8 q4 .. +8.
-    uint4 va[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      if (VT) {
-        const int dim = 16 * nt + n16;
-        va[nt] = *reinterpret_cast<const uint4 *>(vd + dim * 64 + ((q4 ^ vt_swizzle(dim)) * 16));
-      } else {
-        uint2 h[2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int row = 8 * q4 + 4 * hh + (n16 >> 2);
-          const int lc = 2 * nt + ((n16 & 3) >> 1);
-          h[hh] = ds_read_tr16(vd + row * RB + ((lc ^ v_swizzle<CPR>(row)) * 16) + (n16 & 1) * 8);
-        }
-        va[nt] = make_uint4(h[0].x, h[0].y, h[1].x, h[1].y);
+      for (int rr = 0; rr < 16; ++rr) {
+        const int slot = kb * 32 + score_slot(8 * (rr >> 2) + 4 * hb + (rr & 3));
+        if (slot >= lim) sv[rr] = neg_inf();
       }
     }
-    const int keep = s_top - (kb * 32 + 8 * q4);   // this lane's slots below s_top
-    if (keep < 8) {
-      uint32_t msk[4];
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
 #pragma unroll
-      for (int w = 0; w < 4; ++w)
-        msk[w] = (2 * w < keep ? 0x0000ffffu : 0u) | (2 * w + 1 < keep ? 0xffff0000u : 0u);
+    for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
+    mx = fmaxf(mx, sv[15]);
+    mx = max_halves(mx) * sl2;
+    if (__any(mx > m + kLazyRescale)) {
+      const float mn = fmaxf(m, mx);
+      const float f = fast_exp2(m - mn);
+      m = mn;
+      ls *= f;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        va[nt].x &= msk[0];
-        va[nt].y &= msk[1];
-        va[nt].z &= msk[2];
-        va[nt].w &= msk[3];
-      }
+      for (int t = 0; t < NTL; ++t) acc[t] *= f;
     }
     uint4 pb[2];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      float x[8];
+    for (int kk = 0; kk < 2; ++kk) {
+      uint32_t w[4];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int s = kb * 32 + 8 * q4 + j;
-        x[j] = s < lim[qb] ? sc[j >> 2][qb][j & 3] * p.scale_log2 : neg_inf();
+      for (int q = 0; q < 4; ++q) {
+        w[q] = cvt_pk_bf16(fast_exp2(fmaf(sv[8 * kk + 2 * q], sl2, -m)),
+                           fast_exp2(fmaf(sv[8 * kk + 2 * q + 1], sl2, -m)));
+        ls = add_pair(w[q], ls);
       }
-      float mx = x[0];
+      pb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+
+    // Value product: A = V^T[dim 32 t + col][slots 16 kk + 8 hb .. + 8].
+    uint4 va[NTL][2];
 #pragma unroll
-      for (int j = 1; j < 8; ++j) mx = fmaxf(mx, x[j]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m[qb], mx);
-      const float f = fast_exp2(m[qb] - mn);
-      m[qb] = mn;
-      ls[qb] *= f;
+    for (int t = 0; t < NTL; ++t) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[qb][nt] *= f;
-      uint32_t pw[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        pw[w] = cvt_pk_bf16(fast_exp2(x[2 * w] - mn), fast_exp2(x[2 * w + 1] - mn));
-        ls[qb] += __uint_as_float(pw[w] << 16) + __uint_as_float(pw[w] & 0xffff0000u);
+      for (int kk = 0; kk < 2; ++kk) {
+        if (VT) {
+          va[t][kk] = *reinterpret_cast<const uint4 *>(vd + 2048 * t + vaddr[kk]);
+        } else {
+          const uint2 h0 = ds_read_tr16(vd + vaddr[t] + 16 * kk * RB);
+          const uint2 h1 = ds_read_tr16(vd + vaddr[t] + (16 * kk + 4) * RB);
+          va[t][kk] = make_uint4(h0.x, h0.y, h1.x, h1.y);
+        }
       }
-      pb[qb] = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+    }
+    if (kb * 32 + 32 > s_top) {   // the last block: clear the slots past the closed ones
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int keep = s_top - (kb * 32 + 16 * kk + 8 * hb);
+        uint32_t msk[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          msk[q] = (2 * q < keep ? 0x0000ffffu : 0u) | (2 * q + 1 < keep ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int t = 0; t < NTL; ++t) {
+          va[t][kk].x &= msk[0];
+          va[t][kk].y &= msk[1];
+          va[t][kk].z &= msk[2];
+          va[t][kk].w &= msk[3];
+        }
+      }
     }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int t = 0; t < NTL; ++t)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) acc[qb][nt] = mfma_16x16x32(va[nt], pb[qb], acc[qb][nt]);
+      for (int kk = 0; kk < 2; ++kk) acc[t] = mfma_32x32x16(va[t][kk], pb[kk], acc[t]);
+  };
+
+  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
+  static_assert(kStages == 3, "the block loop below is unrolled for a 3-slot ring");
+  for (int kb = 0; kb < nblk; kb += 3) {
+    step(std::integral_constant<int, 0>{}, kb);
+    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
+    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
   }
 
-  // Normalise and store: lane holds dims 16 nt + 4 q4 .. +4 of its columns.
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    float lt = ls[qb];
-    lt += __shfl_xor(lt, 16, 64);
-    lt += __shfl_xor(lt, 32, 64);
-    const int j = tok[qb], h = 16 * qb + n16 - j * G;
-    const int t = a + j;
-    if (t >= p.n) continue;
-    const bool valid = j < cnt;
-    const float inv = valid ? 1.0f / lt : 0.0f;
+  // Normalise and store: lane holds dims 32 t + 8 i + 4 hb .. + 4 of its column.
+  float lt = ls + __shfl_xor(ls, 32, 64);
+  const int t = a + tok;
+  if (t < p.n) {
+    const float inv = colv ? 1.0f / lt : 0.0f;
     char *orow = static_cast<char *>(p.out) +
-                 (b * p.os[0] + int64_t(t) * p.os[1] + (g * G + h) * p.os[2]) * 2;
+                 (b * p.os[0] + int64_t(t) * p.os[1] + (g * G + head) * p.os[2]) * 2;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const uint32_t lo = cvt_pk_bf16(acc[qb][nt][0] * inv, acc[qb][nt][1] * inv);
-      const uint32_t hi = cvt_pk_bf16(acc[qb][nt][2] * inv, acc[qb][nt][3] * inv);
-      *reinterpret_cast<uint2 *>(orow + (16 * nt + 4 * q4) * 2) = make_uint2(lo, hi);
-    }
+    for (int tt = 0; tt < NTL; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = cvt_pk_bf16(acc[tt][4 * i] * inv, acc[tt][4 * i + 1] * inv);
+        const uint32_t hi = cvt_pk_bf16(acc[tt][4 * i + 2] * inv, acc[tt][4 * i + 3] * inv);
+        *reinterpret_cast<uint2 *>(orow + (32 * tt + 8 * i + 4 * hb) * 2) = make_uint2(lo, hi);
+      }
   }
 }
 
