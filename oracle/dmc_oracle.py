@@ -46,7 +46,12 @@ design notes of the repository):
    with GQA but does not say which query head supplies omega.
 7. omega is floored at 2**-100 so that z never becomes 0 (sigmoid underflows
    only for q[0] below about -69, which synthetic inputs never reach).
-8. Prefill (the prompt phase) equals n sequential updates without attention.
+8. Prefill (the prompt phase) equals n sequential updates without attention;
+   prompt-phase attention is each token's update followed by its attention
+   (reading 4 at every prompt position).
+9. Variants of the appendix ablations: uniform weighting (omega = 1) and
+   DMC-HardC (decision and importance of kv head 0 of a batch row shared by
+   all heads of the layer; the paper does not name the head).
 
 Parity pins (see tests/oracle_pins.py): the worked decision example of
 Sec. 3.2, sigmoid(-5) = 0.0067 (Sec. 4), all-append = vanilla attention via
@@ -93,12 +98,16 @@ def importance(q0_group, omega_src="lead"):
     q0_group: [..., G] values q[h, 0] of the G query heads sharing the kv head.
     'lead' takes the first head of the group, 'group_mean' the mean of the
     heads' sigmoids (reading 6); both floored at 2**-100 (reading 7).
+    'uniform' is the uniform-weighting ablation of the appendix: every token
+    of a segment weighs 1, so a slot is the plain mean of its segment.
     """
     q0_group = np.asarray(q0_group, dtype=np.float64)
     if omega_src == "lead":
         w = sigmoid(q0_group[..., 0])
     elif omega_src == "group_mean":
         w = sigmoid(q0_group).mean(axis=-1)
+    elif omega_src == "uniform":
+        return np.ones(q0_group.shape[:-1])
     else:
         raise ValueError(omega_src)
     return np.maximum(w, OMEGA_FLOOR)
@@ -143,11 +152,12 @@ class LayerCache:
         self.z[:] = np.asarray(z, dtype=np.float64)
 
     # -- Algorithm 1 --------------------------------------------------------
-    def update(self, k, v, q0_group, active=None, c=0.0, omega_src="lead"):
+    def update(self, k, v, q0_group, active=None, c=0.0, omega_src="lead", logits=None):
         """One step of Algorithm 1 for every active unit.
 
         k, v: [U, d] new key/value; q0_group: [U, G] first query neuron of the
-        group's query heads.  Returns alpha [U] and the slot index [U] each
+        group's query heads; logits: [U] decision neurons (default k[:, 0],
+        the unit's own key).  Returns alpha [U] and the slot index [U] each
         token went to (-1 for inactive units).
         """
         k = np.array(k, dtype=np.float64)           # private copies: inputs stay const
@@ -155,7 +165,7 @@ class LayerCache:
         active = np.ones(self.U, bool) if active is None else np.asarray(active, bool)
 
         # lines 1-2: alpha_t, omega_t; reading 3: an empty cache appends
-        alpha = decision(k[:, 0], c) * (self.l > 0)
+        alpha = decision(k[:, 0] if logits is None else logits, c) * (self.l > 0)
         omega = importance(q0_group, omega_src)
         # line 3: k_t[0] <- 0  (q_t[0] is zeroed where scores are formed)
         k[:, 0] = 0.0
@@ -206,18 +216,37 @@ class DMCOracle:
     """
 
     def __init__(self, num_layers, batch, num_q_heads, num_kv_heads, head_dim,
-                 max_slots, decision_bias=0.0, omega_src="lead"):
+                 max_slots, decision_bias=0.0, omega_src="lead", decision_src="per_head"):
         assert num_q_heads % num_kv_heads == 0
+        assert decision_src in ("per_head", "shared_layer")
         self.L, self.B = int(num_layers), int(batch)
         self.Hq, self.Hkv, self.d = int(num_q_heads), int(num_kv_heads), int(head_dim)
         self.G = self.Hq // self.Hkv
         self.c, self.omega_src = float(np.float32(decision_bias)), omega_src
+        self.decision_src = decision_src
         self.layers = [LayerCache(self.B * self.Hkv, self.d, max_slots)
                        for _ in range(self.L)]
 
     def _q0_groups(self, q0):
         """[B, Hq] first query neurons -> [B*Hkv, G]."""
         return np.asarray(q0, dtype=np.float64).reshape(self.B * self.Hkv, self.G)
+
+    def _decision_inputs(self, k0, q0):
+        """Decision logits [U] and query-neuron groups [U, G] of one step.
+
+        k0: [B, Hkv] first key neurons, q0: [B, Hq] first query neurons.
+        'shared_layer' (DMC-HardC, appendix ablations: decision and
+        importance shared by the heads of a layer) takes both from kv head 0
+        of the batch row for every head of the row (reading: the paper does
+        not name the head).
+        """
+        k0 = np.asarray(k0, dtype=np.float64)
+        q0g = self._q0_groups(q0).reshape(self.B, self.Hkv, self.G)
+        if self.decision_src == "shared_layer":
+            k0 = np.repeat(k0[:, :1], self.Hkv, axis=1)
+            q0g = np.repeat(q0g[:, :1], self.Hkv, axis=1)
+        U = self.B * self.Hkv
+        return k0.reshape(U), q0g.reshape(U, self.G)
 
     def decode_step(self, layer, q, k, v):
         """One auto-regressive step of one layer: update, then attend.
@@ -228,10 +257,10 @@ class DMCOracle:
         lc = self.layers[layer]
         q = np.asarray(q, dtype=np.float64)
         U = self.B * self.Hkv
+        logits, q0g = self._decision_inputs(np.asarray(k)[:, :, 0], q[:, :, 0])
         _, slot = lc.update(np.asarray(k).reshape(U, self.d),
                             np.asarray(v).reshape(U, self.d),
-                            self._q0_groups(q[:, :, 0]), c=self.c,
-                            omega_src=self.omega_src)
+                            q0g, c=self.c, omega_src=self.omega_src, logits=logits)
         out = np.empty((self.B, self.Hq, self.d))
         qg = q.reshape(U, self.G, self.d)
         for u in range(U):
@@ -257,9 +286,10 @@ class DMCOracle:
         slots = np.full((U, n), -1, dtype=np.int64)
         for t in range(n):
             active = np.repeat(t < lens, self.Hkv)
+            logits, q0g = self._decision_inputs(k[:, t, :, 0], q0[:, t])
             _, slot = lc.update(k[:, t].reshape(U, self.d), v[:, t].reshape(U, self.d),
-                                self._q0_groups(q0[:, t]), active=active,
-                                c=self.c, omega_src=self.omega_src)
+                                q0g, active=active, c=self.c, omega_src=self.omega_src,
+                                logits=logits)
             slots[:, t] = slot
         return slots.reshape(self.B, self.Hkv, n)
 
@@ -286,9 +316,10 @@ class DMCOracle:
         slots = np.full((U, n), -1, dtype=np.int64)
         for t in range(n):
             active = np.repeat(lens > t, self.Hkv)
+            logits, q0g = self._decision_inputs(k[:, t, :, 0], q[:, t, :, 0])
             _, slot = lc.update(k[:, t].reshape(U, self.d), v[:, t].reshape(U, self.d),
-                                self._q0_groups(q[:, t, :, 0]), active=active,
-                                c=self.c, omega_src=self.omega_src)
+                                q0g, active=active, c=self.c, omega_src=self.omega_src,
+                                logits=logits)
             slots[:, t] = slot
             qg = q[:, t].reshape(U, self.G, self.d)
             for u in np.nonzero(active)[0]:

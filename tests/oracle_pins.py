@@ -396,7 +396,74 @@ def check_prefill_attend(O):
             assert slots[b, g, :m].tolist() == (np.cumsum(1 - alpha) - 1).tolist()
 
 
+def check_uniform_weighting(O):
+    """Uniform weighting (appendix ablations): every slot is the plain
+    arithmetic mean of its segment (np.mean), z of the open slot is the
+    segment's token count, and attention is softmax over those means."""
+    rng = np.random.default_rng(41)
+    n, d, G = 37, 6, 2
+    k = rng.standard_normal((n, d))
+    v = rng.standard_normal((n, d))
+    q = rng.standard_normal((n, G, d)) * 3.0          # varied q[0]: learned omega would differ
+    orc = O.DMCOracle(1, 1, G, 1, d, max_slots=n, omega_src="uniform")
+    outs = []
+    for t in range(n):
+        o, _ = orc.decode_step(0, q[t][None], k[t][None, None], v[t][None, None])
+        outs.append(o[0])
+    alpha = (k[:, 0] > 0).astype(int)
+    alpha[0] = 0
+    starts = list(np.nonzero(alpha == 0)[0]) + [n]
+    kh = k.copy()
+    kh[:, 0] = 0.0
+    Km = np.array([kh[a:b].mean(axis=0) for a, b in zip(starts[:-1], starts[1:])])
+    Vm = np.array([v[a:b].mean(axis=0) for a, b in zip(starts[:-1], starts[1:])])
+    K, V, l, z = orc.export(0)
+    L = int(l[0, 0])
+    assert L == len(starts) - 1
+    _close(K[0, 0, :L], Km, what="uniform slots K")
+    _close(V[0, 0, :L], Vm, what="uniform slots V")
+    assert abs(z[0, 0] - (starts[-1] - starts[-2])) < 1e-12
+    qq = q[-1].copy()
+    qq[:, 0] = 0.0
+    sc = qq @ Km.T / math.sqrt(d)
+    p = np.exp(sc - sc.max(axis=1, keepdims=True))
+    _close(outs[-1], (p @ Vm) / p.sum(axis=1, keepdims=True), what="uniform attention")
+
+
+def check_shared_layer_decisions(O):
+    """DMC-HardC (decision and importance shared by a layer's heads, taken
+    from kv head 0 of the row) equals per-head DMC run on inputs whose every
+    head carries head 0's decision and importance neurons; all heads of a row
+    then have equal lengths.  Both omega sources, prefill and decode."""
+    rng = np.random.default_rng(43)
+    B, Hkv, G, d, n = 2, 3, 2, 8, 24
+    Hq = Hkv * G
+    for src in ("lead", "group_mean"):
+        k = rng.standard_normal((B, n, Hkv, d))
+        v = rng.standard_normal((B, n, Hkv, d))
+        q = rng.standard_normal((B, n, Hq, d))
+        k2, q2 = k.copy(), q.copy()
+        for g in range(Hkv):
+            k2[:, :, g, 0] = k[:, :, 0, 0]
+            q2[:, :, g * G:(g + 1) * G, 0] = q[:, :, 0:G, 0]
+        hard = O.DMCOracle(1, B, Hq, Hkv, d, max_slots=2 * n, omega_src=src,
+                           decision_src="shared_layer")
+        ref = O.DMCOracle(1, B, Hq, Hkv, d, max_slots=2 * n, omega_src=src)
+        half = n // 2
+        s1 = hard.prefill(0, k[:, :half], v[:, :half], q[:, :half, :, 0])
+        s2 = ref.prefill(0, k2[:, :half], v[:, :half], q2[:, :half, :, 0])
+        assert (s1 == s2).all()
+        for t in range(half, n):
+            o1, i1 = hard.decode_step(0, q[:, t], k[:, t], v[:, t])
+            o2, i2 = ref.decode_step(0, q2[:, t], k2[:, t], v[:, t])
+            assert (i1 == i2).all()
+            _close(o1, o2, tol=0.0, what=f"shared-layer decode {src}")
+        l = hard.export(0)[2]
+        assert (l == l[:, :1]).all(), l
+
+
 ALL_CHECKS = [check_worked_example, check_sigmoid_c5, check_exact_decisions,
               check_all_append_vanilla, check_all_accumulate, check_segments,
               check_avg_pool, check_bruteforce_unrolled, check_gqa_omega,
-              check_permutation, check_prefill_matches_decode, check_prefill_attend]
+              check_permutation, check_prefill_matches_decode, check_prefill_attend,
+              check_uniform_weighting, check_shared_layer_decisions]

@@ -15,7 +15,7 @@ MUTATIONS = {
     "sigmoid_sign": ("1.0 / (1.0 + np.exp(-x))", "1.0 / (1.0 + np.exp(x))"),
     "tie_rounds_up": ("return (k0 > np.float64", "return (k0 >= np.float64"),
     "no_bias": ("(k0 > np.float64(np.float32(c)))", "(k0 > 0.0)"),
-    "first_token_may_accumulate": ("decision(k[:, 0], c) * (self.l > 0)", "decision(k[:, 0], c)"),
+    "first_token_may_accumulate": ("else logits, c) * (self.l > 0)", "else logits, c)"),
     "key_not_zeroed": ("        k[:, 0] = 0.0\n", "        pass\n"),
     "query_not_zeroed": ("        q[:, 0] = 0.0                                  # Algorithm 1, line 3",
                          "        pass"),
@@ -36,6 +36,10 @@ MUTATIONS = {
                              "active = np.repeat(t < n, self.Hkv)"),
     "prefill_attend_ignores_lens": ("active = np.repeat(lens > t, self.Hkv)",
                                     "active = np.repeat(n > t, self.Hkv)"),
+    "uniform_weight_is_learned": ("        return np.ones(q0_group.shape[:-1])\n",
+                                  "        w = sigmoid(q0_group[..., 0])\n"),
+    "shared_decision_own_head": ("            k0 = np.repeat(k0[:, :1], self.Hkv, axis=1)\n", ""),
+    "shared_importance_own_group": ("            q0g = np.repeat(q0g[:, :1], self.Hkv, axis=1)\n", ""),
 }
 
 
