@@ -65,7 +65,15 @@ typedef enum { DMC_BF16 = 0, DMC_FP32 = 1 } dmc_dtype;
  * (grouped-query attention; the paper combines DMC with GQA, Sec. 5, but
  * does not name the head).  LEAD: query head g*G.  GROUP_MEAN: mean of the
  * G heads' sigmoid(q[0]). */
-typedef enum { DMC_OMEGA_LEAD_QHEAD = 0, DMC_OMEGA_GROUP_MEAN = 1 } dmc_omega_src;
+typedef enum { DMC_OMEGA_LEAD_QHEAD = 0, DMC_OMEGA_GROUP_MEAN = 1, DMC_OMEGA_UNIFORM = 2 } dmc_omega_src;
+
+/* Which heads' neurons decide (alpha) and weigh (omega) each unit's token.
+ * PER_HEAD: every kv head its own (DMC).  SHARED_LAYER: kv head 0 of the
+ * batch row (its k[0]; omega per dmc_omega_src from query group 0) for every
+ * head of the layer -- the DMC-HardC ablation of the appendix, whose heads
+ * therefore keep equal lengths.  UNIFORM omega is the uniform-weighting
+ * ablation (every token of a segment weighs 1). */
+typedef enum { DMC_DECISION_PER_HEAD = 0, DMC_DECISION_SHARED_LAYER = 1 } dmc_decision_src;
 
 typedef struct dmc_cache_config {
   int32_t num_layers;
@@ -74,7 +82,9 @@ typedef struct dmc_cache_config {
   int32_t num_kv_heads;      /* num_q_heads % num_kv_heads == 0, G in {1,2,4,8} */
   int32_t head_dim;          /* 64 or 128 */
   int32_t dtype;             /* dmc_dtype: inputs, cache slots and outputs */
-  int32_t page_size;         /* slots per page, power of two in [8, 256]; the paper uses 32 */
+  int32_t page_size;         /* slots per page, power of two in [8, 65536]; the paper uses 32.
+                                A page as large as max_slots_per_seq gives every unit one
+                                contiguous padded region (the padded-tensor layout of DMC-C) */
   int32_t max_slots_per_seq; /* slot capacity of one unit; page-table width = ceil(/page_size) */
   int64_t num_pages;         /* pool capacity in pages, shared by all units, < 2^31 */
   float decision_bias;       /* c: alpha = round(sigmoid(k[0] - c)) = (k[0] > c); 0 = Algorithm 1 */
@@ -84,6 +94,8 @@ typedef struct dmc_cache_config {
                                 (compressed) slots */
   int32_t max_prompt_len;    /* largest n for dmc_prefill_compress / dmc_prefill_attend;
                                 0 = max_slots_per_seq */
+  int32_t decision_src;      /* dmc_decision_src */
+  int32_t reserved;          /* must be 0 */
 } dmc_cache_config;
 
 typedef struct dmc_cache dmc_cache; /* opaque host handle */

@@ -16,7 +16,11 @@ LIB_PATH = os.path.join(HERE, "libdmc.so")
 
 DMC_OK, DMC_ERR_INVALID_ARG, DMC_ERR_UNSUPPORTED, DMC_ERR_CAPACITY, DMC_ERR_HIP = range(5)
 DMC_BF16, DMC_FP32 = 0, 1
-DMC_OMEGA_LEAD_QHEAD, DMC_OMEGA_GROUP_MEAN = 0, 1
+DMC_OMEGA_LEAD_QHEAD, DMC_OMEGA_GROUP_MEAN, DMC_OMEGA_UNIFORM = 0, 1, 2
+DMC_DECISION_PER_HEAD, DMC_DECISION_SHARED_LAYER = 0, 1
+OMEGA_SRC = {"lead": DMC_OMEGA_LEAD_QHEAD, "group_mean": DMC_OMEGA_GROUP_MEAN,
+             "uniform": DMC_OMEGA_UNIFORM}
+DECISION_SRC = {"per_head": DMC_DECISION_PER_HEAD, "shared_layer": DMC_DECISION_SHARED_LAYER}
 STATUS_NAMES = {0: "DMC_OK", 1: "DMC_ERR_INVALID_ARG", 2: "DMC_ERR_UNSUPPORTED",
                 3: "DMC_ERR_CAPACITY", 4: "DMC_ERR_HIP"}
 
@@ -32,7 +36,7 @@ class CacheConfig(ctypes.Structure):
                 ("num_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int32),
                 ("page_size", c_int32), ("max_slots_per_seq", c_int32), ("num_pages", c_int64),
                 ("decision_bias", c_float), ("omega_src", c_int32), ("split_tile", c_int32),
-                ("max_prompt_len", c_int32)]
+                ("max_prompt_len", c_int32), ("decision_src", c_int32), ("reserved", c_int32)]
 
 
 class DMCError(RuntimeError):
@@ -90,16 +94,19 @@ def check(status: int):
 
 def make_config(num_layers, batch, num_q_heads, num_kv_heads, head_dim, dtype="bf16",
                 page_size=32, max_slots_per_seq=4096, num_pages=None, decision_bias=0.0,
-                omega_src="lead", split_tile=0, max_prompt_len=0) -> CacheConfig:
-    """A dmc_cache_config; num_pages defaults to room for every unit at capacity."""
+                omega_src="lead", split_tile=0, max_prompt_len=0,
+                decision_src="per_head") -> CacheConfig:
+    """A dmc_cache_config; num_pages defaults to room for every unit at capacity.
+
+    omega_src: 'lead' | 'group_mean' | 'uniform'; decision_src: 'per_head' |
+    'shared_layer' (DMC-HardC)."""
     units = num_layers * batch * num_kv_heads
     if num_pages is None:
         num_pages = units * -(-max_slots_per_seq // page_size)
     return CacheConfig(num_layers, batch, num_q_heads, num_kv_heads, head_dim,
                        DMC_FP32 if dtype in ("fp32", "float32") else DMC_BF16, page_size,
-                       max_slots_per_seq, num_pages, decision_bias,
-                       DMC_OMEGA_GROUP_MEAN if omega_src == "group_mean" else DMC_OMEGA_LEAD_QHEAD,
-                       split_tile, max_prompt_len)
+                       max_slots_per_seq, num_pages, decision_bias, OMEGA_SRC[omega_src],
+                       split_tile, max_prompt_len, DECISION_SRC[decision_src], 0)
 
 
 def workspace_bytes(cfg: CacheConfig) -> int:

@@ -81,16 +81,21 @@ dmc_status validate_config(const dmc_cache_config *c) {
     return fail(DMC_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", c->head_dim);
   if (c->dtype != DMC_BF16 && c->dtype != DMC_FP32)
     return fail(DMC_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
-  if (!pow2(c->page_size) || c->page_size < 8 || c->page_size > 256)
-    return fail(DMC_ERR_UNSUPPORTED, "page_size %d must be a power of two in [8,256]", c->page_size);
+  if (!pow2(c->page_size) || c->page_size < 8 || c->page_size > 65536)
+    return fail(DMC_ERR_UNSUPPORTED, "page_size %d must be a power of two in [8,65536]",
+                c->page_size);
   if (c->max_slots_per_seq < 1)
     return fail(DMC_ERR_INVALID_ARG, "max_slots_per_seq must be >= 1");
   if (c->num_pages < 1 || c->num_pages >= (int64_t(1) << 31))
     return fail(DMC_ERR_INVALID_ARG, "num_pages %lld outside [1, 2^31)",
                 static_cast<long long>(c->num_pages));
   if (!std::isfinite(c->decision_bias)) return fail(DMC_ERR_INVALID_ARG, "decision_bias not finite");
-  if (c->omega_src != DMC_OMEGA_LEAD_QHEAD && c->omega_src != DMC_OMEGA_GROUP_MEAN)
+  if (c->omega_src != DMC_OMEGA_LEAD_QHEAD && c->omega_src != DMC_OMEGA_GROUP_MEAN &&
+      c->omega_src != DMC_OMEGA_UNIFORM)
     return fail(DMC_ERR_INVALID_ARG, "unknown omega_src %d", c->omega_src);
+  if (c->decision_src != DMC_DECISION_PER_HEAD && c->decision_src != DMC_DECISION_SHARED_LAYER)
+    return fail(DMC_ERR_INVALID_ARG, "unknown decision_src %d", c->decision_src);
+  if (c->reserved != 0) return fail(DMC_ERR_INVALID_ARG, "reserved config field must be 0");
   if (c->split_tile < 0) return fail(DMC_ERR_INVALID_ARG, "split_tile must be >= 0");
   if (c->max_prompt_len < 0 || c->max_prompt_len > c->max_slots_per_seq)
     return fail(DMC_ERR_INVALID_ARG, "max_prompt_len must be in [0, max_slots_per_seq]");
@@ -293,6 +298,7 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   p.log2p = ilog2(c.page_size);
   p.split_tile = L.split_tile;
   p.omega_src = c.omega_src;
+  p.decision_src = c.decision_src;
   const int64_t grid64 = std::min<int64_t>(int64_t(cache->cu_count) * kDecodeWgPerCu,
                                             kMaxDecodeWaves / 4);
   const int grid = static_cast<int>(grid64);
@@ -366,6 +372,7 @@ dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const 
   p.maxpages = L.maxpages;
   p.log2p = ilog2(c.page_size);
   p.omega_src = c.omega_src;
+  p.decision_src = c.decision_src;
   p.max_prompt = L.max_prompt;
   p.prompt_chunks = L.prompt_chunks;
   p.carry_blocks = L.carry_blocks;

@@ -61,7 +61,7 @@ struct DecodeParams {
   int32_t *meta;           // [U, 2]: first partial record, record count (for the combine)
   float c;                 // decision bias
   float scale_log2;        // log2(e) / sqrt(d)
-  int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src;
+  int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src, decision_src;
 };
 
 struct PrefillParams {
@@ -84,7 +84,7 @@ struct PrefillParams {
                            // every 32-token boundary inside a segment (prompt attention)
   float c;
   int32_t n, units, hkv, hq, maxpages, log2p, omega_src, max_prompt, prompt_chunks,
-      carry_blocks;
+      carry_blocks, decision_src;
 };
 
 // Floats per carry record: sum of omega * k (d), sum of omega * v (d), sum of

@@ -186,8 +186,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
       int open_page = -1;
       if (owner) {
-        k0 = load_elem<ES>(p.k, int64_t(u) * D);
-        q0 = load_elem<ES>(p.q, int64_t(b * p.hq + g * G) * D);
+        const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
+        k0 = load_elem<ES>(p.k, int64_t(b * p.hkv + dg) * D);
+        q0 = load_elem<ES>(p.q, int64_t(b * p.hq + dg * G) * D);
         k_raw = ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES);
         v_raw = ld16(static_cast<const char *>(p.v) + (int64_t(u) * D + part * VN) * ES);
         if (l > 0) {
@@ -312,11 +313,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         float om;
         if (p.omega_src == 0) {
           om = sigmoid_floor(q0);
-        } else {
+        } else if (p.omega_src == 1) {
+          const int dg = p.decision_src ? 0 : g;
           float sum = 0.0f;
           for (int h = 0; h < G; ++h)
-            sum += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + g * G + h) * D));
+            sum += sigmoid_floor(load_elem<ES>(p.q, int64_t(b * p.hq + dg * G + h) * D));
           om = fmaxf(sum / G, 0x1p-100f);
+        } else {
+          om = 1.0f;   // uniform weighting
         }
         float ck[VN], cv[VN];
         V::unpack(k_raw, ck);
@@ -596,8 +600,9 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
       uint4 kt[KS], ko[KS];
       uint16_t vt[NT], vo[NT];
       if (owner) {
-        k0 = load_elem<2>(p.k, int64_t(u) * D);
-        q0 = load_elem<2>(p.q, int64_t(b * p.hq + g * G) * D);
+        const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
+        k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
+        q0 = load_elem<2>(p.q, int64_t(b * p.hq + dg * G) * D);
         const char *kp = static_cast<const char *>(p.k) + int64_t(u) * RB;
         const uint16_t *vp = static_cast<const uint16_t *>(p.v) + int64_t(u) * D;
 #pragma unroll
@@ -628,11 +633,14 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
         float om;
         if (p.omega_src == 0) {
           om = sigmoid_floor(q0);
-        } else {
+        } else if (p.omega_src == 1) {
+          const int dg = p.decision_src ? 0 : g;
           float sum = 0.0f;
           for (int h = 0; h < G; ++h)
-            sum += sigmoid_floor(load_elem<2>(p.q, int64_t(b * p.hq + g * G + h) * D));
+            sum += sigmoid_floor(load_elem<2>(p.q, int64_t(b * p.hq + dg * G + h) * D));
           om = fmaxf(sum / G, 0x1p-100f);
+        } else {
+          om = 1.0f;   // uniform weighting
         }
         int flag = 0, slot, page = open_page;
         bool has_cur = true;
@@ -840,6 +848,7 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
   __shared__ int s_tot[kWaves];
   const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = u / p.hkv, g = u - b * p.hkv, G = p.hq / p.hkv;
+  const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
   const int nb = prompt_len(p, b, tid == 0);
   int total = 0;
   constexpr int kBatch = 8;   // token rows whose decision neurons are in flight per thread
@@ -851,9 +860,9 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
       k0[j] = 0.0f;
       q0[j] = 0.0f;
       if (t < p.n) {
-        k0[j] = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + g * p.ks[2]);
+        k0[j] = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + dg * p.ks[2]);
         if (p.omega_src == 0)
-          q0[j] = load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G) * p.qs[2]);
+          q0[j] = load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G) * p.qs[2]);
       }
     }
 #pragma unroll
@@ -868,11 +877,13 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
         float om;
         if (p.omega_src == 0) {
           om = sigmoid_floor(q0[j]);
-        } else {
+        } else if (p.omega_src == 1) {
           float sum = 0.0f;
           for (int h = 0; h < G; ++h)
-            sum += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (g * G + h) * p.qs[2]));
+            sum += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G + h) * p.qs[2]));
           om = fmaxf(sum / G, 0x1p-100f);
+        } else {
+          om = 1.0f;   // uniform weighting
         }
         p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
         p.omega[int64_t(u) * p.max_prompt + t] = om;

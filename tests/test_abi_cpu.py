@@ -45,7 +45,7 @@ def test_config_struct_matches_header(P):
     fields = re.findall(r"^\s*(?:int32_t|int64_t|float)\s+([a-z_, ]+);", body.group(1), re.M)
     names = [f.strip() for grp in fields for f in grp.split(",")]
     assert names == [f[0] for f in P.CacheConfig._fields_]
-    assert ctypes.sizeof(P.CacheConfig) == 56
+    assert ctypes.sizeof(P.CacheConfig) == 64
 
 
 def test_workspace_bytes(P):
@@ -62,6 +62,7 @@ def test_workspace_bytes(P):
     ("page_size", 4, "page_size"), ("dtype", 7, "dtype"), ("num_pages", 0, "num_pages"),
     ("num_pages", 1 << 31, "num_pages"), ("max_slots_per_seq", 0, "max_slots"),
     ("omega_src", 5, "omega"), ("split_tile", -1, "split_tile"), ("max_prompt_len", 99999, "prompt"),
+    ("decision_src", 2, "decision_src"), ("reserved", 1, "reserved"), ("page_size", 131072, "page_size"),
     ("batch", 0, ">= 1"), ("num_q_heads", 48, "group"),
 ])
 def test_invalid_config(P, field, value, msg):
