@@ -52,6 +52,10 @@ design notes of the repository):
 9. Variants of the appendix ablations: uniform weighting (omega = 1) and
    DMC-HardC (decision and importance of kv head 0 of a batch row shared by
    all heads of the layer; the paper does not name the head).
+10. Window grouping (Sec. 3.3), when a window w is set: every step's
+   partial accumulation runs over the last w tokens only, restarted at the
+   window's first token, so a slot is the omega-weighted mean of the last
+   min(w, length) tokens of its segment; the unit caches those raw tokens.
 
 Parity pins (see tests/oracle_pins.py): the worked decision example of
 Sec. 3.2, sigmoid(-5) = 0.0067 (Sec. 4), all-append = vanilla attention via
@@ -123,16 +127,30 @@ class LayerCache:
     K, V: [U, cap, d] float64 slots (only the first l[u] are meaningful),
     l: [U] slot counts, z: [U] running importance sum of the open (last)
     slot -- the only z Algorithm 1 ever reads again.
+
+    window > 0 selects the window-grouping approximation (Sec. 3.3): the
+    partial accumulation of every step is evaluated over the last `window`
+    tokens only, restarted at the window's first token; the unit keeps those
+    tokens (k with element 0 zeroed, v, omega, alpha) to do so.
     """
 
-    def __init__(self, units, head_dim, cap):
+    def __init__(self, units, head_dim, cap, window=0):
         self.U, self.d, self.cap = int(units), int(head_dim), int(cap)
         self.K = np.zeros((self.U, self.cap, self.d))
         self.V = np.zeros((self.U, self.cap, self.d))
         self.l = np.zeros(self.U, dtype=np.int64)
         self.z = np.zeros(self.U)
+        self.window = int(window)
+        if self.window:
+            w = self.window
+            self.wk = np.zeros((self.U, w, self.d))
+            self.wv = np.zeros((self.U, w, self.d))
+            self.ww = np.zeros((self.U, w))
+            self.wa = np.zeros((self.U, w), dtype=np.int64)
+            self.wn = np.zeros(self.U, dtype=np.int64)   # tokens seen by the unit
 
     def copy(self):
+        assert not self.window, "copy of a windowed cache is not needed"
         other = LayerCache(self.U, self.d, self.cap)
         other.K[:], other.V[:] = self.K, self.V
         other.l[:], other.z[:] = self.l, self.z
@@ -140,6 +158,7 @@ class LayerCache:
 
     def load(self, K, V, lengths, z):
         """Install an existing compressed cache (dense [U, >=max l, d])."""
+        assert not self.window, "a windowed cache needs its token window; it is not imported"
         lengths = np.asarray(lengths, dtype=np.int64)
         assert lengths.shape == (self.U,) and lengths.max(initial=0) <= self.cap
         self.K[:] = 0.0
@@ -173,6 +192,9 @@ class LayerCache:
         acc = np.nonzero(active & (alpha == 1))[0]
         app = np.nonzero(active & (alpha == 0))[0]
         assert np.all(self.l[app] < self.cap), "oracle cache capacity exceeded"
+        if self.window:
+            self._windowed(k, v, alpha, omega, acc, app)
+            return alpha, np.where(active, self.l - 1, -1)
 
         # lines 4-7: accumulate into the last slot l-1
         if acc.size:
@@ -195,6 +217,34 @@ class LayerCache:
         slot = np.where(active, self.l - 1, -1)
         return alpha, slot
 
+    def _windowed(self, k, v, alpha, omega, acc, app):
+        """Window grouping (Sec. 3.3): push the token into the unit's window,
+        then evaluate the partial-accumulation recurrence of Sec. 3.2 over the
+        window, started afresh at its first token (z = omega, state = k):
+        z_j = alpha_j z_{j-1} + omega_j, state_j = (alpha_j state_{j-1} z_{j-1}
+        + k_j omega_j) / z_j.  The result is the open slot (a new one when the
+        token appends)."""
+        w = self.window
+        for u in np.concatenate([acc, app]):
+            pos = self.wn[u] % w
+            self.wk[u, pos], self.wv[u, pos] = k[u], v[u]
+            self.ww[u, pos], self.wa[u, pos] = omega[u], alpha[u]
+            self.wn[u] += 1
+            m = min(self.wn[u], w)
+            order = [(self.wn[u] - m + i) % w for i in range(m)]
+            z = self.ww[u, order[0]]
+            kt, vt = self.wk[u, order[0]].copy(), self.wv[u, order[0]].copy()
+            for i in order[1:]:
+                a, om = self.wa[u, i], self.ww[u, i]
+                zn = a * z + om
+                kt = (a * kt * z + self.wk[u, i] * om) / zn
+                vt = (a * vt * z + self.wv[u, i] * om) / zn
+                z = zn
+            if alpha[u] == 0:
+                self.l[u] += 1
+            self.K[u, self.l[u] - 1], self.V[u, self.l[u] - 1] = kt, vt
+            self.z[u] = z
+
     # -- Sec. 2.1 attention over the compressed sequence ---------------------
     def attend(self, u, q_heads):
         """Softmax attention of the query heads q_heads [G, d] of unit u."""
@@ -216,7 +266,8 @@ class DMCOracle:
     """
 
     def __init__(self, num_layers, batch, num_q_heads, num_kv_heads, head_dim,
-                 max_slots, decision_bias=0.0, omega_src="lead", decision_src="per_head"):
+                 max_slots, decision_bias=0.0, omega_src="lead", decision_src="per_head",
+                 window=0):
         assert num_q_heads % num_kv_heads == 0
         assert decision_src in ("per_head", "shared_layer")
         self.L, self.B = int(num_layers), int(batch)
@@ -224,7 +275,7 @@ class DMCOracle:
         self.G = self.Hq // self.Hkv
         self.c, self.omega_src = float(np.float32(decision_bias)), omega_src
         self.decision_src = decision_src
-        self.layers = [LayerCache(self.B * self.Hkv, self.d, max_slots)
+        self.layers = [LayerCache(self.B * self.Hkv, self.d, max_slots, window)
                        for _ in range(self.L)]
 
     def _q0_groups(self, q0):

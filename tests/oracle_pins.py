@@ -462,8 +462,113 @@ def check_shared_layer_decisions(O):
         assert (l == l[:, :1]).all(), l
 
 
+def _run_window(O, k, v, q, w):
+    n, d = k.shape
+    G = q.shape[1]
+    orc = O.DMCOracle(1, 1, G, 1, d, max_slots=n, window=w)
+    outs, slots = [], []
+    for t in range(n):
+        o, s_ = orc.decode_step(0, q[t][None], k[t][None, None], v[t][None, None])
+        outs.append(o[0])
+        slots.append(int(s_[0, 0]))
+    return np.array(outs), np.array(slots), orc
+
+
+def check_window_segments(O):
+    """Window grouping (Sec. 3.3): every slot is the omega-weighted mean
+    (np.average) of the last min(w, length) tokens of its segment; z is the
+    omega sum of the open segment's last min(w, length) tokens; slot indices
+    are the segment indices.  w = 1 keeps each segment's last token."""
+    rng = np.random.default_rng(47)
+    n, d = 40, 6
+    for w in (1, 3, 12):
+        k = rng.standard_normal((n, d))
+        v = rng.standard_normal((n, d))
+        q = rng.standard_normal((n, 1, d))
+        k[:, 0] = _logits_for(rng.uniform(size=n) < 0.8, rng)   # long runs of accumulation
+        outs, slots, orc = _run_window(O, k, v, q, w)
+        alpha = (k[:, 0] > 0).astype(int)
+        alpha[0] = 0
+        assert slots.tolist() == (np.cumsum(1 - alpha) - 1).tolist()
+        starts = list(np.nonzero(alpha == 0)[0]) + [n]
+        omega = 1.0 / (1.0 + np.exp(-q[:, 0, 0]))
+        kh = k.copy()
+        kh[:, 0] = 0.0
+        K, V, l, z = orc.export(0)
+        assert int(l[0, 0]) == len(starts) - 1
+        for j, (a, b) in enumerate(zip(starts[:-1], starts[1:])):
+            lo = max(a, b - w)
+            _close(K[0, 0, j], np.average(kh[lo:b], axis=0, weights=omega[lo:b]), what=f"w{w} K{j}")
+            _close(V[0, 0, j], np.average(v[lo:b], axis=0, weights=omega[lo:b]), what=f"w{w} V{j}")
+            if w == 1:
+                _close(K[0, 0, j], kh[b - 1], what="w1 last token")
+        a, b = starts[-2], starts[-1]
+        assert abs(z[0, 0] - omega[max(a, b - w):b].sum()) < 1e-12
+
+
+def check_window_wide_is_exact(O):
+    """A window at least as long as the sequence changes nothing."""
+    rng = np.random.default_rng(53)
+    n, d, G = 30, 8, 2
+    k = rng.standard_normal((n, d))
+    v = rng.standard_normal((n, d))
+    q = rng.standard_normal((n, G, d))
+    o1, s1, _ = _run_window(O, k, v, q, n)
+    o2, s2, _ = _run_single_unit(O, k, v, q)
+    assert (s1 == s2).all()
+    _close(o1, o2, tol=1e-12, what="wide window")
+
+
+def windowed_unrolled_attention(k, v, omega, alpha, q, w):
+    """Training-time view with window grouping (Sec. 3.2 + Sec. 3.3): the
+    state of position j is the partial-accumulation recurrence over
+    positions max(0, j-w+1) .. j, started afresh at the first of them; query
+    i sees its own state and each state j < i with alpha_{j+1} = 0."""
+    n, d = k.shape
+    kt, vt = np.zeros_like(k), np.zeros_like(v)
+    for j in range(n):
+        j0 = max(0, j - w + 1)
+        z, ks, vs = omega[j0], k[j0].copy(), v[j0].copy()
+        for i in range(j0 + 1, j + 1):
+            zn = alpha[i] * z + omega[i]
+            ks = (alpha[i] * ks * z + k[i] * omega[i]) / zn
+            vs = (alpha[i] * vs * z + v[i] * omega[i]) / zn
+            z = zn
+        kt[j], vt[j] = ks, vs
+    out = np.zeros((n,) + q.shape[1:])
+    for i in range(n):
+        vis = [j for j in range(i) if alpha[j + 1] == 0] + [i]
+        qq = q[i].copy()
+        qq[:, 0] = 0.0
+        s = qq @ kt[vis].T / math.sqrt(d)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        out[i] = (p @ vt[vis]) / p.sum(axis=1, keepdims=True)
+    return out
+
+
+def check_window_bruteforce(O):
+    """Every decision pattern of a short sequence, windows 2 and 3: decode
+    outputs equal the windowed unrolled-state formulation."""
+    rng = np.random.default_rng(59)
+    n, d = 7, 4
+    for w in (2, 3):
+        for bits in itertools.product([0, 1], repeat=n - 1):
+            alpha = np.array((0,) + bits)
+            k = rng.standard_normal((n, d))
+            v = rng.standard_normal((n, d))
+            q = rng.standard_normal((n, 1, d))
+            k[:, 0] = _logits_for(alpha, rng)
+            outs, _, _ = _run_window(O, k, v, q, w)
+            kh = k.copy()
+            kh[:, 0] = 0.0
+            omega = 1.0 / (1.0 + np.exp(-q[:, 0, 0]))
+            ref = windowed_unrolled_attention(kh, v, omega, alpha, q, w)
+            _close(outs, ref, tol=1e-10, what=f"window {w} pattern {bits}")
+
+
 ALL_CHECKS = [check_worked_example, check_sigmoid_c5, check_exact_decisions,
               check_all_append_vanilla, check_all_accumulate, check_segments,
               check_avg_pool, check_bruteforce_unrolled, check_gqa_omega,
               check_permutation, check_prefill_matches_decode, check_prefill_attend,
-              check_uniform_weighting, check_shared_layer_decisions]
+              check_uniform_weighting, check_shared_layer_decisions, check_window_segments,
+              check_window_wide_is_exact, check_window_bruteforce]

@@ -40,6 +40,9 @@ MUTATIONS = {
                                   "        w = sigmoid(q0_group[..., 0])\n"),
     "shared_decision_own_head": ("            k0 = np.repeat(k0[:, :1], self.Hkv, axis=1)\n", ""),
     "shared_importance_own_group": ("            q0g = np.repeat(q0g[:, :1], self.Hkv, axis=1)\n", ""),
+    "window_never_resets": ("                a, om = self.wa[u, i], self.ww[u, i]",
+                            "                a, om = 1, self.ww[u, i]"),
+    "window_one_short": ("            m = min(self.wn[u], w)", "            m = min(self.wn[u], max(w - 1, 1))"),
 }
 
 
