@@ -95,7 +95,14 @@ typedef struct dmc_cache_config {
   int32_t max_prompt_len;    /* largest n for dmc_prefill_compress / dmc_prefill_attend;
                                 0 = max_slots_per_seq */
   int32_t decision_src;      /* dmc_decision_src */
-  int32_t reserved;          /* must be 0 */
+  int32_t window;            /* 0: exact Algorithm 1.  w in [1, 64]: the window-grouping
+                                approximation of Sec. 3.3 -- every step's partial
+                                accumulation runs over the last w tokens only, so the open
+                                slot is the omega-weighted mean of the last min(w, length)
+                                tokens of its segment and a closed slot keeps that of its
+                                segment's last w tokens.  Each unit then also keeps its open
+                                segment's last w raw tokens (key with element 0 zeroed,
+                                value, omega) in the workspace; the paper uses w = 12 */
 } dmc_cache_config;
 
 typedef struct dmc_cache dmc_cache; /* opaque host handle */
@@ -123,7 +130,8 @@ dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream);
  * token with k[0] > c merges into the open slot and every other token opens
  * a new one.  The result equals n sequential decode-step updates: slot s of
  * a unit is the omega-weighted mean of its segment's keys (element 0 zeroed)
- * and values, z is the omega sum of the last segment.
+ * and values, z is the omega sum of the last segment (with a window w: of
+ * the segment's last min(w, length) tokens, which the unit also keeps).
  *   k_dev, v_dev: logical [B, n, Hkv, d] of the config dtype; k_strides /
  *     v_strides give the element strides of the B, n and Hkv axes (the d axis
  *     is contiguous); base pointers 16-byte aligned, strides multiples of 8.
@@ -203,7 +211,9 @@ dmc_status dmc_cache_export(const dmc_cache *cache, int32_t layer, void *k_dense
  * taken from k_dense_dev / v_dense_dev [B, Hkv, dense_slots, d] and the
  * running sum z_dev[u] of its open slot.  Pages come from the pool.  Lengths
  * outside [0, min(dense_slots, max_slots_per_seq)] raise the device flag and
- * are treated as 0. */
+ * are treated as 0.  A cache configured with a window returns
+ * DMC_ERR_UNSUPPORTED: its open segment's raw tokens cannot be rebuilt from
+ * slots. */
 dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense_dev,
                             const void *v_dense_dev, int32_t dense_slots,
                             const int32_t *lengths_dev, const float *z_dev,

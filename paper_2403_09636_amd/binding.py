@@ -36,7 +36,7 @@ class CacheConfig(ctypes.Structure):
                 ("num_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int32),
                 ("page_size", c_int32), ("max_slots_per_seq", c_int32), ("num_pages", c_int64),
                 ("decision_bias", c_float), ("omega_src", c_int32), ("split_tile", c_int32),
-                ("max_prompt_len", c_int32), ("decision_src", c_int32), ("reserved", c_int32)]
+                ("max_prompt_len", c_int32), ("decision_src", c_int32), ("window", c_int32)]
 
 
 class DMCError(RuntimeError):
@@ -95,18 +95,18 @@ def check(status: int):
 def make_config(num_layers, batch, num_q_heads, num_kv_heads, head_dim, dtype="bf16",
                 page_size=32, max_slots_per_seq=4096, num_pages=None, decision_bias=0.0,
                 omega_src="lead", split_tile=0, max_prompt_len=0,
-                decision_src="per_head") -> CacheConfig:
+                decision_src="per_head", window=0) -> CacheConfig:
     """A dmc_cache_config; num_pages defaults to room for every unit at capacity.
 
     omega_src: 'lead' | 'group_mean' | 'uniform'; decision_src: 'per_head' |
-    'shared_layer' (DMC-HardC)."""
+    'shared_layer' (DMC-HardC); window: 0 (exact) or the window-grouping width."""
     units = num_layers * batch * num_kv_heads
     if num_pages is None:
         num_pages = units * -(-max_slots_per_seq // page_size)
     return CacheConfig(num_layers, batch, num_q_heads, num_kv_heads, head_dim,
                        DMC_FP32 if dtype in ("fp32", "float32") else DMC_BF16, page_size,
                        max_slots_per_seq, num_pages, decision_bias, OMEGA_SRC[omega_src],
-                       split_tile, max_prompt_len, DECISION_SRC[decision_src], 0)
+                       split_tile, max_prompt_len, DECISION_SRC[decision_src], window)
 
 
 def workspace_bytes(cfg: CacheConfig) -> int:

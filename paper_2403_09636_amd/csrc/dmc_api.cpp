@@ -95,13 +95,15 @@ dmc_status validate_config(const dmc_cache_config *c) {
     return fail(DMC_ERR_INVALID_ARG, "unknown omega_src %d", c->omega_src);
   if (c->decision_src != DMC_DECISION_PER_HEAD && c->decision_src != DMC_DECISION_SHARED_LAYER)
     return fail(DMC_ERR_INVALID_ARG, "unknown decision_src %d", c->decision_src);
-  if (c->reserved != 0) return fail(DMC_ERR_INVALID_ARG, "reserved config field must be 0");
+  if (c->window < 0) return fail(DMC_ERR_INVALID_ARG, "window must be >= 0");
+  if (c->window > dmc::kMaxWindow)
+    return fail(DMC_ERR_UNSUPPORTED, "window %d exceeds %d", c->window, dmc::kMaxWindow);
   if (c->split_tile < 0) return fail(DMC_ERR_INVALID_ARG, "split_tile must be >= 0");
   if (c->max_prompt_len < 0 || c->max_prompt_len > c->max_slots_per_seq)
     return fail(DMC_ERR_INVALID_ARG, "max_prompt_len must be in [0, max_slots_per_seq]");
   const int64_t units = int64_t(c->batch) * c->num_kv_heads;
   if (units > (int64_t(1) << 20)) return fail(DMC_ERR_UNSUPPORTED, "too many units per layer");
-  if (dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim) > kMaxDecodeLds)
+  if (dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim, c->window > 0) > kMaxDecodeLds)
     return fail(DMC_ERR_UNSUPPORTED,
                 "batch * num_kv_heads = %lld units exceed the decode kernel's LDS tile table",
                 static_cast<long long>(units));
@@ -126,6 +128,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.max_prompt = c.max_prompt_len > 0 ? c.max_prompt_len : c.max_slots_per_seq;
   L.prompt_chunks = (L.max_prompt + 63) / 64;
   L.carry_blocks = (L.max_prompt + 31) / 32;
+  L.window = c.window;
   L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
   // Grouped-query caches decode on matrix cores with value pages transposed.
   L.v_trans = c.dtype == DMC_BF16 && L.group >= 4 && c.page_size == 32;
@@ -148,6 +151,9 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.pf_count = take(U * size_t(L.prompt_chunks) * 4);
   L.pf_pagebase = take(U * 4);
   L.pf_carry = take(U * size_t(L.carry_blocks) * dmc::carry_stride(c.head_dim) * 4);
+  L.win = take(NL * U * size_t(L.window) * 2 * c.head_dim * es);
+  L.win_omega = take(NL * U * size_t(L.window) * 4);
+  L.win_len = take(L.window > 0 ? NL * U * 4 : 0);
   L.total = off;
   return L;
 }
@@ -178,6 +184,20 @@ int32_t *lens_of(const dmc_cache *c, int layer, int parity) {
   return at<int32_t>(c, c->lay.lens) + (size_t(parity) * c->cfg.num_layers + layer) * c->lay.units;
 }
 
+// Token-window ring of one layer (all null when the cache has no window).
+dmc::WindowState window_of(const dmc_cache *c, int layer) {
+  dmc::WindowState w{};
+  const dmc::Layout &L = c->lay;
+  w.window = L.window;
+  if (L.window > 0) {
+    const size_t units = size_t(L.units) * L.window;
+    w.ring = c->ws + L.win + size_t(layer) * units * 2 * c->cfg.head_dim * elem_bytes(c->cfg);
+    w.omega = at<float>(c, L.win_omega) + size_t(layer) * units;
+    w.seg_len = at<int32_t>(c, L.win_len) + size_t(layer) * L.units;
+  }
+  return w;
+}
+
 dmc_status check_layer(const dmc_cache *c, int32_t layer) {
   if (!c) return fail(DMC_ERR_INVALID_ARG, "cache is NULL");
   if (layer < 0 || layer >= c->cfg.num_layers)
@@ -199,6 +219,9 @@ dmc_status enqueue_reset(dmc_cache *c, hipStream_t s) {
     return hip_fail(e, "reset control block");
   if ((e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.meta), 0, 2 * U, s)) != hipSuccess)
     return hip_fail(e, "reset tile table");
+  if (c->lay.window > 0 &&
+      (e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.win_len), 0, NL * U, s)) != hipSuccess)
+    return hip_fail(e, "reset window lengths");
   for (auto &p : c->parity) p = 0;
   return DMC_OK;
 }
@@ -288,6 +311,7 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   p.slot_index = slot_index;
   p.partials = at<float>(cache, L.partials);
   p.meta = at<int32_t>(cache, L.meta);
+  p.win = window_of(cache, layer);
   p.c = c.decision_bias;
   p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(c.head_dim)));
   p.units = L.units;
@@ -364,6 +388,7 @@ dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const 
   p.count = at<int32_t>(cache, L.pf_count);
   p.page_base = at<int32_t>(cache, L.pf_pagebase);
   p.carry = nullptr;
+  p.win = window_of(cache, layer);
   p.c = c.decision_bias;
   p.n = n;
   p.units = L.units;
@@ -422,7 +447,8 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer, const void *k,
   if (c.dtype == DMC_BF16 && (int64_t(n) + c.page_size - 1) / c.page_size > dmc::kPromptMaxPages)
     return fail(DMC_ERR_UNSUPPORTED, "prompt of %d tokens exceeds %d pages per unit", n,
                 dmc::kPromptMaxPages);
-  p.carry = at<float>(cache, L.pf_carry);
+  // Windowed open states need no carry records (they span at most w tokens).
+  p.carry = L.window > 0 ? nullptr : at<float>(cache, L.pf_carry);
   dmc::PromptParams a{};
   a.pool = p.pool;
   a.page_bytes = p.page_bytes;
@@ -453,6 +479,7 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer, const void *k,
   a.max_prompt = L.max_prompt;
   a.prompt_chunks = L.prompt_chunks;
   a.carry_blocks = L.carry_blocks;
+  a.window = L.window;
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -526,6 +553,9 @@ dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense
     return fail(DMC_ERR_INVALID_ARG, "k_dense, v_dense, lengths and z must be non-NULL");
   if (!aligned16(k_dense) || !aligned16(v_dense))
     return fail(DMC_ERR_INVALID_ARG, "dense tensors must be 16-byte aligned");
+  if (cache->lay.window > 0)
+    return fail(DMC_ERR_UNSUPPORTED,
+                "a cache with a window keeps its open segments' raw tokens; slots cannot supply them");
   dmc::DenseParams p = dense_params(cache, layer, dense_slots);
   p.kd = const_cast<void *>(k_dense);
   p.vd = const_cast<void *>(v_dense);

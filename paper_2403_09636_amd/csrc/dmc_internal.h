@@ -30,7 +30,7 @@ struct Control {
 // Byte offsets of the workspace sections (all 256-byte aligned).
 struct Layout {
   size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_pagebase,
-      pf_carry;
+      pf_carry, win, win_omega, win_len;
   size_t total;
   int64_t page_bytes;     // 2 * P * d * elem_bytes (K rows, then V rows)
   int32_t units;          // B * Hkv per layer
@@ -41,7 +41,19 @@ struct Layout {
   int32_t max_prompt;     // prefill staging capacity (tokens)
   int32_t prompt_chunks;  // ceil(max_prompt / 64)
   int32_t carry_blocks;   // ceil(max_prompt / 32)
+  int32_t window;         // window-grouping width (0 = exact Algorithm 1)
   bool v_trans;           // value pages stored transposed (matrix-core decode)
+};
+
+// Window grouping: per unit, a ring of `window` raw tokens of its open
+// segment (token j of the segment in entry j mod window): a key row with
+// element 0 zeroed, then a value row, in the cache dtype; their omegas
+// (fp32) and the open segment's token count.
+struct WindowState {
+  char *ring;              // [U][window][2][d] of this layer
+  float *omega;            // [U][window]
+  int32_t *seg_len;        // [U]
+  int32_t window;          // 0 = no window
 };
 
 // Everything the decode kernel needs for one layer.
@@ -59,6 +71,7 @@ struct DecodeParams {
   int32_t *slot_index;     // optional [U]
   float *partials;         // [tiles, G, d + 4]
   int32_t *meta;           // [U, 2]: first partial record, record count (for the combine)
+  WindowState win;
   float c;                 // decision bias
   float scale_log2;        // log2(e) / sqrt(d)
   int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src, decision_src;
@@ -82,6 +95,7 @@ struct PrefillParams {
   int32_t *page_base;      // [U]
   float *carry;            // optional [U, carry_blocks, carry_stride]: open-segment sums at
                            // every 32-token boundary inside a segment (prompt attention)
+  WindowState win;
   float c;
   int32_t n, units, hkv, hq, maxpages, log2p, omega_src, max_prompt, prompt_chunks,
       carry_blocks, decision_src;
@@ -109,6 +123,7 @@ struct PromptParams {
   const float *carry;      // [U, carry_blocks, carry_stride(d)]
   float scale_log2;        // log2(e) / sqrt(d)
   int32_t n, units, hkv, hq, maxpages, log2p, max_prompt, prompt_chunks, carry_blocks;
+  int32_t window;          // window grouping: open states over the last `window` tokens
 };
 
 struct DenseParams {
@@ -140,6 +155,9 @@ hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillPa
 hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 
+// Largest window-grouping width.
+constexpr int kMaxWindow = 64;
+
 // Largest prompt, in pages per unit, of the matrix-core prompt attention
 // (its page-table slice is held in LDS).
 constexpr int kPromptMaxPages = 1024;
@@ -150,7 +168,8 @@ constexpr int kPromptMaxPages = 1024;
 hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
                                 const PromptParams &p, const Control *ctrl, hipStream_t s);
 
-// Dynamic LDS bytes of the decode kernel for a unit count / group / head dim.
-size_t decode_lds_bytes(int units, int group, int head_dim);
+// Dynamic LDS bytes of the decode kernel for a unit count / group / head dim
+// (and whether the cache has a window).
+size_t decode_lds_bytes(int units, int group, int head_dim, bool window);
 
 }  // namespace dmc

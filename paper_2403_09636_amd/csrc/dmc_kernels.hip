@@ -22,7 +22,6 @@
 namespace dmc {
 namespace {
 
-constexpr int kChunk = 32;  // max rows of a matrix-core chunk
 #ifndef DMC_VALU_CHUNK
 #define DMC_VALU_CHUNK 16
 #endif
@@ -51,6 +50,69 @@ constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
 // built (the page allocator's bump counter aside).
 // ---------------------------------------------------------------------------
 
+
+// Window grouping (Sec. 3.3): with the new token at position j of its
+// segment, the open slot is the omega-weighted mean of the segment's
+// positions j - m + 1 .. j, m = min(j + 1, w) -- the ring holds the earlier
+// ones (entry i mod w).  Vector-ALU layout: rows of LPR lanes, each lane a
+// 16-byte slice; the RPI row groups of the wave take every RPI-th ring entry
+// and their sums are added across groups.  On entry ck, cv hold the new
+// token's slice (key element 0 zeroed) and om its omega; on return they
+// hold the mean, and the omega sum of the window is returned.
+template <int ES, int LPR>
+__device__ __forceinline__ float window_mean_rows(const WindowState &w, int u, int j, int grp,
+                                                  int part, float *ck, float *cv, float om) {
+  using V = V16<ES>;
+  constexpr int VN = V::N, RB = LPR * 16, RPI = 64 / LPR, kBatch = 4;
+  const int W = w.window;
+  const int m = min(j + 1, W);
+  const char *ring = w.ring + int64_t(u) * W * 2 * RB + part * 16;
+  const float *wo = w.omega + int64_t(u) * W;
+  float sk[VN], sv[VN], zs = 0.0f;
+#pragma unroll
+  for (int e = 0; e < VN; ++e) sk[e] = sv[e] = 0.0f;
+  for (int i0 = j - m + 1 + grp; i0 < j; i0 += kBatch * RPI) {
+    uint4 kr[kBatch], vr[kBatch];
+    float wt[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int i = i0 + q * RPI;
+      const int ent = (i < j ? i : j - 1) % W;   // past the window: any entry, weight 0
+      kr[q] = ld16(ring + int64_t(ent) * 2 * RB);
+      vr[q] = ld16(ring + int64_t(ent) * 2 * RB + RB);
+      wt[q] = i < j ? wo[ent] : 0.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      float kf[VN], vf[VN];
+      V::unpack(kr[q], kf);
+      V::unpack(vr[q], vf);
+#pragma unroll
+      for (int e = 0; e < VN; ++e) {
+        sk[e] = fmaf(wt[q], kf[e], sk[e]);
+        sv[e] = fmaf(wt[q], vf[e], sv[e]);
+      }
+      zs += wt[q];
+    }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1) {
+#pragma unroll
+    for (int e = 0; e < VN; ++e) {
+      sk[e] += __shfl_xor(sk[e], o, 64);
+      sv[e] += __shfl_xor(sv[e], o, 64);
+    }
+    zs += __shfl_xor(zs, o, 64);
+  }
+  zs += om;
+  const float inv = 1.0f / zs;
+#pragma unroll
+  for (int e = 0; e < VN; ++e) {
+    ck[e] = fmaf(om, ck[e], sk[e]) * inv;
+    cv[e] = fmaf(om, cv[e], sv[e]) * inv;
+  }
+  return zs;
+}
 
 // Merge (m2, l2, a2) into (m, l, a); scores are in the log2 domain.
 template <int N>
@@ -125,7 +187,7 @@ __device__ __forceinline__ int unit_at(const int *s_off, int U, int pos) {
   return lo;
 }
 
-template <int ES, int D, int G>
+template <int ES, int D, int G, bool WIN>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   using V = V16<ES>;
   constexpr int VN = V::N;        // elements per 16-byte lane chunk
@@ -184,9 +246,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       // slot is attended to after the update, as merged or as it was.
       uint4 k_raw = make_uint4(0, 0, 0, 0), v_raw = k_raw, ok_raw = k_raw, ov_raw = k_raw;
       float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
-      int open_page = -1;
+      int open_page = -1, seg_len = 0;
       if (owner) {
         const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
+        if (WIN && l > 0) seg_len = p.win.seg_len[u];
         k0 = load_elem<ES>(p.k, int64_t(b * p.hkv + dg) * D);
         q0 = load_elem<ES>(p.q, int64_t(b * p.hq + dg * G) * D);
         k_raw = ld16(static_cast<const char *>(p.k) + (int64_t(u) * D + part * VN) * ES);
@@ -329,7 +392,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         int flag = 0, slot, page = open_page;
         bool has_cur = true;
         float znew;
-        if (alpha) {
+        if (WIN && alpha) {   // window grouping: mean of the last w tokens
+          slot = l - 1;
+          znew = window_mean_rows<ES, LPR>(p.win, u, seg_len, grp, part, ck, cv, om);
+        } else if (alpha) {
           float ok[VN], ov[VN];
           V::unpack(ok_raw, ok);
           V::unpack(ov_raw, ov);
@@ -371,6 +437,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
             }
           }
           // otherwise slot l shares the open slot's page
+        }
+        if (WIN && has_cur) {   // the token joins its segment's window ring
+          const int W = p.win.window, j = alpha ? seg_len : 0, ent = j % W;
+          if (grp == 0) {
+            uint4 kh = k_raw;
+            if (part == 0) kh.x &= ES == 2 ? 0xffff0000u : 0u;   // k_t[0] <- 0
+            char *er = p.win.ring + (int64_t(u) * W + ent) * 2 * RB + part * 16;
+            st16(er, kh);
+            st16(er + RB, v_raw);
+          }
+          if (lane == 0) {
+            p.win.omega[int64_t(u) * W + ent] = om;
+            p.win.seg_len[u] = j + 1;
+          }
         }
         if (has_cur) {
           const uint4 kp = V::pack(ck), vp = V::pack(cv);   // ck, cv become the stored values
@@ -424,6 +504,66 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   }
 }
 
+// Window grouping for the matrix-core decode: the mean of the segment's
+// positions j - m + 1 .. j (m = min(j + 1, w); ring entries, then the new
+// token from k, v with omega om) is formed in a vector layout -- lane owns
+// elements E lane .. E lane + E - 1 -- and left in this wave's LDS area
+// (fp32 key mean, then value mean) for the operand layout to pick up.
+// Returns the window's omega sum.
+template <int D>
+__device__ __forceinline__ float window_mean_lds(const DecodeParams &p, int u, int j, float om,
+                                                 float *lds) {
+  constexpr int E = D / 64, RB = D * 2, kBatch = 4;
+  const int lane = threadIdx.x & 63;
+  const int W = p.win.window;
+  const int m = min(j + 1, W);
+  const char *ring = p.win.ring + int64_t(u) * W * 2 * RB + lane * E * 2;
+  const float *wo = p.win.omega + int64_t(u) * W;
+  float sk[E], sv[E], zs = 0.0f;
+  {
+    float kf[E], vf[E];
+    load_e<2, E>(static_cast<const char *>(p.k) + int64_t(u) * RB + lane * E * 2, kf);
+    load_e<2, E>(static_cast<const char *>(p.v) + int64_t(u) * RB + lane * E * 2, vf);
+    if (lane == 0) kf[0] = 0.0f;   // k_t[0] <- 0
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      sk[e] = om * kf[e];
+      sv[e] = om * vf[e];
+    }
+  }
+  for (int i0 = j - m + 1; i0 < j; i0 += kBatch) {
+    float kf[kBatch][E], vf[kBatch][E], wt[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int i = i0 + q;
+      const int ent = (i < j ? i : j - 1) % W;   // past the window: any entry, weight 0
+      load_e<2, E>(ring + int64_t(ent) * 2 * RB, kf[q]);
+      load_e<2, E>(ring + int64_t(ent) * 2 * RB + RB, vf[q]);
+      wt[q] = i < j ? wo[ent] : 0.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        sk[e] = fmaf(wt[q], kf[q][e], sk[e]);
+        sv[e] = fmaf(wt[q], vf[q][e], sv[e]);
+      }
+      zs += wt[q];
+    }
+  }
+  zs += om;
+  const float inv = 1.0f / zs;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    lds[lane * E + e] = sk[e] * inv;
+    lds[D + lane * E + e] = sv[e] * inv;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  return zs;
+}
+
 // ---------------------------------------------------------------------------
 // Grouped-query decode on matrix cores (bf16, G >= 4, pages of 32 slots).
 //
@@ -442,7 +582,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
 // 16-byte load.  P enters the value product rounded to bf16; its row sum is
 // taken over the same rounded values.
 // ---------------------------------------------------------------------------
-template <int D, int G>
+template <int D, int G, bool WIN>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
   constexpr int NT = D / 16;      // 16-dim tiles of the value product
@@ -454,6 +594,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
   __shared__ int s_wsum[kWaves];
   const int U = p.units;
   int *s_off = reinterpret_cast<int *>(smem);
+  const size_t win_lds_off = align_up(size_t(U + 1) * 4, 16);   // windowed means, 2 D fp32 per wave
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, q = lane >> 4;      // MFMA column (head or dim) and k-group
   const int P = 1 << p.log2p;
@@ -596,11 +737,12 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
 
       // Owner: Algorithm 1 loads (issued after the stream to keep registers free).
       float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
-      int open_page = -1;
+      int open_page = -1, seg_len = 0;
       uint4 kt[KS], ko[KS];
       uint16_t vt[NT], vo[NT];
       if (owner) {
         const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
+        if (WIN && l > 0) seg_len = p.win.seg_len[u];
         k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
         q0 = load_elem<2>(p.q, int64_t(b * p.hq + dg * G) * D);
         const char *kp = static_cast<const char *>(p.k) + int64_t(u) * RB;
@@ -670,6 +812,14 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
             }
           }
         }
+        if (q == 0) kt[0].x &= 0xffff0000u;     // Algorithm 1: k_t[0] <- 0
+        // Window grouping: the open slot is the mean of its segment's last w tokens,
+        // formed in this wave's LDS area.
+        const bool windowed = WIN && alpha;
+        const float *wmean = reinterpret_cast<const float *>(smem + win_lds_off) + wave * 2 * D;
+        if (windowed)
+          znew = window_mean_lds<D>(p, u, seg_len, om,
+                                    reinterpret_cast<float *>(smem + win_lds_off) + wave * 2 * D);
         // Current key (lanes hold dims 32 ks + 8q .. +8) and value (dims 16 nt + n).
         uint4 kc[KS];
 #pragma unroll
@@ -677,8 +827,12 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
           float kf[8], of[8];
           V16<2>::unpack(kt[ks], kf);
           V16<2>::unpack(ko[ks], of);
-          if (ks == 0 && q == 0) kf[0] = 0.0f;            // Algorithm 1: k_t[0] <- 0
-          if (alpha) {
+          if (windowed) {
+            const float4 x0 = *reinterpret_cast<const float4 *>(wmean + 32 * ks + 8 * q);
+            const float4 x1 = *reinterpret_cast<const float4 *>(wmean + 32 * ks + 8 * q + 4);
+            kf[0] = x0.x; kf[1] = x0.y; kf[2] = x0.z; kf[3] = x0.w;
+            kf[4] = x1.x; kf[5] = x1.y; kf[6] = x1.z; kf[7] = x1.w;
+          } else if (alpha) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) kf[e] = (of[e] * zold + kf[e] * om) / znew;
           }
@@ -688,8 +842,26 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           float vf = __uint_as_float(uint32_t(vt[nt]) << 16);
-          if (alpha) vf = (__uint_as_float(uint32_t(vo[nt]) << 16) * zold + vf * om) / znew;
+          if (windowed) vf = wmean[D + 16 * nt + n];
+          else if (alpha) vf = (__uint_as_float(uint32_t(vo[nt]) << 16) * zold + vf * om) / znew;
           vc[nt] = static_cast<uint16_t>(bf16_bits(vf));
+        }
+        if (WIN && has_cur) {   // the token joins its segment's window ring
+          const int W = p.win.window, j = alpha ? seg_len : 0, ent = j % W;
+          char *er = p.win.ring + (int64_t(u) * W + ent) * 2 * RB;
+          if (n == 0) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) st16(er + ks * 64 + q * 16, kt[ks]);
+          }
+          if (q == 0) {
+            uint16_t *ev = reinterpret_cast<uint16_t *>(er + RB);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) ev[16 * nt + n] = vt[nt];
+          }
+          if (lane == 0) {
+            p.win.omega[int64_t(u) * W + ent] = om;
+            p.win.seg_len[u] = j + 1;
+          }
         }
         if (has_cur) {
           char *pg = p.pool + int64_t(page) * p.page_bytes;
@@ -1097,6 +1269,162 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
   if (t_stop >= nb && lane == 0) p.z[u] = zs;   // the unit's last segment
 }
 
+// Pass 3 with window grouping (Sec. 3.3), one wave per (unit, 64-token
+// chunk): every segment whose first token lies in the chunk becomes the
+// omega-weighted mean of its last min(w, length) tokens -- the state the
+// windowed partial accumulation reaches at the segment's end.  Only those
+// tokens are read: the wave lists, in order, the tokens of its segments that
+// lie within w of their segment's end (at most 64 in the chunk, plus up to w
+// of the last segment past the chunk end) and streams them in batches,
+// flushing a slot whenever the segment changes.  The wave holding the
+// unit's last segment also fills the unit's token ring (position j of the
+// segment in entry j mod w) and writes z and the open segment's length.
+// Slot indices of every token come from the segment-start mask.
+template <int ES, int D>
+__global__ __launch_bounds__(kThreads) void prefill_window_kernel(PrefillParams p) {
+  constexpr int E = D / 64;  // elements per lane
+  constexpr int RB = D * ES;
+  constexpr int kRows = 8;   // token rows in flight per wave
+  __shared__ int s_list[kWaves][64 + kMaxWindow];
+  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ch = blockIdx.x * kWaves + wave;
+  const int tlo = ch * 64;
+  if (tlo >= p.n) return;
+  const int pb = p.page_base[u];
+  if (pb < 0) return;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int nb = prompt_len(p, b, false);
+  if (tlo >= nb) return;
+  const uint8_t *al = p.alpha + int64_t(u) * p.max_prompt;
+  const float *om = p.omega + int64_t(u) * p.max_prompt;
+  auto starts = [&](int wb) -> unsigned long long {
+    const int t = wb + lane;
+    return __ballot(t < nb && al[t] == 0);
+  };
+  const unsigned long long m0 = starts(tlo);
+  if (m0 == 0) return;
+  int before = 0;
+  for (int j = lane; j < ch; j += 64) before += p.count[int64_t(u) * p.prompt_chunks + j];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o, 64);
+  const int t0 = tlo + __ffsll(static_cast<long long>(m0)) - 1;
+  int t_stop = nb;
+  for (int wb = tlo + 64; wb < nb; wb += 64) {
+    const unsigned long long mk = starts(wb);
+    if (mk) {
+      t_stop = wb + __ffsll(static_cast<long long>(mk)) - 1;
+      break;
+    }
+  }
+  const int W = p.win.window;
+  const int nseg = __popcll(m0);
+  const int a_last = tlo + 63 - __clzll(static_cast<long long>(m0));   // start of the last segment
+  // Segment of token t in [t0, t_stop) (relative to `before`).
+  auto seg_of = [&](int t) {
+    const int rel = t - tlo;
+    return rel < 64 ? __popcll(m0 & (rel == 63 ? ~0ull : ((2ull << rel) - 1ull))) - 1 : nseg - 1;
+  };
+
+  // Slot index of every token of the chunk's segments.
+  if (p.slot_index) {
+    for (int tb = t0; tb < t_stop; tb += 64) {
+      const int t = tb + lane;
+      if (t < t_stop) p.slot_index[int64_t(u) * p.n + t] = before + seg_of(t);
+    }
+  }
+
+  // Token list: chunk tokens within w of their segment's end, then the last
+  // segment's tokens past the chunk end that are within w of t_stop.
+  int total;
+  {
+    const int t = tlo + lane;
+    const unsigned long long later = m0 & (lane == 63 ? 0ull : (~0ull << (lane + 1)));
+    const int seg_end = later ? tlo + __ffsll(static_cast<long long>(later)) - 1 : t_stop;
+    const bool keep = t >= t0 && t < t_stop && t >= seg_end - W;
+    const unsigned long long mk = __ballot(keep);
+    if (keep) s_list[wave][__popcll(mk & ((1ull << lane) - 1ull))] = t;
+    const int nin = __popcll(mk);
+    const int tail0 = max(tlo + 64, t_stop - W);
+    const int ntail = max(0, t_stop - tail0);   // <= W
+    for (int i = lane; i < ntail; i += 64) s_list[wave][nin + i] = tail0 + i;
+    total = nin + ntail;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+
+  const int P = 1 << p.log2p;
+  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
+  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
+  const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
+  const bool last_unit_seg = t_stop >= nb;   // the chunk's last segment is the unit's last
+  char *ring = p.win.ring + int64_t(u) * W * 2 * RB + lane * E * ES;
+  float *ring_w = p.win.omega + int64_t(u) * W;
+  int s = -1;
+  float ak[E], av[E], zs = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+  auto flush = [&]() {   // write slot before + s = sums / zs
+    const int sl = before + s;
+    const float inv = 1.0f / zs;
+    float kq[E], vq[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      kq[e] = ak[e] * inv;
+      vq[e] = av[e] * inv;
+    }
+    char *row = p.pool + int64_t(pb + (sl >> p.log2p)) * p.page_bytes + int64_t(sl & (P - 1)) * RB +
+                lane * E * ES;
+    store_e<ES, E>(row, kq);
+    store_e<ES, E>(row + int64_t(P) * RB, vq);
+    if (lane == 0 && (sl & (P - 1)) == 0)
+      p.ptab[int64_t(u) * p.maxpages + (sl >> p.log2p)] = pb + (sl >> p.log2p);
+  };
+  for (int i0 = 0; i0 < total; i0 += kRows) {
+    const int cnt = min(kRows, total - i0);
+    int tk[kRows];
+    float kk[kRows][E], vv[kRows][E], ww[kRows];
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      tk[j] = s_list[wave][i0 + min(j, cnt - 1)];
+      load_e<ES, E>(kbase + tk[j] * kst, kk[j]);
+      load_e<ES, E>(vbase + tk[j] * vst, vv[j]);
+      ww[j] = om[tk[j]];
+    }
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      if (j < cnt) {
+        const int sj = seg_of(tk[j]);
+        if (sj != s) {   // the next segment's window begins
+          if (s >= 0) flush();
+          s = sj;
+          zs = 0.0f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+        }
+        if (lane == 0) kk[j][0] = 0.0f;   // k_t[0] <- 0
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          ak[e] = fmaf(ww[j], kk[j][e], ak[e]);
+          av[e] = fmaf(ww[j], vv[j][e], av[e]);
+        }
+        zs += ww[j];
+        if (last_unit_seg && sj == nseg - 1) {   // the unit's open segment: fill its ring
+          const int ent = (tk[j] - a_last) % W;
+          store_e<ES, E>(ring + int64_t(ent) * 2 * RB, kk[j]);
+          store_e<ES, E>(ring + int64_t(ent) * 2 * RB + RB, vv[j]);
+          if (lane == 0) ring_w[ent] = ww[j];
+        }
+      }
+    }
+  }
+  flush();
+  if (last_unit_seg && lane == 0) {
+    p.z[u] = zs;
+    p.win.seg_len[u] = t_stop - a_last;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Dense <-> paged copies (import / export) and small utilities.
 // ---------------------------------------------------------------------------
@@ -1230,18 +1558,25 @@ hipError_t launch_transpose(char *pool, int64_t page_bytes, const Control *ctrl,
   return hipGetLastError();
 }
 
+template <int ES, int D, int G, bool WIN>
+void launch_decode_kernel(const DecodeParams &p, int grid, bool vt, size_t lds, hipStream_t s) {
+  if constexpr (ES == 2 && G >= 4) {
+    if (vt) {
+      hipLaunchKernelGGL((decode_mfma_kernel<D, G, WIN>), dim3(grid), dim3(kThreads), lds, s, p);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN>), dim3(grid), dim3(kThreads), lds, s, p);
+}
+
 template <int ES, int D, int G>
 hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) {
-  const size_t lds = decode_lds_bytes(p.units, G, D);
-  if constexpr (ES == 2 && G >= 4) {
-    if (vt)
-      hipLaunchKernelGGL((decode_mfma_kernel<D, G>), dim3(grid), dim3(kThreads), lds, s, p);
-    else
-      hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
-  } else {
-    if (vt) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((decode_kernel<ES, D, G>), dim3(grid), dim3(kThreads), lds, s, p);
-  }
+  const size_t lds = decode_lds_bytes(p.units, G, D, p.win.window > 0);
+  if (vt && !(ES == 2 && G >= 4)) return hipErrorInvalidValue;
+  if (p.win.window > 0)
+    launch_decode_kernel<ES, D, G, true>(p, grid, vt, lds, s);
+  else
+    launch_decode_kernel<ES, D, G, false>(p, grid, vt, lds, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int batch = p.units / p.hkv;
@@ -1277,8 +1612,12 @@ hipError_t prefill_impl(const PrefillParams &p, bool vt, hipStream_t s) {
   e = hipGetLastError();
   if (e != hipSuccess || p.n == 0) return e;
   const int nch = (p.n + 63) / 64;
-  hipLaunchKernelGGL((prefill_reduce_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
-                     dim3(kThreads), 0, s, p);
+  if (p.win.window > 0)
+    hipLaunchKernelGGL((prefill_window_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
+                       dim3(kThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL((prefill_reduce_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
+                       dim3(kThreads), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess || !vt) return e;
   return launch_transpose<D>(p.pool, p.page_bytes, p.ctrl, s);
@@ -1312,10 +1651,11 @@ hipError_t export_impl(const DenseParams &p, bool vt, hipStream_t s) {
 
 }  // namespace
 
-size_t decode_lds_bytes(int units, int group, int head_dim) {
+size_t decode_lds_bytes(int units, int group, int head_dim, bool window) {
   (void)group;
-  (void)head_dim;
-  return align_up(size_t(units + 1) * 4, 16);
+  // slot-space prefix [units + 1]; with a window, 2 * head_dim fp32 per wave
+  // for the matrix-core decode's windowed means
+  return align_up(size_t(units + 1) * 4, 16) + (window ? size_t(kWaves) * 2 * head_dim * 4 : 0);
 }
 
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s) {

@@ -128,6 +128,82 @@ __device__ __forceinline__ void walk_open_state(const PromptParams &p, int u, in
   }
 }
 
+// Window grouping (Sec. 3.3): the open state of token t is the omega-
+// weighted mean of its segment's tokens max(segment start, t - w + 1) .. t.
+// Same interface as walk_open_state.  The walk starts at the 8-aligned token
+// at or below a - w + 1 with empty sums (no carry records: a window never
+// reaches further back), adds each token, restarts at segment starts and
+// removes the token that leaves the window (t - w, when it lies in the
+// current segment and was added), so the sums always cover the window.
+template <int ES, int D, typename Snap, typename BatchEnd>
+__device__ __forceinline__ void walk_window_state(const PromptParams &p, int u, int b, int g,
+                                                  int a, int cnt, Snap &&snap,
+                                                  BatchEnd &&batch_end) {
+  constexpr int E = D / 64;
+  constexpr int kRows = 8;
+  const int lane = threadIdx.x & 63;
+  const int W = p.window;
+  const int bs = max(a - W + 1, 0) & ~7, end = a + cnt;
+  const uint8_t *al = p.alpha + int64_t(u) * p.max_prompt;
+  const float *om = p.omega + int64_t(u) * p.max_prompt;
+  float ak[E], av[E], zs = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+  int first = bs;   // first token in the sums: the walk's start or the segment's
+  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
+  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
+  const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
+  for (int t0 = bs; t0 < end; t0 += kRows) {
+    float kk[kRows][E], vv[kRows][E], ww[kRows];
+    float ko[kRows][E], vo[kRows][E], wo[kRows];
+    bool st[kRows];
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      const int tj = min(t0 + j, end - 1);
+      const int to = max(tj - W, 0);
+      load_e<ES, E>(kbase + tj * kst, kk[j]);
+      load_e<ES, E>(vbase + tj * vst, vv[j]);
+      load_e<ES, E>(kbase + to * kst, ko[j]);
+      load_e<ES, E>(vbase + to * vst, vo[j]);
+      ww[j] = om[tj];
+      wo[j] = om[to];
+      st[j] = al[tj] == 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+      const int tj = t0 + j;
+      if (tj < end) {
+        if (st[j]) {
+          zs = 0.0f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
+          first = tj;
+        }
+        if (lane == 0) {   // k_t[0] <- 0
+          kk[j][0] = 0.0f;
+          ko[j][0] = 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          ak[e] = fmaf(ww[j], kk[j][e], ak[e]);
+          av[e] = fmaf(ww[j], vv[j][e], av[e]);
+        }
+        zs += ww[j];
+        if (tj - W >= first) {   // token tj - W leaves the window
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            ak[e] = fmaf(-wo[j], ko[j][e], ak[e]);
+            av[e] = fmaf(-wo[j], vo[j][e], av[e]);
+          }
+          zs -= wo[j];
+        }
+        if (tj >= a) snap(tj, ak, av, zs);
+      }
+    }
+    batch_end(t0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 on matrix cores.  One workgroup = 4 waves = one unit's 128 query
 // columns (token-major: column c is token c / G, head c % G of the group);
@@ -306,9 +382,7 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   if (cnt > 0) {
     float *stage = reinterpret_cast<float *>(smem) + wave * STAGE;
     constexpr int E = D / 64;
-    walk_open_state<2, D>(
-        p, u, b, g, a, cnt,
-        [&](int t, const float *ak, const float *av, float zs) {
+    auto snap = [&](int t, const float *ak, const float *av, float zs) {
           const float inv = 1.0f / zs;
           float *row = stage + (t & 7) * 2 * D;
 #pragma unroll
@@ -316,8 +390,8 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
             row[lane * E + e] = ak[e] * inv;
             row[D + lane * E + e] = av[e] * inv;
           }
-        },
-        [&](int t0) {
+        };
+    auto batch_end = [&](int t0) {
           if (t0 + 8 <= a) return;   // nothing staged in this batch
           wave_lds_sync();
           const int t = a + tok;
@@ -358,7 +432,11 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
               }
           }
           wave_lds_sync();
-        });
+        };
+    if (p.window > 0)
+      walk_window_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
+    else
+      walk_open_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
   }
   __syncthreads();   // slot limits published; staging area free again
 
@@ -614,9 +692,7 @@ __global__ __launch_bounds__(kThreads) void prompt_valu_kernel(PromptParams p, i
   int seg = -1, lim[TG];
   if (cnt > 0) {
     seg = token_slots(p, u, a, cnt);
-    walk_open_state<ES, D>(
-        p, u, b, g, a, cnt,
-        [&](int t, const float *ak, const float *av, float zs) {
+    auto snap = [&](int t, const float *ak, const float *av, float zs) {
           const float inv = 1.0f / zs;
 #pragma unroll
           for (int r = 0; r < R; ++r) {
@@ -628,8 +704,11 @@ __global__ __launch_bounds__(kThreads) void prompt_valu_kernel(PromptParams p, i
 #pragma unroll
             for (int e = 0; e < E; ++e) acc[r][e] = av[e] * inv;
           }
-        },
-        [](int) {});
+        };
+    if (p.window > 0)
+      walk_window_state<ES, D>(p, u, b, g, a, cnt, snap, [](int) {});
+    else
+      walk_open_state<ES, D>(p, u, b, g, a, cnt, snap, [](int) {});
   }
   int hi = 0;
 #pragma unroll

@@ -58,13 +58,14 @@ class Pair:
 
     def __init__(self, L, B, Hq, Hkv, d, dtype="bf16", page_size=32, max_slots=512,
                  num_pages=None, bias=0.0, omega_src="lead", split_tile=0, max_prompt_len=0,
-                 decision_src="per_head"):
+                 decision_src="per_head", window=0):
         import paper_2403_09636_amd as P
         self.cfg = P.make_config(L, B, Hq, Hkv, d, dtype, page_size, max_slots, num_pages, bias,
-                                 omega_src, split_tile, max_prompt_len, decision_src)
+                                 omega_src, split_tile, max_prompt_len, decision_src, window)
         self.gpu = P.DMCCache(self.cfg, device="cuda")
         self.orc = oracle.DMCOracle(L, B, Hq, Hkv, d, max_slots, decision_bias=bias,
-                                    omega_src=omega_src, decision_src=decision_src)
+                                    omega_src=omega_src, decision_src=decision_src,
+                                    window=window)
         self.dtype, self.B, self.Hq, self.Hkv, self.d = dtype, B, Hq, Hkv, d
 
     def decode(self, layer, q, k, v, check_out=True):

@@ -62,7 +62,8 @@ def test_workspace_bytes(P):
     ("page_size", 4, "page_size"), ("dtype", 7, "dtype"), ("num_pages", 0, "num_pages"),
     ("num_pages", 1 << 31, "num_pages"), ("max_slots_per_seq", 0, "max_slots"),
     ("omega_src", 5, "omega"), ("split_tile", -1, "split_tile"), ("max_prompt_len", 99999, "prompt"),
-    ("decision_src", 2, "decision_src"), ("reserved", 1, "reserved"), ("page_size", 131072, "page_size"),
+    ("decision_src", 2, "decision_src"), ("window", -1, "window"), ("window", 65, "window"),
+    ("page_size", 131072, "page_size"),
     ("batch", 0, ">= 1"), ("num_q_heads", 48, "group"),
 ])
 def test_invalid_config(P, field, value, msg):
