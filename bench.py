@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--prompt", action="store_true",
                     help="measure prompt-phase attention (dmc_prefill_attend) instead of decode")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
+    ap.add_argument("--window", type=int, default=0,
+                    help="window-grouping width (Sec. 3.3); prefilled workloads only")
     ap.add_argument("--calib-copy", action="store_true",
                     help="finish with plain 1 GiB device copies (counter calibration)")
     return ap.parse_args()
@@ -58,6 +60,47 @@ def algorithmic_bytes(lens_before, lens_after, w, page):
     la = lens_after.astype(np.int64)
     per = 2 * d * s * lb + 2 * d * s + (2 * G + 2) * d * s + 16 + 4 * ((la + page - 1) // page)
     return int(per.sum())
+
+
+def window_bytes(alpha, seg_len, w, window):
+    """Extra algorithmic bytes of one windowed decode step over units:
+    an accumulating token reads the min(seg_len + 1, window) - 1 earlier
+    window tokens of its segment (key, value rows and omega); every token is
+    written to the ring (rows and omega); the segment length is read and
+    written (8 B)."""
+    row = 2 * w.head_dim * w.elem_bytes + 4
+    reads = np.where(alpha == 1, np.minimum(seg_len + 1, window) - 1, 0).astype(np.int64)
+    return int((reads * row).sum() + alpha.size * (row + 8))
+
+
+def segment_lengths_after_prompt(k0, prompt_len):
+    """Open-segment length of every unit after a prompt whose decision
+    neurons are k0 [B, n, H] (first token appends, alpha = k0 > 0)."""
+    app = ~(k0 > 0.0)
+    app[:, 0, :] = True
+    last = prompt_len - 1 - np.argmax(app[:, ::-1, :], axis=1)   # index of the last append
+    return (prompt_len - last).astype(np.int64)                     # [B, H]
+
+
+def windowed_prompt_reads(k0, window):
+    """Prompt tokens a windowed compaction needs: per segment, its last
+    min(window, length) tokens."""
+    B, n, H = k0.shape
+    app = ~(k0 > 0.0)
+    app[:, 0, :] = True
+    seg = np.cumsum(app, axis=1)                                   # segment ids 1..l per unit
+    # distance of each token to its segment's end = tokens after it in the same segment
+    rev = seg[:, ::-1, :]
+    # position from the end within the segment: count of equal ids after each token
+    pos_from_end = np.zeros_like(seg)
+    run = np.zeros((B, H), dtype=np.int64)
+    prev = np.full((B, H), -1)
+    for t in range(n):
+        cur = rev[:, t, :]
+        run = np.where(cur == prev, run + 1, 0)
+        pos_from_end[:, n - 1 - t, :] = run
+        prev = cur
+    return int((pos_from_end < window).sum())
 
 
 def profiled_traffic(workload):
@@ -142,7 +185,7 @@ def bench_prompt(args):
     torch.cuda.set_device(dev)
     n = w.prompt_len
     cfg = P.make_config(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
-                        w.page_size, n, None, 0.0, "lead", 0, n)
+                        w.page_size, n, None, 0.0, "lead", 0, n, window=args.window)
     cache = P.DMCCache(cfg, device=dev)
     k, v, q = W.prompt_full_torch(w, 0, dev)
     out = torch.empty_like(q)
@@ -183,7 +226,7 @@ def bench_prompt(args):
         "data": "synthetic",
         "config": {"workload": w.name, "layers": 1, "batch": w.batch, "q_heads": w.num_q_heads,
                    "kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "prompt": n,
-                   "page_size": w.page_size,
+                   "page_size": w.page_size, "window": args.window,
                    "global_cr": round(float(n * lens.size / lens.sum()), 3)},
         "roofline": {"bound": "mfma", "achieved": round(flops / (t_kernel * 1e-3) / 1e12, 1),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -212,6 +255,11 @@ def main():
     import workloads as W
 
     w = W.WORKLOADS[args.workload]
+    if args.window and w.cache_kind == "precompressed":
+        print(f"bench.py: workload {w.name} imports pre-compressed slots, which a windowed "
+              "cache cannot take (its raw token windows are unknown); use a prefilled "
+              "workload with --window", file=sys.stderr)
+        sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     K, Wm = args.steps, args.warmup
@@ -224,9 +272,10 @@ def main():
     pages = W.pool_pages(w, total_steps)
     cfg = P.make_config(w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim,
                         w.dtype, P_SIZE, max_slots, pages, 0.0, "lead", args.split_tile,
-                        w.prompt_len if w.cache_kind == "prefill" else 0)
+                        w.prompt_len if w.cache_kind == "prefill" else 0, window=args.window)
     cache = P.DMCCache(cfg, device=dev)
     prefill_ms = []
+    seg_len0, prompt_reads = [], 0   # window bookkeeping (host side, from the decisions)
     for layer in range(w.num_layers):
         if w.cache_kind == "precompressed":
             Kd, Vd, lt, zt = W.precompressed_torch(w, layer, dev)
@@ -234,6 +283,11 @@ def main():
             del Kd, Vd
         else:
             k, v, q0 = W.prompt_torch(w, layer, dev)
+            if args.window:
+                k0p = k[..., 0].float().cpu().numpy()
+                seg_len0.append(segment_lengths_after_prompt(k0p, w.prompt_len))
+                if layer == 0:
+                    prompt_reads = windowed_prompt_reads(k0p, args.window)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             cache.prefill(layer, k, v, q0)
@@ -254,10 +308,13 @@ def main():
     k0 = np.stack([np.stack([inputs[s][l][1][:, :, 0].float().cpu().numpy()
                              for l in range(w.num_layers)]) for s in range(total_steps)])
     lens_seq = [lens0]
+    seg_seq = [np.stack(seg_len0)] if args.window else None
     for s in range(total_steps):
         prev = lens_seq[-1]
         app = ~((k0[s] > 0.0) & (prev > 0))
         lens_seq.append(prev + app.astype(prev.dtype))
+        if args.window:
+            seg_seq.append(np.where(app, 1, seg_seq[-1] + 1))
     setup_s = time.time() - t_setup
 
     stream = torch.cuda.current_stream()
@@ -290,6 +347,9 @@ def main():
     for s in range(Wm, total_steps):
         for l in range(w.num_layers):
             alg += algorithmic_bytes(lens_seq[s][l], lens_seq[s + 1][l], w, P_SIZE)
+            if args.window:
+                alpha = (lens_seq[s + 1][l] == lens_seq[s][l]).astype(np.int64)
+                alg += window_bytes(alpha, seg_seq[s][l], w, args.window)
     final = np.stack([cache.lengths(l).cpu().numpy() for l in range(w.num_layers)])
     assert (final == lens_seq[-1]).all(), "device lengths differ from the decision count"
     alg_per_launch = alg / n_launch
@@ -307,7 +367,8 @@ def main():
                    "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
                    "context": w.prompt_len, "page_size": P_SIZE,
                    "global_cr": round(float(w.prompt_len * lens0.size / lens0.sum()), 3),
-                   "split_tile": cache.cfg.split_tile, "parallelism": "none (1 GPU)"},
+                   "split_tile": cache.cfg.split_tile, "window": args.window,
+                   "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic(w.name),
@@ -320,6 +381,9 @@ def main():
         n = w.prompt_len
         rd = w.batch * w.num_kv_heads * n * 2 * w.head_dim * w.elem_bytes
         wr = int(lens0[0].sum()) * 2 * w.head_dim * w.elem_bytes
+        if args.window:   # only each segment's last w tokens are read; the ring is written
+            rd = prompt_reads * 2 * w.head_dim * w.elem_bytes
+            wr += int(np.minimum(seg_seq[0][0], args.window).sum()) * (2 * w.head_dim * w.elem_bytes + 4)
         res["prefill"] = {"avg_layer_ms": round(float(np.mean(prefill_ms)), 3),
                           "alg_GBps": round((rd + wr) / (np.mean(prefill_ms) * 1e-3) / 1e9, 1)}
     if not args.no_cpu_baseline:

@@ -101,3 +101,25 @@ def test_bench_refuses_more_than_one_gpu(n):
                          text=True, cwd=__import__("os").path.dirname(__import__("os").path.dirname(
                              __import__("os").path.abspath(__file__))))
     assert res.returncode == 2 and "one GPU" in res.stderr
+
+
+def test_bench_window_bookkeeping():
+    """The benchmark's host-side window accounting (open-segment lengths
+    after a prompt, prompt tokens a windowed compaction reads) against a
+    per-unit loop over the segments."""
+    import bench
+    rng = np.random.default_rng(0)
+    for _ in range(20):
+        B, n, H = 2, 50, 3
+        k0 = rng.standard_normal((B, n, H)) + rng.uniform(-1, 2)
+        w = int(rng.integers(1, 15))
+        ref_sl = np.zeros((B, H), int)
+        ref_reads = 0
+        for b in range(B):
+            for h in range(H):
+                starts = [0] + [t for t in range(1, n) if not k0[b, t, h] > 0]
+                ends = starts[1:] + [n]
+                ref_sl[b, h] = ends[-1] - starts[-1]
+                ref_reads += sum(min(w, e - s) for s, e in zip(starts, ends))
+        assert (bench.segment_lengths_after_prompt(k0, n) == ref_sl).all()
+        assert bench.windowed_prompt_reads(k0, w) == ref_reads
