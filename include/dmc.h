@@ -227,6 +227,62 @@ dmc_status dmc_cache_check(dmc_cache *cache, dmc_stream_t stream);
 /* Synchronise `stream` and return the number of pool pages handed out. */
 dmc_status dmc_cache_pages_used(dmc_cache *cache, int64_t *pages_out, dmc_stream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Training-time DMC attention of one layer (Sec. 3.2 "Training", Sec. 3.3
+ * window grouping, and the masking appendix).  Forward and backward over a
+ * whole sequence, for continued pre-training that teaches a model DMC:
+ *   - decisions relaxed by Gumbel-sigmoid: alpha_t = sigmoid((k_t[0] - c +
+ *     g_t) / tau), g_t logistic noise drawn by the caller (noise_dev);
+ *   - importance omega_t = sigmoid(q_t[0]) of the group's first query head
+ *     (floored at 2^-100), or 1 with DMC_OMEGA_UNIFORM;
+ *   - unrolled states: every position j keeps the partial accumulation
+ *     (Sec. 3.2) of its last w tokens, started afresh at the window's first
+ *     token, with continuous alpha; keys enter with element 0 zeroed;
+ *   - query i attends to states j <= i with the additive mask
+ *     log(1 - alpha_{j+1}) for j < i and 0 for j = i, scores over elements
+ *     1..d-1 of q and the state, scaled by 1/sqrt(d).
+ * Layouts: q, out, dout, dq [B, n, Hq, d]; k, v, dk, dv [B, n, Hkv, d]; all
+ * contiguous in the config dtype, 16-byte aligned.  noise, alpha, dalpha:
+ * fp32 [B, n, Hkv] contiguous.  The workspace (caller-owned device memory,
+ * 256-byte aligned, dmc_train_workspace_bytes) carries what the forward saves
+ * for the backward (states, decisions, softmax statistics); pass the same
+ * workspace, untouched, to the backward of the same inputs.
+ * ------------------------------------------------------------------------- */
+typedef struct dmc_train_config {
+  int32_t batch;
+  int32_t seq_len;           /* n >= 1 */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;      /* G = num_q_heads / num_kv_heads in {1,2,4,8} */
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t dtype;             /* dmc_dtype of q, k, v, out and the gradients */
+  float decision_bias;       /* c; the paper uses 5 */
+  float temperature;         /* tau > 0; the paper uses 0.1 */
+  int32_t window;            /* w in [1, 64]; the paper uses 12 */
+  int32_t omega_src;         /* DMC_OMEGA_LEAD_QHEAD or DMC_OMEGA_UNIFORM */
+} dmc_train_config;
+
+/* Workspace bytes for a training configuration (0 if invalid). */
+size_t dmc_train_workspace_bytes(const dmc_train_config *cfg);
+
+/* Forward: out_dev [B, n, Hq, d] and, when alpha_dev is not NULL, the relaxed
+ * decisions alpha [B, n, Hkv] (fp32; what the compression loss of Sec. 3.2
+ * sums).  Fills the workspace for dmc_train_backward. */
+dmc_status dmc_train_forward(const dmc_train_config *cfg, const void *q_dev, const void *k_dev,
+                             const void *v_dev, const float *noise_dev, void *out_dev,
+                             float *alpha_dev, void *workspace_dev, size_t workspace_bytes,
+                             dmc_stream_t stream);
+
+/* Backward: gradients of sum(out * dout) + sum(alpha * dalpha) with respect
+ * to q, k and v (dalpha_dev may be NULL), given the forward's inputs and
+ * outputs and its workspace.  dq, dk, dv are written in full (the decision
+ * and importance neurons k[0], q[0] get their gradients through alpha and
+ * omega).  Outputs must not overlap the inputs. */
+dmc_status dmc_train_backward(const dmc_train_config *cfg, const void *q_dev, const void *k_dev,
+                              const void *v_dev, const float *noise_dev, const void *out_dev,
+                              const void *dout_dev, const float *dalpha_dev, void *dq_dev,
+                              void *dk_dev, void *dv_dev, void *workspace_dev,
+                              size_t workspace_bytes, dmc_stream_t stream);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *dmc_last_error(void);
 

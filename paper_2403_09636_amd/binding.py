@@ -27,7 +27,8 @@ STATUS_NAMES = {0: "DMC_OK", 1: "DMC_ERR_INVALID_ARG", 2: "DMC_ERR_UNSUPPORTED",
 #: Every entry point declared in include/dmc.h.
 EXPORTS = ("dmc_cache_workspace_bytes", "dmc_cache_alloc", "dmc_cache_free", "dmc_cache_reset",
            "dmc_prefill_compress", "dmc_prefill_attend", "dmc_decode_step", "dmc_cache_lengths", "dmc_cache_export",
-           "dmc_cache_import", "dmc_cache_check", "dmc_cache_pages_used", "dmc_last_error")
+           "dmc_cache_import", "dmc_cache_check", "dmc_cache_pages_used", "dmc_last_error",
+           "dmc_train_workspace_bytes", "dmc_train_forward", "dmc_train_backward")
 
 
 class CacheConfig(ctypes.Structure):
@@ -37,6 +38,14 @@ class CacheConfig(ctypes.Structure):
                 ("page_size", c_int32), ("max_slots_per_seq", c_int32), ("num_pages", c_int64),
                 ("decision_bias", c_float), ("omega_src", c_int32), ("split_tile", c_int32),
                 ("max_prompt_len", c_int32), ("decision_src", c_int32), ("window", c_int32)]
+
+
+class TrainConfig(ctypes.Structure):
+    """Mirror of dmc_train_config."""
+    _fields_ = [("batch", c_int32), ("seq_len", c_int32), ("num_q_heads", c_int32),
+                ("num_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int32),
+                ("decision_bias", c_float), ("temperature", c_float), ("window", c_int32),
+                ("omega_src", c_int32)]
 
 
 class DMCError(RuntimeError):
@@ -73,8 +82,15 @@ def _load():
     lib.dmc_cache_pages_used.argtypes = [c_void_p, i64p, c_void_p]
     lib.dmc_last_error.argtypes = []
     lib.dmc_last_error.restype = c_char_p
+    lib.dmc_train_workspace_bytes.argtypes = [POINTER(TrainConfig)]
+    lib.dmc_train_workspace_bytes.restype = c_size_t
+    lib.dmc_train_forward.argtypes = [POINTER(TrainConfig), c_void_p, c_void_p, c_void_p, c_void_p,
+                                      c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.dmc_train_backward.argtypes = [POINTER(TrainConfig), c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_size_t, c_void_p]
     for name in EXPORTS:
-        if name not in ("dmc_cache_workspace_bytes", "dmc_last_error"):
+        if name not in ("dmc_cache_workspace_bytes", "dmc_last_error", "dmc_train_workspace_bytes"):
             getattr(lib, name).restype = c_int32
     return lib
 
@@ -237,3 +253,47 @@ class DMCCache:
 def torch_empty_like(t):
     import torch
     return torch.empty_like(t, memory_format=torch.contiguous_format)
+
+
+def make_train_config(batch, seq_len, num_q_heads, num_kv_heads, head_dim, dtype="bf16",
+                      decision_bias=5.0, temperature=0.1, window=12, omega_src="lead") -> TrainConfig:
+    """A dmc_train_config (defaults: the paper's c = 5, tau = 0.1, w = 12)."""
+    return TrainConfig(batch, seq_len, num_q_heads, num_kv_heads, head_dim,
+                       DMC_FP32 if dtype in ("fp32", "float32") else DMC_BF16, decision_bias,
+                       temperature, window, OMEGA_SRC[omega_src])
+
+
+class DMCTrainer:
+    """Training-time DMC attention of one layer shape (forward + backward)
+    with its workspace in one torch allocation on the current GPU."""
+
+    def __init__(self, cfg: TrainConfig, device="cuda"):
+        import torch
+        self.cfg = cfg
+        n = lib.dmc_train_workspace_bytes(ctypes.byref(cfg))
+        if n == 0:
+            raise DMCError(DMC_ERR_INVALID_ARG, last_error())
+        self.workspace = torch.empty(n + 256, dtype=torch.uint8, device=device)
+        self._ws = c_void_p((self.workspace.data_ptr() + 255) // 256 * 256)
+        self._ws_bytes = n
+
+    def forward(self, q, k, v, noise, out=None, alpha=None, stream=None):
+        """out [B, n, Hq, d] (and alpha [B, n, Hkv] fp32 if given)."""
+        if out is None:
+            out = torch_empty_like(q)
+        check(lib.dmc_train_forward(ctypes.byref(self.cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(noise),
+                                    _ptr(out), _ptr(alpha), self._ws, self._ws_bytes,
+                                    _stream(stream)))
+        return out
+
+    def backward(self, q, k, v, noise, out, dout, dalpha=None, dq=None, dk=None, dv=None,
+                 stream=None):
+        """(dq, dk, dv) of sum(out * dout) + sum(alpha * dalpha)."""
+        dq = torch_empty_like(q) if dq is None else dq
+        dk = torch_empty_like(k) if dk is None else dk
+        dv = torch_empty_like(v) if dv is None else dv
+        check(lib.dmc_train_backward(ctypes.byref(self.cfg), _ptr(q), _ptr(k), _ptr(v),
+                                     _ptr(noise), _ptr(out), _ptr(dout), _ptr(dalpha), _ptr(dq),
+                                     _ptr(dk), _ptr(dv), self._ws, self._ws_bytes,
+                                     _stream(stream)))
+        return dq, dk, dv

@@ -13,7 +13,7 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libdmc.so")
 SOURCES = [os.path.join(HERE, "dmc_api.cpp"), os.path.join(HERE, "dmc_kernels.hip"),
-           os.path.join(HERE, "dmc_prompt.hip")]
+           os.path.join(HERE, "dmc_prompt.hip"), os.path.join(HERE, "dmc_train.hip")]
 ARCH = "gfx950"
 
 # Packed-fp32 VALU forms are disabled for every HIP translation unit.

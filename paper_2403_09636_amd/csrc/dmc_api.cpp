@@ -569,6 +569,135 @@ dmc_status dmc_cache_import(dmc_cache *cache, int32_t layer, const void *k_dense
   return DMC_OK;
 }
 
+namespace {
+
+dmc_status validate_train(const dmc_train_config *c) {
+  if (!c) return fail(DMC_ERR_INVALID_ARG, "config is NULL");
+  if (c->batch < 1 || c->seq_len < 1 || c->num_q_heads < 1 || c->num_kv_heads < 1)
+    return fail(DMC_ERR_INVALID_ARG, "batch, seq_len and head counts must be >= 1");
+  if (c->num_q_heads % c->num_kv_heads != 0)
+    return fail(DMC_ERR_INVALID_ARG, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)",
+                c->num_q_heads, c->num_kv_heads);
+  const int G = c->num_q_heads / c->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(DMC_ERR_UNSUPPORTED, "query group size %d not in {1,2,4,8}", G);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(DMC_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", c->head_dim);
+  if (c->dtype != DMC_BF16 && c->dtype != DMC_FP32)
+    return fail(DMC_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+  if (!std::isfinite(c->decision_bias)) return fail(DMC_ERR_INVALID_ARG, "decision_bias not finite");
+  if (!(c->temperature > 0.0f) || !std::isfinite(c->temperature))
+    return fail(DMC_ERR_INVALID_ARG, "temperature must be a finite value > 0");
+  if (c->window < 1 || c->window > dmc::kMaxWindow)
+    return fail(DMC_ERR_INVALID_ARG, "training window %d outside [1, %d]", c->window, dmc::kMaxWindow);
+  if (c->omega_src != DMC_OMEGA_LEAD_QHEAD && c->omega_src != DMC_OMEGA_UNIFORM)
+    return fail(DMC_ERR_UNSUPPORTED, "training omega_src must be LEAD_QHEAD or UNIFORM");
+  const int64_t rows = int64_t(c->batch) * c->seq_len * c->num_q_heads;
+  if (rows > (int64_t(1) << 31) / c->head_dim)
+    return fail(DMC_ERR_UNSUPPORTED, "tensors larger than 2^31 elements");
+  return DMC_OK;
+}
+
+int train_elem_bytes(const dmc_train_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
+
+dmc::TrainLayout train_layout_of(const dmc_train_config &c) {
+  return dmc::train_layout(c.batch, c.seq_len, c.num_q_heads, c.num_kv_heads, c.head_dim,
+                           train_elem_bytes(c), c.window);
+}
+
+// Common checks and parameter set-up of the two training entry points.
+dmc_status train_params(const dmc_train_config *cfg, const void *q, const void *k, const void *v,
+                        const float *noise, void *ws, size_t bytes, dmc::TrainParams *p) {
+  dmc_status st = validate_train(cfg);
+  if (st != DMC_OK) return st;
+  if (!q || !k || !v || !noise || !ws)
+    return fail(DMC_ERR_INVALID_ARG, "q, k, v, noise and workspace must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v))
+    return fail(DMC_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(ws) & 255u)
+    return fail(DMC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  const dmc::TrainLayout L = train_layout_of(*cfg);
+  if (bytes < L.total)
+    return fail(DMC_ERR_INVALID_ARG, "workspace has %zu bytes, needs %zu", bytes, L.total);
+  char *w = static_cast<char *>(ws);
+  *p = dmc::TrainParams{};
+  p->q = q;
+  p->k = k;
+  p->v = v;
+  p->noise = noise;
+  p->ks = w + L.ks;
+  p->vs = w + L.vs;
+  p->x = reinterpret_cast<float *>(w + L.x);
+  p->alpha = reinterpret_cast<float *>(w + L.alpha);
+  p->omega = reinterpret_cast<float *>(w + L.omega);
+  p->z = reinterpret_cast<float *>(w + L.z);
+  p->mask = reinterpret_cast<float *>(w + L.mask);
+  p->lse = reinterpret_cast<float *>(w + L.lse);
+  p->dsum = reinterpret_cast<float *>(w + L.dsum);
+  p->dks = reinterpret_cast<float *>(w + L.dks);
+  p->dvs = reinterpret_cast<float *>(w + L.dvs);
+  p->dmask = reinterpret_cast<float *>(w + L.dmask);
+  p->e = reinterpret_cast<float *>(w + L.e);
+  p->c = cfg->decision_bias;
+  p->tau = cfg->temperature;
+  p->scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(cfg->head_dim)));
+  p->batch = cfg->batch;
+  p->n = cfg->seq_len;
+  p->hq = cfg->num_q_heads;
+  p->hkv = cfg->num_kv_heads;
+  p->window = cfg->window;
+  p->omega_src = cfg->omega_src;
+  return DMC_OK;
+}
+
+}  // namespace
+
+size_t dmc_train_workspace_bytes(const dmc_train_config *cfg) {
+  if (validate_train(cfg) != DMC_OK) return 0;
+  return train_layout_of(*cfg).total;
+}
+
+dmc_status dmc_train_forward(const dmc_train_config *cfg, const void *q, const void *k,
+                             const void *v, const float *noise, void *out, float *alpha,
+                             void *ws, size_t bytes, dmc_stream_t stream) {
+  dmc::TrainParams p;
+  dmc_status st = train_params(cfg, q, k, v, noise, ws, bytes, &p);
+  if (st != DMC_OK) return st;
+  if (!out) return fail(DMC_ERR_INVALID_ARG, "out must be non-NULL");
+  if (!aligned16(out)) return fail(DMC_ERR_INVALID_ARG, "out must be 16-byte aligned");
+  p.out = out;
+  p.alpha_out = alpha;
+  hipError_t e = dmc::launch_train_forward(train_elem_bytes(*cfg), cfg->head_dim,
+                                           cfg->num_q_heads / cfg->num_kv_heads, p,
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "training forward launch");
+  return DMC_OK;
+}
+
+dmc_status dmc_train_backward(const dmc_train_config *cfg, const void *q, const void *k,
+                              const void *v, const float *noise, const void *out,
+                              const void *dout, const float *dalpha, void *dq, void *dk, void *dv,
+                              void *ws, size_t bytes, dmc_stream_t stream) {
+  dmc::TrainParams p;
+  dmc_status st = train_params(cfg, q, k, v, noise, ws, bytes, &p);
+  if (st != DMC_OK) return st;
+  if (!out || !dout || !dq || !dk || !dv)
+    return fail(DMC_ERR_INVALID_ARG, "out, dout, dq, dk and dv must be non-NULL");
+  if (!aligned16(out) || !aligned16(dout) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+    return fail(DMC_ERR_INVALID_ARG, "out, dout, dq, dk and dv must be 16-byte aligned");
+  p.out = const_cast<void *>(out);
+  p.dout = dout;
+  p.dalpha = dalpha;
+  p.dq = dq;
+  p.dk = dk;
+  p.dv = dv;
+  hipError_t e = dmc::launch_train_backward(train_elem_bytes(*cfg), cfg->head_dim,
+                                            cfg->num_q_heads / cfg->num_kv_heads, p,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "training backward launch");
+  return DMC_OK;
+}
+
 static dmc_status read_control(dmc_cache *cache, dmc_stream_t stream, dmc::Control *out) {
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");

@@ -142,6 +142,41 @@ struct DenseParams {
   int32_t dense_slots, units, maxpages, log2p, max_slots;
 };
 
+// Training-time forward/backward (Sec. 3.2 + 3.3).  Units u = b * hkv + g;
+// per-unit arrays are [U][n] (or [U][n][d] for rows).
+struct TrainParams {
+  const void *q, *k, *v;     // [B, n, H, d] contiguous
+  const float *noise;        // [B, n, Hkv]
+  void *out;                 // [B, n, Hq, d]
+  float *alpha_out;          // optional [B, n, Hkv]
+  const void *dout;          // [B, n, Hq, d]
+  const float *dalpha;       // optional [B, n, Hkv]
+  void *dq, *dk, *dv;
+  // workspace
+  void *ks, *vs;             // unrolled states [U][n][d], config dtype
+  float *x, *alpha, *omega;  // per token [U][n]: Gumbel-sigmoid logit, alpha, omega
+  float *z;                  // state normalisers [U][n]
+  float *mask;               // [U][n]: log(1 - alpha_{j+1}) for state j < n - 1
+  float *lse;                // [U][G][n]: log2-sum-exp of each query row (log2 domain)
+  float *dsum;               // [U][G][n]: sum(dout * out) of each query row
+  float *dks, *dvs;          // [U][n][d] fp32: gradients of the states
+  float *dmask;              // [U][n]
+  float *e;                  // [U][n][w]: d loss / d weight of token t in state t + i
+  float c, tau, scale_log2;
+  int32_t batch, n, hq, hkv, window, omega_src;
+};
+
+// Workspace layout of a training configuration.
+struct TrainLayout {
+  size_t ks, vs, x, alpha, omega, z, mask, lse, dsum, dks, dvs, dmask, e, total;
+};
+TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int elem_bytes, int window);
+
+hipError_t launch_train_forward(int elem_bytes, int head_dim, int group, const TrainParams &p,
+                                hipStream_t s);
+hipError_t launch_train_backward(int elem_bytes, int head_dim, int group, const TrainParams &p,
+                                 hipStream_t s);
+
 // Launchers (return hipGetLastError() after enqueueing).
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s);
 hipError_t launch_fill_u8(void *p, size_t bytes, hipStream_t s);

@@ -139,3 +139,45 @@ def test_missing_library_fails_loudly(tmp_path):
     res = subprocess.run([sys.executable, "-c", "import paper_2403_09636_amd"], cwd=tmp_path,
                          capture_output=True, text=True)
     assert res.returncode != 0 and "not built" in res.stderr
+
+
+def test_train_config_struct_matches_header(P):
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct dmc_train_config \{(.*?)\} dmc_train_config;", text, re.S)
+    fields = re.findall(r"^\s*(?:int32_t|int64_t|float)\s+([a-z_, ]+);", body.group(1), re.M)
+    names = [f.strip() for grp in fields for f in grp.split(",")]
+    assert names == [f[0] for f in P.TrainConfig._fields_]
+    assert ctypes.sizeof(P.TrainConfig) == 40
+
+
+@pytest.mark.parametrize("field,value,msg", [
+    ("num_kv_heads", 3, "multiple"), ("head_dim", 96, "head_dim"), ("dtype", 9, "dtype"),
+    ("temperature", 0.0, "temperature"), ("temperature", -1.0, "temperature"),
+    ("window", 0, "window"), ("window", 65, "window"), ("omega_src", 1, "omega_src"),
+    ("seq_len", 0, ">= 1"), ("num_q_heads", 24, "group"),
+])
+def test_invalid_train_config(P, field, value, msg):
+    cfg = P.make_train_config(2, 128, 16, 4, 128)
+    assert P.binding.lib.dmc_train_workspace_bytes(ctypes.byref(cfg)) > 0
+    setattr(cfg, field, value)
+    assert P.binding.lib.dmc_train_workspace_bytes(ctypes.byref(cfg)) == 0
+    assert msg in P.binding.last_error()
+
+
+def test_train_entry_points_reject_before_hip(P):
+    lib = P.binding.lib
+    cfg = P.make_train_config(1, 64, 4, 2, 64, window=12)
+    n = lib.dmc_train_workspace_bytes(ctypes.byref(cfg))
+    a = ctypes.c_void_p(0x1000)
+    ws = ctypes.c_void_p(0x10000)
+    assert lib.dmc_train_forward(ctypes.byref(cfg), None, a, a, a, a, None, ws, n, None) == 1
+    assert "NULL" in P.binding.last_error()
+    assert lib.dmc_train_forward(ctypes.byref(cfg), a, a, a, a, a, None, ws, n - 1, None) == 1
+    assert "needs" in P.binding.last_error()
+    assert lib.dmc_train_forward(ctypes.byref(cfg), ctypes.c_void_p(0x1008), a, a, a, a, None, ws,
+                                 n, None) == 1
+    assert "aligned" in P.binding.last_error()
+    assert lib.dmc_train_backward(ctypes.byref(cfg), a, a, a, a, a, a, None, None, a, a, ws, n,
+                                  None) == 1
+    assert "NULL" in P.binding.last_error()
+    assert lib.dmc_train_backward(None, a, a, a, a, a, a, None, a, a, a, ws, n, None) == 1

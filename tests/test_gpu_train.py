@@ -1,0 +1,91 @@
+"""Training-time DMC attention (Sec. 3.2, 3.3, masking appendix) on the GPU
+against the float64 training oracle (autograd backward), through the C ABI:
+forward outputs and relaxed decisions, then dq, dk, dv."""
+import numpy as np
+import pytest
+
+import oracle.dmc_train as T
+from tests.gpu_helpers import TOL, f64, log, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(rng, B, n, Hkv, G, d, crs, c):
+    """q, k, v ~ N(0, 1); k[0] = c + log(CR - 1) per kv head, so that with
+    the logistic noise P(alpha > 1/2) = 1 - 1/CR (CR = 1: c - 3)."""
+    q = rng.standard_normal((B, n, Hkv * G, d)).astype(np.float32)
+    k = rng.standard_normal((B, n, Hkv, d)).astype(np.float32)
+    v = rng.standard_normal((B, n, Hkv, d)).astype(np.float32)
+    crs = np.asarray(crs, dtype=np.float64)
+    k0 = np.where(crs > 1, c + np.log(np.maximum(crs - 1, 1e-12)), c - 3.0)
+    k[..., 0] = k0[None, None, :].astype(np.float32) + 0.3 * rng.standard_normal((B, n, Hkv)).astype(np.float32)
+    noise = rng.logistic(size=(B, n, Hkv)).astype(np.float32)
+    dout = rng.standard_normal((B, n, Hkv * G, d)).astype(np.float32)
+    dalpha = (0.5 * rng.standard_normal((B, n, Hkv))).astype(np.float32)
+    return q, k, v, noise, dout, dalpha
+
+
+def _grad_close(got, want, dtype, what):
+    """Gradients: elementwise |got - want| <= atol * max|want| + rtol * |want|
+    (the reference's scale: a gradient tensor's entries span several orders
+    of magnitude, so the absolute term follows its largest entry)."""
+    atol, rtol = TOL[dtype]
+    got, want = np.asarray(got, np.float64), np.asarray(want, np.float64)
+    scale = max(1.0, float(np.abs(want).max(initial=0.0)))
+    err = np.abs(got - want)
+    bad = err > atol * scale + rtol * np.abs(want)
+    worst = float(err.max(initial=0.0)) / scale
+    if bad.any():
+        i = np.unravel_index(np.argmax(err - rtol * np.abs(want)), err.shape)
+        raise AssertionError(f"{what}: {bad.sum()} of {bad.size} outside tolerance; worst at {i}: "
+                             f"got {got[i]!r} want {want[i]!r}; max err / scale {worst:.3e}")
+    return worst
+
+
+CASES = [
+    # dtype, d, G, B, Hkv, n, window, c, tau, crs, omega, dalpha
+    ("fp32", 64, 1, 2, 2, 70, 12, 5.0, 0.1, [2.0, 8.0], "lead", False),
+    ("fp32", 128, 2, 1, 2, 100, 3, 1.0, 1.0, [1.0, 4.0], "lead", True),
+    ("fp32", 64, 8, 1, 1, 40, 1, 0.0, 0.5, [3.0], "lead", True),
+    ("fp32", 64, 4, 1, 2, 90, 64, 5.0, 0.3, [20.0, 2.0], "lead", False),
+    ("fp32", 128, 1, 1, 2, 33, 12, 5.0, 0.1, [4.0, 4.0], "uniform", True),
+    ("fp32", 64, 2, 2, 1, 1, 12, 5.0, 0.1, [4.0], "lead", True),
+    ("bf16", 128, 1, 2, 2, 100, 12, 5.0, 0.1, [2.0, 6.0], "lead", True),
+    ("bf16", 128, 8, 1, 2, 64, 12, 5.0, 0.5, [4.0, 1.0], "lead", False),
+    ("bf16", 64, 2, 1, 2, 80, 5, 2.0, 1.0, [3.0, 10.0], "lead", True),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "-".join(str(x) for x in c[:7]))
+def test_train_forward_backward(torch_cuda, case):
+    import torch
+    import paper_2403_09636_amd as P
+    dtype, d, G, B, Hkv, n, w, c, tau, crs, omega, use_dalpha = case
+    log(f"case train {case}")
+    rng = np.random.default_rng(900 + d + 10 * G + n + w)
+    q, k, v, noise, dout, dalpha = _inputs(rng, B, n, Hkv, G, d, crs, c)
+    dt = torch_dtype(dtype)
+    qt, kt, vt, dot = (torch.from_numpy(x).to(dt).cuda() for x in (q, k, v, dout))
+    nt = torch.from_numpy(noise).cuda()
+    dat = torch.from_numpy(dalpha).cuda() if use_dalpha else None
+    cfg = P.make_train_config(B, n, Hkv * G, Hkv, d, dtype, decision_bias=c, temperature=tau,
+                              window=w, omega_src=omega)
+    tr = P.DMCTrainer(cfg)
+    alpha = torch.empty((B, n, Hkv), dtype=torch.float32, device="cuda")
+    out = tr.forward(qt, kt, vt, nt, alpha=alpha)
+    dq, dk, dv = tr.backward(qt, kt, vt, nt, out, dot, dalpha=dat)
+    torch.cuda.synchronize()
+
+    qo, ko, vo, do = (torch.from_numpy(f64(x)) for x in (qt, kt, vt, dot))
+    no = torch.from_numpy(noise.astype(np.float64))
+    o_ref, a_ref = T.train_forward(qo, ko, vo, no, c, tau, w, omega)
+    rq, rk, rv = T.train_backward(qo, ko, vo, no, do, dalpha.astype(np.float64) if use_dalpha else None,
+                                  c, tau, w, omega)
+    atol, rtol = TOL[dtype]
+    a_err = np.abs(alpha.cpu().numpy() - a_ref.detach().numpy()).max()
+    assert a_err < 1e-5, f"alpha error {a_err}"
+    o_err = np.abs(f64(out) - o_ref.detach().numpy())
+    assert (o_err <= atol + rtol * np.abs(o_ref.detach().numpy())).all(), f"output max err {o_err.max()}"
+    errs = [_grad_close(f64(x), r.numpy(), dtype, name)
+            for x, r, name in ((dq, rq, "dq"), (dk, rk, "dk"), (dv, rv, "dv"))]
+    log(f"  out {o_err.max():.2e}  dq {errs[0]:.2e}  dk {errs[1]:.2e}  dv {errs[2]:.2e} (of scale)")
