@@ -16,6 +16,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -39,6 +40,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--prompt", action="store_true",
                     help="measure prompt-phase attention (dmc_prefill_attend) instead of decode")
+    ap.add_argument("--train", action="store_true",
+                    help="measure the training-time forward + backward (dmc_train_*)")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
     ap.add_argument("--window", type=int, default=0,
                     help="window-grouping width (Sec. 3.3); prefilled workloads only")
@@ -238,6 +241,117 @@ def bench_prompt(args):
     print(json.dumps(res), flush=True)
 
 
+def cpu_baseline_train(w, seconds):
+    """The float64 training oracle (autograd backward), one thread, on
+    (batch row, kv head) units over the first 512 tokens of a sequence (a
+    4096-token unit alone takes minutes in the oracle): tokens/s = 512 /
+    (time per unit x kv heads).  Its cost is dominated by the per-position
+    window recurrence, linear in n; the attention part grows with n, so at
+    the full length the oracle is slower than this figure."""
+    import torch
+    from threadpoolctl import threadpool_limits
+
+    import oracle.dmc_train as T
+    import workloads as W
+
+    rng = np.random.default_rng(11)
+    n, d, G = min(512, w.prompt_len), w.head_dim, w.group
+    times = []
+    with threadpool_limits(limits=1):
+        torch.set_num_threads(1)
+        t_end = time.perf_counter() + seconds
+        while time.perf_counter() < t_end or not times:
+            q = torch.from_numpy(rng.standard_normal((1, n, G, d)))
+            k = torch.from_numpy(rng.standard_normal((1, n, 1, d)))
+            v = torch.from_numpy(rng.standard_normal((1, n, 1, d)))
+            k[..., 0] = W.TRAIN_C + math.log(3.0)
+            noise = torch.from_numpy(rng.logistic(size=(1, n, 1)))
+            dout = torch.from_numpy(rng.standard_normal((1, n, G, d)))
+            t0 = time.perf_counter()
+            T.train_backward(q, k, v, noise, dout, None, W.TRAIN_C, W.TRAIN_TAU, W.TRAIN_WINDOW)
+            times.append(time.perf_counter() - t0)
+    per_unit = float(np.mean(times))
+    return {"value": n / (per_unit * w.num_kv_heads), "unit": "tokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{len(times)} units (one kv head x the first {n} tokens, forward + "
+                      f"autograd backward, float64 torch, 1 thread); tokens/s = {n} / (time per "
+                      f"unit x {w.num_kv_heads} kv heads)"}
+
+
+def bench_train(args):
+    """Training-time DMC attention of one layer: dmc_train_forward and
+    dmc_train_backward, each timed per call with HIP events on the launch
+    stream (median).  Algorithmic flops per (query row, visible state): 4 d
+    forward (scores, weighted values), 8 d backward (dP, dV, dQ, dK)."""
+    import torch
+
+    import paper_2403_09636_amd as P
+    import workloads as W
+
+    name = args.workload if args.workload in W.WORKLOADS and \
+        W.WORKLOADS[args.workload].cache_kind == "train" else "llama7b_train"
+    w = W.WORKLOADS[name]
+    if args.batch:
+        w = W.scaled(w, batch=args.batch)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n, B = w.prompt_len, w.batch
+    window = args.window or W.TRAIN_WINDOW
+    cfg = P.make_train_config(B, n, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                              W.TRAIN_C, W.TRAIN_TAU, window)
+    tr = P.DMCTrainer(cfg, device=dev)
+    q, k, v, noise, dout = W.train_inputs_torch(w, 0, dev)
+    out = torch.empty_like(q)
+    alpha = torch.empty((B, n, w.num_kv_heads), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return float(np.median(ms))
+
+    fwd = lambda: tr.forward(q, k, v, noise, out=out, alpha=alpha)  # noqa: E731
+    bwd = lambda: tr.backward(q, k, v, noise, out, dout, dq=dq, dk=dk, dv=dv)  # noqa: E731
+    fwd()
+    timed(bwd, max(1, args.warmup))
+    t_bwd = timed(bwd, args.steps)
+    timed(fwd, max(1, args.warmup))
+    t_fwd = timed(fwd, args.steps)
+    pairs = B * w.num_q_heads * n * (n + 1) / 2.0
+    f_fwd, f_bwd = 4.0 * w.head_dim * pairs, 8.0 * w.head_dim * pairs
+    tf = (f_fwd + f_bwd) / ((t_fwd + t_bwd) * 1e-3) / 1e12
+    acc = float((alpha[:, 1:] > 0.5).float().mean().item())
+    res = {
+        "metric": f"training tokens/s (DMC attention forward + backward, one layer), {w.name}",
+        "value": round(B * n / ((t_fwd + t_bwd) * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_fwd + t_bwd, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": 1, "batch": B, "q_heads": w.num_q_heads,
+                   "kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "seq_len": n,
+                   "c": W.TRAIN_C, "tau": W.TRAIN_TAU, "window": window,
+                   "accumulate_fraction": round(acc, 4)},
+        "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": "dmc_train_forward + dmc_train_backward",
+                     "alg_flops_per_launch": int(f_fwd + f_bwd),
+                     "avg_launch_us": round((t_fwd + t_bwd) * 1e3, 1)},
+        "forward_ms": round(t_fwd, 4), "backward_ms": round(t_bwd, 4),
+        "forward_TFLOPs": round(f_fwd / (t_fwd * 1e-3) / 1e12, 1),
+        "backward_TFLOPs": round(f_bwd / (t_bwd * 1e-3) / 1e12, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_train(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -247,6 +361,9 @@ def main():
         sys.exit(2)
     if args.prompt:
         bench_prompt(args)
+        return
+    if args.train:
+        bench_train(args)
         return
 
     import torch

@@ -84,7 +84,17 @@ WORKLOADS = {
                              notes="Llama-2-70B GQA shape, 64 query / 8 kv heads, batch "
                                    "256, 4096-token prompts compressed by prefill at CR 2 "
                                    "per kv head, 64 decode steps"),
+    "llama7b_train": Workload("llama7b_train", 6, 1, 4, 32, 32, 128, "bf16", 4096, 0, "train",
+                              "uniform_1248",
+                              notes="one Llama-2-7B attention layer in continued pre-training: "
+                                    "4 sequences of 4096 tokens (the paper's sequence length), "
+                                    "c = 5, tau = 0.1, w = 12, per-head target CR from "
+                                    "{1,2,4,8}"),
 }
+
+# Training hyperparameters of the paper (Sec. 4): Gumbel-sigmoid constant c,
+# temperature tau and window w.
+TRAIN_C, TRAIN_TAU, TRAIN_WINDOW = 5.0, 0.1, 12
 
 
 def scaled(w: Workload, **kw) -> Workload:
@@ -374,3 +384,28 @@ def sample_units(w: Workload, count: int, seed: int = 12345):
             if (0, 0, g) not in units:
                 units.append((0, 0, g))
     return sorted(units)
+
+
+def train_inputs_torch(w: Workload, layer: int, device, c: float = TRAIN_C):
+    """Training-step inputs of one layer on the device: q [B, n, Hq, d], k, v
+    [B, n, Hkv, d] ~ N(0, 1) in the workload dtype, k[..., 0] = c + log(CR - 1)
+    + N(0, 0.3) per kv head (c - 3 for CR 1), so that with the logistic
+    noise [B, n, Hkv] (fp32, the Gumbel-sigmoid's draws) a decision
+    accumulates with probability about 1 - 1/CR; dout ~ N(0, 1) is the
+    incoming gradient."""
+    import torch
+    g = _gen(w, PROMPT_STREAM, layer, device)
+    n = w.prompt_len
+    B, Hq, Hkv, d = w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim
+    dt = _torch_dtype(w)
+    q = _randn_rows((B, n, Hq, d), g, device, dt)
+    k = _randn_rows((B, n, Hkv, d), g, device, dt)
+    v = _randn_rows((B, n, Hkv, d), g, device, dt)
+    dout = _randn_rows((B, n, Hq, d), g, device, dt)
+    cr = torch.as_tensor(head_crs(w)[layer], dtype=torch.float32, device=device)
+    k0 = torch.where(cr > 1, c + torch.log(torch.clamp(cr - 1, min=1e-30)), torch.full_like(cr, c - 3))
+    jitter = 0.3 * torch.randn((B, n, Hkv), generator=g, device=device)
+    k[..., 0] = (k0[None, None, :] + jitter).to(dt)
+    u = torch.rand((B, n, Hkv), generator=g, device=device).clamp(1e-7, 1 - 1e-7)
+    noise = (torch.log(u) - torch.log1p(-u)).contiguous()
+    return q, k, v, noise, dout
