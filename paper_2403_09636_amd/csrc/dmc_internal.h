@@ -153,12 +153,13 @@ struct TrainParams {
   const float *dalpha;       // optional [B, n, Hkv]
   void *dq, *dk, *dv;
   // workspace
-  void *ks, *vs;             // unrolled states [U][n][d], config dtype
+  void *ks, *vs;             // unrolled states [U][n][d] (+ 32 zero rows), config dtype;
+                             // key element 0 holds the state's mask entry * sqrt(d)
   float *x, *alpha, *omega;  // per token [U][n]: Gumbel-sigmoid logit, alpha, omega
   float *z;                  // state normalisers [U][n]
   float *mask;               // [U][n]: log(1 - alpha_{j+1}) for state j < n - 1
-  float *lse;                // [U][G][n]: log2-sum-exp of each query row (log2 domain)
-  float *dsum;               // [U][G][n]: sum(dout * out) of each query row
+  float *lse;                // [U][n][G]: log2-sum-exp of each query row (log2 domain)
+  float *dsum;               // [U][n][G]: sum(dout * out) of each query row
   float *dks, *dvs;          // [U][n][d] fp32: gradients of the states
   float *dmask;              // [U][n]
   float *e;                  // [U][n][w]: d loss / d weight of token t in state t + i

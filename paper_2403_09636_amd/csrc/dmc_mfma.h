@@ -1,0 +1,109 @@
+// Matrix-core and LDS helpers shared by the gfx950 attention kernels of the
+// DMC library (prompt-phase attention and training): direct global-to-LDS
+// transfers, v_mfma_f32_32x32x16_bf16 operands, transposed LDS reads and the
+// XOR swizzles of the LDS row layouts.  Internal; included by .hip files only.
+#pragma once
+
+#include "dmc_device.h"
+
+namespace dmc {
+namespace {
+
+constexpr float kLazyRescale = 8.0f;        // log2 of the largest unnormalised probability
+
+// Orders this wave's LDS writes before its later LDS reads (and the reverse).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+template <int CPR>
+__device__ __forceinline__ int k_swizzle(int row) { return row & (CPR - 1); }
+template <int CPR>
+__device__ __forceinline__ int v_swizzle(int row) {
+  return CPR == 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
+}
+__device__ __forceinline__ int vt_swizzle(int dim) { return (dim >> 2) & 3; }
+__device__ __forceinline__ int score_slot(int m) {   // pi(m): bits 2 and 3 swapped
+  return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void *p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char *)p));
+}
+
+// 16 bytes per lane from global memory straight into LDS at
+// lds_base + 16 * lane (lds_base wave-uniform).  Issued as inline assembly so
+// that the compiler neither waits for it nor reorders LDS accesses around it;
+// completion is awaited with wait_vmcnt before the workgroup barrier.
+__device__ __forceinline__ void dma16(uint32_t lds_base, const void *g) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory");
+}
+
+// Same, with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane offset.
+__device__ __forceinline__ void dma16_s(uint32_t lds_base, const char *sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory");
+}
+
+// A wave-uniform pointer, made visibly uniform (SGPRs) for dma16_s.
+__device__ __forceinline__ const char *uniform_ptr(const char *ptr) {
+  const uint64_t x = reinterpret_cast<uint64_t>(ptr);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x >> 32));
+  return reinterpret_cast<const char *>((uint64_t(hi) << 32) | lo);
+}
+
+// s_waitcnt with only the vector-memory count (at most N outstanding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint2 ds_read_tr16(const void *p) {
+  const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4_t *)((__attribute__((address_space(3))) char *)p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+__device__ __forceinline__ f32x16_t mfma_32x32x16(const uint4 &a, const uint4 &b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Maximum of x over lanes l and l ^ 32 (v_permlane32_swap of x with itself
+// leaves each lane's value and its partner's in the two results).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                  __builtin_bit_cast(unsigned, x), false, false);
+  return fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
+               __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
+}
+
+// Two floats -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  typedef float f2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2_t{lo, hi}, b2_t));
+}
+
+// Sum of a packed bf16 pair added to acc (exact products by 1, fp32 sum).
+__device__ __forceinline__ float add_pair(uint32_t pair, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pair),
+                                         __builtin_bit_cast(bf16x2_t, 0x3f803f80u), acc, false);
+}
+
+}  // namespace
+}  // namespace dmc

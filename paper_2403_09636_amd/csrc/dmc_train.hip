@@ -18,9 +18,13 @@
 // states' gradients are carried back to the tokens (the closed form above),
 // and the decision / importance neurons get theirs through alpha and omega.
 //
-// These are vector-ALU kernels (lanes own head-dim elements, one wave per
-// group of rows); they work for every dtype.
-#include "dmc_device.h"
+// Vector-ALU kernels (lanes own head-dim elements, one wave per group of
+// rows) serve every dtype; bf16 attention runs on the matrix cores
+// (v_mfma_f32_32x32x16_bf16) in three kernels: forward, dq, and the state
+// gradients dK~, dV~ with the mask gradient.
+#include <type_traits>
+
+#include "dmc_mfma.h"
 
 namespace dmc {
 
@@ -34,14 +38,15 @@ TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int el
     off = align_up(off + bytes, 256);
     return at;
   };
-  L.ks = take(U * N * D * elem_bytes);
-  L.vs = take(U * N * D * elem_bytes);
+  // states: 32 rows of (zeroed) padding so that 32-row blocks never leave the buffer
+  L.ks = take((U * N + 32) * D * elem_bytes);
+  L.vs = take((U * N + 32) * D * elem_bytes);
   L.x = take(U * N * 4);
   L.alpha = take(U * N * 4);
   L.omega = take(U * N * 4);
   L.z = take(U * N * 4);
   L.mask = take(U * N * 4);
-  L.lse = take(U * G * N * 4);
+  L.lse = take(U * G * N * 4);        // [U][n][G]
   L.dsum = take(U * G * N * 4);
   L.dks = take(U * N * D * 4);
   L.dvs = take(U * N * D * 4);
@@ -110,6 +115,7 @@ __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
   const char *kb = static_cast<const char *>(p.k) + (row_k(p, b, 0, g, D) + lane * E) * ES;
   const char *vb = static_cast<const char *>(p.v) + (row_k(p, b, 0, g, D) + lane * E) * ES;
   const int64_t rs = int64_t(p.hkv) * D * ES;   // bytes between tokens
+  const float sqrt_d = kLog2e / p.scale_log2;
   for (int j = j0; j < j1; ++j) {
     const int a = max(0, j - p.window + 1);
     float sk[E], sv[E], zs = 0.0f, P = 1.0f;
@@ -145,6 +151,10 @@ __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
       sk[e] *= inv;
       sv[e] *= inv;
     }
+    // Element 0 of a key state is never part of a score; it carries the
+    // state's mask entry times sqrt(d), which the matrix-core kernels add to
+    // the scores through a query element fixed at 1.
+    if (lane == 0) sk[0] = p.mask[int64_t(u) * p.n + j] * sqrt_d;
     const int64_t o = (int64_t(u) * p.n + j) * D + lane * E;
     store_e<ES, E>(static_cast<char *>(p.ks) + o * ES, sk);
     store_e<ES, E>(static_cast<char *>(p.vs) + o * ES, sv);
@@ -234,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void train_fwd_kernel(TrainParams p, int 
 #pragma unroll
     for (int e = 0; e < E; ++e) o[e] = acc[r][e] * inv;
     store_e<ES, E>(static_cast<char *>(p.out) + (row_q(p, b, a + j, g * G + h, D) + lane * E) * ES, o);
-    if (lane == 0) p.lse[(int64_t(u) * G + h) * p.n + a + j] = m[r] + __log2f(l[r]);
+    if (lane == 0) p.lse[(int64_t(u) * p.n + a + j) * G + h] = m[r] + __log2f(l[r]);
   }
 }
 
@@ -269,8 +279,8 @@ __global__ __launch_bounds__(kThreads) void train_dq_kernel(TrainParams p, int n
 #pragma unroll
       for (int e = 0; e < E; ++e) d = fmaf(dor[r][e], of[e], d);
       Dr[r] = wsum(d);
-      Lr[r] = p.lse[(int64_t(u) * G + h) * p.n + a + j];
-      if (lane == 0) p.dsum[(int64_t(u) * G + h) * p.n + a + j] = Dr[r];
+      Lr[r] = p.lse[(int64_t(u) * p.n + a + j) * G + h];
+      if (lane == 0) p.dsum[(int64_t(u) * p.n + a + j) * G + h] = Dr[r];
     }
     if (lane == 0) qr[r][0] = 0.0f;
   }
@@ -354,8 +364,8 @@ __global__ __launch_bounds__(kThreads) void train_dkv_kernel(TrainParams p, int 
       load_e<ES, E>(static_cast<const char *>(p.q) + ro * ES, qf);
       load_e<ES, E>(static_cast<const char *>(p.dout) + ro * ES, df);
       if (lane == 0) qf[0] = 0.0f;
-      const float L = p.lse[(int64_t(u) * G + h) * p.n + t];
-      const float Dt = p.dsum[(int64_t(u) * G + h) * p.n + t];
+      const float L = p.lse[(int64_t(u) * p.n + t) * G + h];
+      const float Dt = p.dsum[(int64_t(u) * p.n + t) * G + h];
 #pragma unroll
       for (int i = 0; i < KB; ++i) {
         const int s = j0 + i;
@@ -494,6 +504,461 @@ __global__ __launch_bounds__(kThreads) void train_neurons_kernel(TrainParams p) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 attention on the matrix cores.
+//
+// Query-major kernels (forward, dq): one workgroup = 4 waves = 128 query
+// columns of one unit, token-major (column c = token c / G, head c % G); a
+// wave owns 32 columns.  The unit's states stream through LDS in blocks of 32
+// rows (direct global -> LDS transfers, a 3-slot ring two blocks ahead), and
+// per block and wave, lane l holding column l % 32 and half l / 32:
+//   S^T[state][col] = K'[state] . Q'[col]     (A = K' rows, B = Q'^T)
+// Score row m is state pi(m) (bits 2 and 3 of m swapped), so a lane's score
+// registers 8 kk .. 8 kk + 7 are its B-operand slice for states
+// 16 kk + 8 half .. + 8 of the products that contract over states:
+//   forward: O^T[dim][col] += V^T[dim][state] P^T[state][col]
+//   dq:      dQ^T[dim][col] += K^T[dim][state] dS^T[state][col]
+// The mask is folded into the score product: key-state element 0 holds the
+// state's mask entry times sqrt(d) and query element 0 is set to 1 (neither
+// is otherwise part of a score); the diagonal takes it out again, and states
+// past a column's token are masked in the blocks that reach the diagonal.
+//
+// State-major kernel (dK~, dV~, mask gradient): one workgroup = 4 waves =
+// 128 states of one unit, a wave owning 32 (its K~, V~ rows are operands in
+// registers); query rows (token, head) stream through LDS in blocks of 32:
+//   S[row][state] = Q[row] . K~[state],  dP[row][state] = dO[row] . V~[state]
+// with rows pi-permuted so that P^T and dS^T come out as A operands of
+//   dV~[state][dim] += P^T[state][row] dO[row][dim]
+//   dK~[state][dim] += dS^T[state][row] Q[row][dim].
+// Rows read as "8 consecutive rows of one dim" (V^T, K^T, dO, Q) use the
+// transposed LDS read ds_read_b64_tr_b16 on rows stored with the value
+// swizzle.
+// ---------------------------------------------------------------------------
+
+// Transposed operand: A or B slice "rows r0 + 8 half + 0..7 of dim 32 t + col"
+// from a 32-row block stored with the value swizzle (vaddr per tile t).
+template <int RB>
+__device__ __forceinline__ uint4 tr_operand(const char *blk, uint32_t vaddr, int kk) {
+  const uint2 h0 = ds_read_tr16(blk + vaddr + 16 * kk * RB);
+  const uint2 h1 = ds_read_tr16(blk + vaddr + (16 * kk + 4) * RB);
+  return make_uint4(h0.x, h0.y, h1.x, h1.y);
+}
+
+// Per-lane offsets of the transposed reads (one per 32-dim tile).
+template <int D>
+__device__ __forceinline__ void tr_offsets(int lane, uint32_t (&vaddr)[D / 32]) {
+  constexpr int RB = D * 2, CPR = D / 8;
+  const int g16 = lane >> 4, r16 = lane & 15;
+  const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
+#pragma unroll
+  for (int t = 0; t < D / 32; ++t) {
+    const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+    vaddr[t] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+  }
+}
+
+// Row-read offsets: 16 bytes (dims 16 ks + 8 half .. + 8) of row `row` of a
+// block stored with swizzle SW (0: key swizzle, 1: value swizzle).
+template <int D, int SW>
+__device__ __forceinline__ uint32_t row_offset(int row, int ks, int hb) {
+  constexpr int RB = D * 2, CPR = D / 8;
+  const int sw = SW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row);
+  return row * RB + (((2 * ks + hb) ^ sw) * 16);
+}
+
+// Query-major kernels: MODE 0 = forward, 1 = dq.
+template <int D, int G, int MODE>
+__global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p, int ntiles) {
+  constexpr int kSt = 3;               // ring slots
+  constexpr int T = 32 / G;            // tokens per wave
+  constexpr int TW = kWaves * T;       // tokens per workgroup
+  constexpr int KS = D / 16;           // 16-dim k-steps of the score product
+  constexpr int NTL = D / 32;          // 32-dim tiles of the contraction over states
+  constexpr int RB = D * 2;
+  constexpr int CPR = D / 8;
+  constexpr int BLK = 32 * RB;
+  constexpr int DPW = BLK / 16 / kThreads;
+  constexpr int KSW = MODE == 0 ? 0 : 1;   // dq also reads keys transposed
+  constexpr int VSW = MODE == 0 ? 1 : 0;   // forward reads values transposed
+  static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
+  __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
+
+  const int U = p.batch * p.hkv;
+  const int bid = blockIdx.x;
+  const int xcd = bid & 7, r = bid >> 3;
+  const int ul = r / ntiles, tile = ntiles - 1 - (r - ul * ntiles);
+  const int u = ul * 8 + xcd;
+  if (u >= U) return;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hb = lane >> 5;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int a = tile * TW + wave * T;
+  const int cnt = max(0, min(T, p.n - a));
+  const int tok = col / G, head = col - tok * G;
+  const bool colv = tok < cnt;
+  const int t = a + tok;
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  const int s_top = min(p.n, tile * TW + TW);   // states 0 .. s_top - 1 feed this tile
+  const int nblk = (s_top + 31) >> 5;
+  const int wave_hi = a + cnt;                  // states < wave_hi feed this wave
+  const float sl2 = p.scale_log2;
+
+  // Q'^T operand: Q[col][16 ks + 8 hb .. + 8] with element 0 set to 1.
+  uint4 qop[KS], dop[MODE == 1 ? KS : 1];
+  float Lc = 0.0f, Dc = 0.0f, diag = 0.0f;
+  {
+    const int64_t ro = row_q(p, b, colv ? t : 0, g * G + head, D);
+    const char *qr = static_cast<const char *>(p.q) + ro * 2;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qop[ks] = colv ? ld16(qr + ks * 32 + hb * 16) : zero4;
+    if (hb == 0) qop[0].x = (qop[0].x & 0xffff0000u) | 0x3f80u;
+    // the diagonal state's mask entry as stored (bf16 of mask * sqrt(d))
+    if (colv) {
+      const float md = p.mask[int64_t(u) * p.n + t] * (kLog2e / sl2);
+      diag = __uint_as_float(bf16_bits(md) << 16);
+    }
+    if constexpr (MODE == 1) {
+      const char *dr = static_cast<const char *>(p.dout) + ro * 2;
+      const char *orow = static_cast<const char *>(p.out) + ro * 2;
+      float part = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        dop[ks] = colv ? ld16(dr + ks * 32 + hb * 16) : zero4;
+        const uint4 ov = colv ? ld16(orow + ks * 32 + hb * 16) : zero4;
+        float df[8], of[8];
+        V16<2>::unpack(dop[ks], df);
+        V16<2>::unpack(ov, of);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) part = fmaf(df[e], of[e], part);
+      }
+      Dc = part + __shfl_xor(part, 32, 64);
+      if (colv) Lc = p.lse[(int64_t(u) * p.n + t) * G + head];
+      if (colv && hb == 0) p.dsum[(int64_t(u) * p.n + t) * G + head] = Dc;
+    }
+  }
+
+  float m = -1e30f, ls = 0.0f;
+  f32x16_t acc[NTL];
+#pragma unroll
+  for (int i = 0; i < NTL; ++i) acc[i] = f32x16_t{};
+
+  // Block transfers (same chunk mapping as prompt attention; the unit's
+  // states are contiguous, so one wave-uniform base per block).
+  const uint32_t ring = lds_offset(smem);
+  uint32_t koff[DPW], voff[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int c = (i * kWaves + wave) * 64 + lane;
+    const int row = c / CPR, pc = c - row * CPR;
+    koff[i] = row * RB + (pc ^ (KSW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row))) * 16;
+    voff[i] = row * RB + (pc ^ (VSW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row))) * 16;
+  }
+  const char *kst = static_cast<const char *>(p.ks) + int64_t(u) * p.n * RB;
+  const char *vst = static_cast<const char *>(p.vs) + int64_t(u) * p.n * RB;
+  auto issue = [&](int kb, int st) {
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
+      dma16_s(kdst, uniform_ptr(kst + int64_t(kb) * BLK), koff[i]);
+      dma16_s(kdst + BLK, uniform_ptr(vst + int64_t(kb) * BLK), voff[i]);
+    }
+  };
+
+  const int krow = score_slot(col);
+  uint32_t kaddr[KS], vrow[MODE == 1 ? KS : 1];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kaddr[ks] = row_offset<D, KSW>(krow, ks, hb);
+    if constexpr (MODE == 1) vrow[ks] = row_offset<D, VSW>(krow, ks, hb);
+  }
+  uint32_t traddr[NTL];
+  tr_offsets<D>(lane, traddr);
+
+  auto step = [&](auto stage_c, int kb) {
+    constexpr int ST = decltype(stage_c)::value;
+    const int after = min(nblk - 1 - kb, kSt - 2);
+    if (after >= 1) wait_vmcnt<2 * DPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();   // block kb is in LDS for every wave; the slot of kb - 1 is free
+    if (kb + kSt - 1 < nblk) issue(kb + kSt - 1, (ST + kSt - 1) % kSt);
+    if (kb * 32 >= wave_hi) return;
+    const char *kd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
+    const char *vd = kd + BLK;
+
+    f32x16_t sc = f32x16_t{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(kd + kaddr[ks]), qop[ks], sc);
+    float sv[16];
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) sv[rr] = sc[rr];
+    if (kb * 32 + 32 > a) {   // the block reaches the diagonal
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int st = kb * 32 + score_slot(8 * (rr >> 2) + 4 * hb + (rr & 3));
+        if (st > t) sv[rr] = neg_inf();
+        else if (st == t) sv[rr] -= diag;
+      }
+    }
+    if constexpr (MODE == 0) {
+      float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+#pragma unroll
+      for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
+      mx = fmaxf(mx, sv[15]);
+      mx = max_halves(mx) * sl2;
+      if (__any(mx > m + kLazyRescale)) {
+        const float mn = fmaxf(m, mx);
+        const float f = fast_exp2(m - mn);
+        m = mn;
+        ls *= f;
+#pragma unroll
+        for (int i = 0; i < NTL; ++i) acc[i] *= f;
+      }
+      uint4 pb[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          w[q] = cvt_pk_bf16(fast_exp2(fmaf(sv[8 * kk + 2 * q], sl2, -m)),
+                             fast_exp2(fmaf(sv[8 * kk + 2 * q + 1], sl2, -m)));
+          ls = add_pair(w[q], ls);
+        }
+        pb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+      for (int i = 0; i < NTL; ++i)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          acc[i] = mfma_32x32x16(tr_operand<RB>(vd, traddr[i], kk), pb[kk], acc[i]);
+    } else {
+      // dP^T = V . dO^T, then dS^T = P^T (dP^T - D) with P from the forward's statistics.
+      f32x16_t dp = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(vd + vrow[ks]), dop[ks], dp);
+      uint4 sb[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r0 = 8 * kk + 2 * q;
+          const float p0 = fast_exp2(fmaf(sv[r0], sl2, -Lc));
+          const float p1 = fast_exp2(fmaf(sv[r0 + 1], sl2, -Lc));
+          w[q] = cvt_pk_bf16(p0 * (dp[r0] - Dc), p1 * (dp[r0 + 1] - Dc));
+        }
+        sb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+      for (int i = 0; i < NTL; ++i)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          acc[i] = mfma_32x32x16(tr_operand<RB>(kd, traddr[i], kk), sb[kk], acc[i]);
+    }
+  };
+
+  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(kb, kb);
+  for (int kb = 0; kb < nblk; kb += 3) {
+    step(std::integral_constant<int, 0>{}, kb);
+    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
+    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+  }
+
+  // Lane holds dims 32 i + 8 j + 4 hb .. + 4 of its column.
+  if (!colv) return;
+  char *orow = static_cast<char *>(MODE == 0 ? p.out : p.dq) + row_q(p, b, t, g * G + head, D) * 2;
+  float sc_out;
+  if constexpr (MODE == 0) {
+    const float lt = ls + __shfl_xor(ls, 32, 64);
+    sc_out = 1.0f / lt;
+    if (hb == 0) p.lse[(int64_t(u) * p.n + t) * G + head] = m + __log2f(lt);
+  } else {
+    sc_out = sl2 / kLog2e;   // 1 / sqrt(d)
+  }
+#pragma unroll
+  for (int i = 0; i < NTL; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float x0 = acc[i][4 * j] * sc_out, x1 = acc[i][4 * j + 1] * sc_out;
+      if (MODE == 1 && i == 0 && j == 0 && hb == 0) x0 = 0.0f;   // dq[0]: through omega only
+      const uint32_t lo = cvt_pk_bf16(x0, x1);
+      const uint32_t hi = cvt_pk_bf16(acc[i][4 * j + 2] * sc_out, acc[i][4 * j + 3] * sc_out);
+      *reinterpret_cast<uint2 *>(orow + (32 * i + 8 * j + 4 * hb) * 2) = make_uint2(lo, hi);
+    }
+}
+
+// State-major kernel: dK~, dV~ and the mask gradient of 128 states per
+// workgroup (32 per wave); query rows (token-major, G per token) stream
+// through LDS in blocks of 32 rows.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams p, int ntiles) {
+  constexpr int kSt = 3;
+  constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
+  constexpr int DPW = BLK / 16 / kThreads;
+  static_assert(DPW >= 1, "block split");
+  __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
+
+  const int U = p.batch * p.hkv;
+  const int bid = blockIdx.x;
+  const int xcd = bid & 7, r = bid >> 3;
+  const int ul = r / ntiles, tile = r - ul * ntiles;   // earliest states (most rows) first
+  const int u = ul * 8 + xcd;
+  if (u >= U) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hb = lane >> 5;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int s0 = tile * 128 + wave * 32;             // this wave's first state
+  const int js = s0 + col;                            // this lane's state (column)
+  const bool sv_ok = js < p.n;
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  const float sl2 = p.scale_log2;
+
+  // K~ and V~ of the lane's state as B operands (dims 16 ks + 8 hb .. + 8);
+  // key element 0 (the mask carrier) is left out of the scores.
+  uint4 kop[KS], vop[KS];
+  float bias = 0.0f;
+  {
+    const int64_t so = (int64_t(u) * p.n + (sv_ok ? js : 0)) * RB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kop[ks] = sv_ok ? ld16(static_cast<const char *>(p.ks) + so + ks * 32 + hb * 16) : zero4;
+      vop[ks] = sv_ok ? ld16(static_cast<const char *>(p.vs) + so + ks * 32 + hb * 16) : zero4;
+    }
+    if (hb == 0) kop[0].x &= 0xffff0000u;
+    // the mask entry as the forward used it: bf16 of mask * sqrt(d), back to log2 units
+    if (sv_ok)
+      bias = __uint_as_float(bf16_bits(p.mask[int64_t(u) * p.n + js] * (kLog2e / sl2)) << 16) * sl2;
+  }
+
+  // Query rows r = t * G + h; the workgroup needs rows of tokens >= its
+  // first state.
+  const int row_lo = tile * 128 * G;
+  const int nrows = p.n * G;
+  const int qb0 = row_lo >> 5, qb1 = (nrows + 31) >> 5;
+  const int nblk = qb1 - qb0;
+  const uint32_t ring = lds_offset(smem);
+  int64_t qoff[DPW];
+  uint32_t loff[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int c = (i * kWaves + wave) * 64 + lane;
+    const int row = c / CPR, pc = c - row * CPR;
+    loff[i] = row;
+    qoff[i] = (pc ^ v_swizzle<CPR>(row)) * 16;
+  }
+  auto issue = [&](int qb, int st) {
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const uint32_t dst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
+      const int rg = min(qb * 32 + int(loff[i]), nrows - 1);   // rows past the sequence: in bounds, masked
+      const int tq = rg / G, h = rg - tq * G;
+      const int64_t ro = row_q(p, b, tq, g * G + h, D) * 2 + qoff[i];
+      dma16(dst, static_cast<const char *>(p.q) + ro);
+      dma16(dst + BLK, static_cast<const char *>(p.dout) + ro);
+    }
+  };
+  const int qrow = score_slot(col);
+  uint32_t raddr[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) raddr[ks] = row_offset<D, 1>(qrow, ks, hb);
+  uint32_t traddr[NTL];
+  tr_offsets<D>(lane, traddr);
+
+  f32x16_t dk[NTL], dv[NTL];
+#pragma unroll
+  for (int i = 0; i < NTL; ++i) dk[i] = dv[i] = f32x16_t{};
+  float dm = 0.0f;
+
+  auto step = [&](auto stage_c, int kb) {
+    constexpr int ST = decltype(stage_c)::value;
+    const int after = min(nblk - 1 - kb, kSt - 2);
+    if (after >= 1) wait_vmcnt<2 * DPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kb + kSt - 1 < nblk) issue(qb0 + kb + kSt - 1, (ST + kSt - 1) % kSt);
+    const int rb = (qb0 + kb) * 32;                  // first row of the block
+    if (rb + 31 < s0 * G) return;                    // every row precedes this wave's states
+    const char *qd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
+    const char *dd = qd + BLK;
+    f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(qd + raddr[ks]), kop[ks], sc);
+      dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
+    }
+    // register 8 kk + q of this lane: row rb + 16 kk + 8 hb + q (pi-permuted rows)
+    float Lr[16], Dr[16];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int rg = min(rb + 16 * kk + 8 * hb + q, nrows - 1);
+        const int tq = rg / G, h = rg - tq * G;
+        Lr[8 * kk + q] = p.lse[(int64_t(u) * p.n + tq) * G + h];
+        Dr[8 * kk + q] = p.dsum[(int64_t(u) * p.n + tq) * G + h];
+      }
+    uint4 pa[2], da[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint32_t wp[4], wd[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float pv[2], dsv[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int i = 8 * kk + 2 * q + e;
+          const int rg = rb + 16 * kk + 8 * hb + 2 * q + e;
+          const int tq = rg / G;
+          const bool vis = sv_ok && rg < nrows && tq >= js;
+          const float x = sc[i] * sl2 + (tq > js ? bias : 0.0f);
+          pv[e] = vis ? fast_exp2(x - Lr[i]) : 0.0f;
+          dsv[e] = pv[e] * (dp[i] - Dr[i]);
+          if (vis && tq > js) dm += dsv[e];
+        }
+        wp[q] = cvt_pk_bf16(pv[0], pv[1]);
+        wd[q] = cvt_pk_bf16(dsv[0], dsv[1]);
+      }
+      pa[kk] = make_uint4(wp[0], wp[1], wp[2], wp[3]);
+      da[kk] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < NTL; ++i)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        dv[i] = mfma_32x32x16(pa[kk], tr_operand<RB>(dd, traddr[i], kk), dv[i]);
+        dk[i] = mfma_32x32x16(da[kk], tr_operand<RB>(qd, traddr[i], kk), dk[i]);
+      }
+  };
+
+  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(qb0 + kb, kb);
+  for (int kb = 0; kb < nblk; kb += 3) {
+    step(std::integral_constant<int, 0>{}, kb);
+    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
+    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+  }
+
+  // Outputs: C[state][dim] -- lane holds dim 32 i + col of states
+  // s0 + 8 (j / 4) + 4 hb + j % 4.
+  dm += __shfl_xor(dm, 32, 64);
+  if (hb == 0 && sv_ok) p.dmask[int64_t(u) * p.n + js] = dm;
+  const float sc_k = sl2 / kLog2e;
+#pragma unroll
+  for (int i = 0; i < NTL; ++i)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int st = s0 + 8 * (j >> 2) + 4 * hb + (j & 3);
+      if (st >= p.n) continue;
+      const int dim = 32 * i + col;
+      const int64_t o = (int64_t(u) * p.n + st) * D + dim;
+      p.dks[o] = dim == 0 ? 0.0f : dk[i][j] * sc_k;
+      p.dvs[o] = dv[i][j];
+    }
+}
+
 int blocks_for(int64_t threads) {
   return static_cast<int>((threads + kThreads - 1) / kThreads);
 }
@@ -501,24 +966,45 @@ int blocks_for(int64_t threads) {
 template <int ES, int D, int G>
 hipError_t train_forward_impl(const TrainParams &p, hipStream_t s) {
   const int U = p.batch * p.hkv;
+  const size_t states = size_t(U) * p.n * D * ES, pad = size_t(32) * D * ES;
+  hipError_t e = launch_fill_u8(static_cast<char *>(p.ks) + states, pad, s);
+  if (e == hipSuccess) e = launch_fill_u8(static_cast<char *>(p.vs) + states, pad, s);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((train_decide_kernel<ES, D>), dim3(blocks_for(int64_t(U) * p.n)), dim3(kThreads),
                      0, s, p);
   hipLaunchKernelGGL((train_states_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
-  const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
-  hipLaunchKernelGGL((train_fwd_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * ngroups * 64)),
-                     dim3(kThreads), 0, s, p, ngroups);
+  if constexpr (ES == 2) {
+    constexpr int TW = kWaves * (32 / G);
+    const int ntiles = (p.n + TW - 1) / TW;
+    hipLaunchKernelGGL((train_qmajor_kernel<D, G, 0>), dim3(8 * ((U + 7) / 8) * ntiles),
+                       dim3(kThreads), 0, s, p, ntiles);
+  } else {
+    const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
+    hipLaunchKernelGGL((train_fwd_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * ngroups * 64)),
+                       dim3(kThreads), 0, s, p, ngroups);
+  }
   return hipGetLastError();
 }
 
 template <int ES, int D, int G>
 hipError_t train_backward_impl(const TrainParams &p, hipStream_t s) {
   const int U = p.batch * p.hkv;
-  const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
-  hipLaunchKernelGGL((train_dq_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * ngroups * 64)),
-                     dim3(kThreads), 0, s, p, ngroups);
-  const int nblocks = (p.n + 3) / 4;
-  hipLaunchKernelGGL((train_dkv_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * nblocks * 64)),
-                     dim3(kThreads), 0, s, p, nblocks);
+  if constexpr (ES == 2) {
+    constexpr int TW = kWaves * (32 / G);
+    const int ntiles = (p.n + TW - 1) / TW;
+    hipLaunchKernelGGL((train_qmajor_kernel<D, G, 1>), dim3(8 * ((U + 7) / 8) * ntiles),
+                       dim3(kThreads), 0, s, p, ntiles);
+    const int stiles = (p.n + 127) / 128;
+    hipLaunchKernelGGL((train_dkv_mfma_kernel<D, G>), dim3(8 * ((U + 7) / 8) * stiles),
+                       dim3(kThreads), 0, s, p, stiles);
+  } else {
+    const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
+    hipLaunchKernelGGL((train_dq_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * ngroups * 64)),
+                       dim3(kThreads), 0, s, p, ngroups);
+    const int nblocks = (p.n + 3) / 4;
+    hipLaunchKernelGGL((train_dkv_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * nblocks * 64)),
+                       dim3(kThreads), 0, s, p, nblocks);
+  }
   hipLaunchKernelGGL((train_tokens_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
   hipLaunchKernelGGL((train_neurons_kernel<ES, D>), dim3(blocks_for(int64_t(U) * p.n)),
                      dim3(kThreads), 0, s, p);

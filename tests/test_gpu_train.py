@@ -53,6 +53,10 @@ CASES = [
     ("bf16", 128, 1, 2, 2, 100, 12, 5.0, 0.1, [2.0, 6.0], "lead", True),
     ("bf16", 128, 8, 1, 2, 64, 12, 5.0, 0.5, [4.0, 1.0], "lead", False),
     ("bf16", 64, 2, 1, 2, 80, 5, 2.0, 1.0, [3.0, 10.0], "lead", True),
+    # several 128-token tiles and 32-row blocks, ragged tail
+    ("bf16", 128, 1, 1, 2, 300, 12, 5.0, 0.1, [1.0, 8.0], "lead", True),
+    ("bf16", 64, 4, 1, 2, 201, 12, 5.0, 0.1, [2.0, 4.0], "uniform", False),
+    ("bf16", 128, 2, 2, 1, 161, 64, 5.0, 0.2, [16.0], "lead", True),
 ]
 
 
