@@ -46,8 +46,8 @@ TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int el
   L.omega = take(U * N * 4);
   L.z = take(U * N * 4);
   L.mask = take(U * N * 4);
-  L.lse = take(U * G * N * 4);        // [U][n][G]
-  L.dsum = take(U * G * N * 4);
+  L.lse = take((U * G * N + 32) * 4);   // [U][n][G], padded for 32-row statistics transfers
+  L.dsum = take((U * G * N + 32) * 4);
   L.dks = take(U * N * D * 4);
   L.dvs = take(U * N * D * 4);
   L.dmask = take(U * N * 4);
@@ -101,12 +101,15 @@ __global__ __launch_bounds__(kThreads) void train_decide_kernel(TrainParams p) {
   if (t == p.n - 1) p.mask[i] = 0.0f;   // the last state has no successor
 }
 
-// Unrolled states, one wave per (unit, 64 positions): state j is the
-// closed-form partial accumulation over its window, walked from j down to
-// the window start with the running product of alphas.
+// Unrolled states, one wave per (unit, 64 positions), NP positions at a
+// time: state j is the closed-form partial accumulation over its window,
+// summed from token j down to the window start with the running product of
+// alphas.  The NP positions share their tokens' rows, which are loaded in
+// batches and added to every position whose window holds them (each
+// position's sum runs over its tokens in the same descending order).
 template <int ES, int D>
 __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
-  constexpr int E = D / 64, kB = 4;
+  constexpr int E = D / 64, NP = 8, kB = 8;
   const int u = blockIdx.y, lane = threadIdx.x;
   const int b = u / p.hkv, g = u - b * p.hkv;
   const int j0 = blockIdx.x * 64, j1 = min(j0 + 64, p.n);
@@ -116,16 +119,23 @@ __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
   const char *vb = static_cast<const char *>(p.v) + (row_k(p, b, 0, g, D) + lane * E) * ES;
   const int64_t rs = int64_t(p.hkv) * D * ES;   // bytes between tokens
   const float sqrt_d = kLog2e / p.scale_log2;
-  for (int j = j0; j < j1; ++j) {
-    const int a = max(0, j - p.window + 1);
-    float sk[E], sv[E], zs = 0.0f, P = 1.0f;
+  for (int jg = j0; jg < j1; jg += NP) {
+    const int np = min(NP, j1 - jg);
+    const int jl = jg + np - 1;                   // last position of the group
+    const int lo = max(0, jg - p.window + 1);     // first token any of them needs
+    float sk[NP][E], sv[NP][E], zs[NP], P[NP];
 #pragma unroll
-    for (int e = 0; e < E; ++e) sk[e] = sv[e] = 0.0f;
-    for (int t0 = j; t0 >= a; t0 -= kB) {
+    for (int i = 0; i < NP; ++i) {
+      zs[i] = 0.0f;
+      P[i] = 1.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) sk[i][e] = sv[i][e] = 0.0f;
+    }
+    for (int t0 = jl; t0 >= lo; t0 -= kB) {
       float kk[kB][E], vv[kB][E], wa[kB], wo[kB];
 #pragma unroll
       for (int q = 0; q < kB; ++q) {
-        const int t = max(t0 - q, a);
+        const int t = max(t0 - q, lo);
         load_e<ES, E>(kb + t * rs, kk[q]);
         load_e<ES, E>(vb + t * rs, vv[q]);
         wa[q] = al[t];
@@ -133,32 +143,43 @@ __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
       }
 #pragma unroll
       for (int q = 0; q < kB; ++q) {
-        if (t0 - q < a) break;
+        const int t = t0 - q;
+        if (t < lo) break;
         if (lane == 0) kk[q][0] = 0.0f;   // k_t[0] <- 0
-        const float c = wo[q] * P;        // omega_t * prod_{r = t+1 .. j} alpha_r
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          sk[e] = fmaf(c, kk[q][e], sk[e]);
-          sv[e] = fmaf(c, vv[q][e], sv[e]);
+        for (int i = 0; i < NP; ++i) {
+          const int j = jg + i;
+          if (i >= np || t > j || t < j - p.window + 1) continue;
+          const float c = wo[q] * P[i];    // omega_t * prod_{r = t+1 .. j} alpha_r
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            sk[i][e] = fmaf(c, kk[q][e], sk[i][e]);
+            sv[i][e] = fmaf(c, vv[q][e], sv[i][e]);
+          }
+          zs[i] += c;
+          P[i] *= wa[q];
         }
-        zs += c;
-        P *= wa[q];
       }
     }
-    const float inv = 1.0f / zs;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      sk[e] *= inv;
-      sv[e] *= inv;
+    for (int i = 0; i < NP; ++i) {
+      if (i >= np) break;
+      const int j = jg + i;
+      const float inv = 1.0f / zs[i];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        sk[i][e] *= inv;
+        sv[i][e] *= inv;
+      }
+      // Element 0 of a key state is never part of a score; it carries the
+      // state's mask entry times sqrt(d), which the matrix-core kernels add
+      // to the scores through a query element fixed at 1.
+      if (lane == 0) sk[i][0] = p.mask[int64_t(u) * p.n + j] * sqrt_d;
+      const int64_t o = (int64_t(u) * p.n + j) * D + lane * E;
+      store_e<ES, E>(static_cast<char *>(p.ks) + o * ES, sk[i]);
+      store_e<ES, E>(static_cast<char *>(p.vs) + o * ES, sv[i]);
+      if (lane == 0) p.z[int64_t(u) * p.n + j] = zs[i];
     }
-    // Element 0 of a key state is never part of a score; it carries the
-    // state's mask entry times sqrt(d), which the matrix-core kernels add to
-    // the scores through a query element fixed at 1.
-    if (lane == 0) sk[0] = p.mask[int64_t(u) * p.n + j] * sqrt_d;
-    const int64_t o = (int64_t(u) * p.n + j) * D + lane * E;
-    store_e<ES, E>(static_cast<char *>(p.ks) + o * ES, sk);
-    store_e<ES, E>(static_cast<char *>(p.vs) + o * ES, sv);
-    if (lane == 0) p.z[int64_t(u) * p.n + j] = zs;
   }
 }
 
@@ -402,53 +423,84 @@ __global__ __launch_bounds__(kThreads) void train_dkv_kernel(TrainParams p, int 
   }
 }
 
-// States -> tokens, part 1, one wave per (unit, 64 tokens): token t feeds
-// states j = t .. t + w - 1 with weight c_tj / z_j; its key and value
-// gradients gather those states' gradients, and e_tj = d loss / d c_tj =
-// ((k^_t - K~_j) . dK~_j + (v_t - V~_j) . dV~_j) / z_j is kept for part 2.
+// States -> tokens, part 1, one wave per (unit, 64 tokens), NT tokens at a
+// time: token t feeds states j = t .. t + w - 1 with weight c_tj / z_j; its
+// key and value gradients gather those states' gradients, and e_tj = d loss /
+// d c_tj = ((k^_t - K~_j) . dK~_j + (v_t - V~_j) . dV~_j) / z_j is kept for
+// part 2.  The NT tokens share their states, which are loaded in batches.
 template <int ES, int D>
 __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
-  constexpr int E = D / 64;
+  constexpr int E = D / 64, NT = 8, kB = 4;
   const int u = blockIdx.y, lane = threadIdx.x;
   const int b = u / p.hkv, g = u - b * p.hkv;
   const int t0 = blockIdx.x * 64, t1 = min(t0 + 64, p.n);
   const float *al = p.alpha + int64_t(u) * p.n;
   const float *om = p.omega + int64_t(u) * p.n;
   const float *zz = p.z + int64_t(u) * p.n;
-  for (int t = t0; t < t1; ++t) {
-    const int64_t ro = row_k(p, b, t, g, D) + lane * E;
-    float kt[E], vt[E];
-    load_e<ES, E>(static_cast<const char *>(p.k) + ro * ES, kt);
-    load_e<ES, E>(static_cast<const char *>(p.v) + ro * ES, vt);
-    if (lane == 0) kt[0] = 0.0f;
-    float dk[E], dv[E], P = 1.0f;
+  const int W = p.window;
+  for (int tg = t0; tg < t1; tg += NT) {
+    const int nt = min(NT, t1 - tg);
+    float kt[NT][E], vt[NT][E], dk[NT][E], dv[NT][E], P[NT], wt[NT];
 #pragma unroll
-    for (int e = 0; e < E; ++e) dk[e] = dv[e] = 0.0f;
-    const int jl = min(t + p.window - 1, p.n - 1);
-    for (int j = t; j <= jl; ++j) {
-      if (j > t) P *= al[j];
-      const float zj = zz[j];
-      const float cz = om[t] * P / zj;
-      const int64_t so = (int64_t(u) * p.n + j) * D + lane * E;
-      float ks[E], vs[E], dks[E], dvs[E];
-      load_e<ES, E>(static_cast<const char *>(p.ks) + so * ES, ks);
-      load_e<ES, E>(static_cast<const char *>(p.vs) + so * ES, vs);
-      float ev = 0.0f;
+    for (int i = 0; i < NT; ++i) {
+      const int t = tg + min(i, nt - 1);
+      const int64_t ro = row_k(p, b, t, g, D) + lane * E;
+      load_e<ES, E>(static_cast<const char *>(p.k) + ro * ES, kt[i]);
+      load_e<ES, E>(static_cast<const char *>(p.v) + ro * ES, vt[i]);
+      if (lane == 0) kt[i][0] = 0.0f;
+      wt[i] = om[t];
+      P[i] = 1.0f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        dks[e] = p.dks[so + e];
-        dvs[e] = p.dvs[so + e];
-        dk[e] = fmaf(cz, dks[e], dk[e]);
-        dv[e] = fmaf(cz, dvs[e], dv[e]);
-        ev = fmaf(kt[e] - ks[e], dks[e], ev);
-        ev = fmaf(vt[e] - vs[e], dvs[e], ev);
-      }
-      ev = wsum(ev) / zj;
-      if (lane == 0) p.e[(int64_t(u) * p.n + t) * p.window + (j - t)] = ev;
+      for (int e = 0; e < E; ++e) dk[i][e] = dv[i][e] = 0.0f;
     }
-    if (lane == 0) dk[0] = 0.0f;   // element 0 gets the decision gradient in part 2
-    store_e<ES, E>(static_cast<char *>(p.dk) + ro * ES, dk);
-    store_e<ES, E>(static_cast<char *>(p.dv) + ro * ES, dv);
+    const int jl = min(tg + nt - 1 + W - 1, p.n - 1);   // last state any of them feeds
+    for (int jb = tg; jb <= jl; jb += kB) {
+      float ks[kB][E], vs[kB][E], dks[kB][E], dvs[kB][E], zj[kB], aj[kB];
+#pragma unroll
+      for (int q = 0; q < kB; ++q) {
+        const int j = min(jb + q, jl);
+        const int64_t so = (int64_t(u) * p.n + j) * D + lane * E;
+        load_e<ES, E>(static_cast<const char *>(p.ks) + so * ES, ks[q]);
+        load_e<ES, E>(static_cast<const char *>(p.vs) + so * ES, vs[q]);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          dks[q][e] = p.dks[so + e];
+          dvs[q][e] = p.dvs[so + e];
+        }
+        zj[q] = zz[j];
+        aj[q] = al[j];
+      }
+#pragma unroll
+      for (int q = 0; q < kB; ++q) {
+        const int j = jb + q;
+        if (j > jl) break;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+          const int t = tg + i;
+          if (i >= nt || j < t || j > t + W - 1) continue;
+          if (j > t) P[i] *= aj[q];            // prod_{r = t+1 .. j} alpha_r
+          const float cz = wt[i] * P[i] / zj[q];
+          float ev = 0.0f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            dk[i][e] = fmaf(cz, dks[q][e], dk[i][e]);
+            dv[i][e] = fmaf(cz, dvs[q][e], dv[i][e]);
+            ev = fmaf(kt[i][e] - ks[q][e], dks[q][e], ev);
+            ev = fmaf(vt[i][e] - vs[q][e], dvs[q][e], ev);
+          }
+          ev = wsum(ev) / zj[q];
+          if (lane == 0) p.e[(int64_t(u) * p.n + t) * W + (j - t)] = ev;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      if (i >= nt) break;
+      const int64_t ro = row_k(p, b, tg + i, g, D) + lane * E;
+      if (lane == 0) dk[i][0] = 0.0f;   // element 0 gets the decision gradient in part 2
+      store_e<ES, E>(static_cast<char *>(p.dk) + ro * ES, dk[i]);
+      store_e<ES, E>(static_cast<char *>(p.dv) + ro * ES, dv[i]);
+    }
   }
 }
 
@@ -798,8 +850,9 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
   constexpr int kSt = 3;
   constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
+  constexpr int SLOT = 2 * BLK + 256;   // query rows, dO rows, 32 x (L, D) statistics
   static_assert(DPW >= 1, "block split");
-  __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
+  __shared__ __align__(16) unsigned char smem[kSt * SLOT];
 
   const int U = p.batch * p.hkv;
   const int bid = blockIdx.x;
@@ -850,16 +903,22 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
     loff[i] = row;
     qoff[i] = (pc ^ v_swizzle<CPR>(row)) * 16;
   }
+  // Statistics of rows 8 wave .. 8 wave + 7 of a block: lanes 0, 1 move their
+  // L (32 bytes), lanes 2, 3 their D ([U][n][G] is row-contiguous and padded
+  // by 32 rows), so every wave issues the same number of transfers.
+  const char *stat_src = reinterpret_cast<const char *>(lane < 2 ? p.lse : p.dsum) +
+                         (int64_t(u) * p.n * G + 8 * wave) * 4 + (lane & 1) * 16;
   auto issue = [&](int qb, int st) {
 #pragma unroll
     for (int i = 0; i < DPW; ++i) {
-      const uint32_t dst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
+      const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
       const int rg = min(qb * 32 + int(loff[i]), nrows - 1);   // rows past the sequence: in bounds, masked
       const int tq = rg / G, h = rg - tq * G;
       const int64_t ro = row_q(p, b, tq, g * G + h, D) * 2 + qoff[i];
       dma16(dst, static_cast<const char *>(p.q) + ro);
       dma16(dst + BLK, static_cast<const char *>(p.dout) + ro);
     }
+    if (lane < 4) dma16(ring + st * SLOT + 2 * BLK + wave * 64, stat_src + int64_t(qb) * 128);
   };
   const int qrow = score_slot(col);
   uint32_t raddr[KS];
@@ -876,13 +935,13 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
     const int after = min(nblk - 1 - kb, kSt - 2);
-    if (after >= 1) wait_vmcnt<2 * DPW>();
+    if (after >= 1) wait_vmcnt<2 * DPW + 1>();
     else wait_vmcnt<0>();
     __syncthreads();
     if (kb + kSt - 1 < nblk) issue(qb0 + kb + kSt - 1, (ST + kSt - 1) % kSt);
     const int rb = (qb0 + kb) * 32;                  // first row of the block
     if (rb + 31 < s0 * G) return;                    // every row precedes this wave's states
-    const char *qd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
+    const char *qd = reinterpret_cast<const char *>(smem) + ST * SLOT;
     const char *dd = qd + BLK;
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
@@ -890,17 +949,23 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
       sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(qd + raddr[ks]), kop[ks], sc);
       dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
     }
-    // register 8 kk + q of this lane: row rb + 16 kk + 8 hb + q (pi-permuted rows)
+    // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
+    // 8 hb + q (pi-permuted rows), from the block's LDS statistics area
+    // ([4][8 L, 8 D] floats).
+    const float *sd = reinterpret_cast<const float *>(qd + 2 * BLK);
     float Lr[16], Dr[16];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int rg = min(rb + 16 * kk + 8 * hb + q, nrows - 1);
-        const int tq = rg / G, h = rg - tq * G;
-        Lr[8 * kk + q] = p.lse[(int64_t(u) * p.n + tq) * G + h];
-        Dr[8 * kk + q] = p.dsum[(int64_t(u) * p.n + tq) * G + h];
-      }
+    for (int kk = 0; kk < 2; ++kk) {
+      const float *e8 = sd + (2 * kk + hb) * 16;
+      const float4 l0 = *reinterpret_cast<const float4 *>(e8);
+      const float4 l1 = *reinterpret_cast<const float4 *>(e8 + 4);
+      const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 8);
+      const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 12);
+      Lr[8 * kk + 0] = l0.x; Lr[8 * kk + 1] = l0.y; Lr[8 * kk + 2] = l0.z; Lr[8 * kk + 3] = l0.w;
+      Lr[8 * kk + 4] = l1.x; Lr[8 * kk + 5] = l1.y; Lr[8 * kk + 6] = l1.z; Lr[8 * kk + 7] = l1.w;
+      Dr[8 * kk + 0] = d0.x; Dr[8 * kk + 1] = d0.y; Dr[8 * kk + 2] = d0.z; Dr[8 * kk + 3] = d0.w;
+      Dr[8 * kk + 4] = d1.x; Dr[8 * kk + 5] = d1.y; Dr[8 * kk + 6] = d1.z; Dr[8 * kk + 7] = d1.w;
+    }
     uint4 pa[2], da[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -916,7 +981,7 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
           const bool vis = sv_ok && rg < nrows && tq >= js;
           const float x = sc[i] * sl2 + (tq > js ? bias : 0.0f);
           pv[e] = vis ? fast_exp2(x - Lr[i]) : 0.0f;
-          dsv[e] = pv[e] * (dp[i] - Dr[i]);
+          dsv[e] = vis ? pv[e] * (dp[i] - Dr[i]) : 0.0f;   // statistics past the rows are not read
           if (vis && tq > js) dm += dsv[e];
         }
         wp[q] = cvt_pk_bf16(pv[0], pv[1]);
