@@ -198,9 +198,8 @@ constexpr int kMaxWindow = 64;
 // (its page-table slice is held in LDS).
 constexpr int kPromptMaxPages = 1024;
 
-// Prompt-phase attention; bf16 runs on matrix cores (value pages of caches
-// stored as rows are transposed in place around it, over the pages of the
-// last allocation named in ctrl), fp32 on the vector ALUs.
+// Prompt-phase attention; bf16 runs on matrix cores (value pages read as rows,
+// or as the transposed pages of grouped-query caches), fp32 on the vector ALUs.
 hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
                                 const PromptParams &p, const Control *ctrl, hipStream_t s);
 
