@@ -93,3 +93,38 @@ def test_train_forward_backward(torch_cuda, case):
     errs = [_grad_close(f64(x), r.numpy(), dtype, name)
             for x, r, name in ((dq, rq, "dq"), (dk, rk, "dk"), (dv, rv, "dv"))]
     log(f"  out {o_err.max():.2e}  dq {errs[0]:.2e}  dk {errs[1]:.2e}  dv {errs[2]:.2e} (of scale)")
+
+
+def test_train_full_size_sampled(torch_cuda):
+    """The bench's training workload (one Llama-2-7B layer: 4 x 4096 tokens,
+    32 heads, d = 128, bf16, c = 5, tau = 0.1, w = 12) in its launch
+    configuration; one (batch row, head) unit checked in full against the
+    oracle -- forward rows, relaxed decisions and dq, dk, dv of that unit
+    (units are independent, so its slice of the inputs fixes them)."""
+    import torch
+    import paper_2403_09636_amd as P
+    import workloads as W
+    w = W.WORKLOADS["llama7b_train"]
+    log("case train full size sampled")
+    q, k, v, noise, dout = W.train_inputs_torch(w, 0, "cuda")
+    B, n = w.batch, w.prompt_len
+    cfg = P.make_train_config(B, n, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                              W.TRAIN_C, W.TRAIN_TAU, W.TRAIN_WINDOW)
+    tr = P.DMCTrainer(cfg)
+    alpha = torch.empty((B, n, w.num_kv_heads), dtype=torch.float32, device="cuda")
+    out = tr.forward(q, k, v, noise, alpha=alpha)
+    dq, dk, dv = tr.backward(q, k, v, noise, out, dout)
+    torch.cuda.synchronize()
+    b, g = 2, 19
+    sl = (slice(b, b + 1), slice(None), slice(g, g + 1))
+    qo, ko, vo, do = (torch.from_numpy(f64(x[sl])) for x in (q, k, v, dout))
+    no = torch.from_numpy(f64(noise[sl]))
+    o_ref, a_ref = T.train_forward(qo, ko, vo, no, W.TRAIN_C, W.TRAIN_TAU, W.TRAIN_WINDOW)
+    rq, rk, rv = T.train_backward(qo, ko, vo, no, do, None, W.TRAIN_C, W.TRAIN_TAU, W.TRAIN_WINDOW)
+    a_err = np.abs(f64(alpha[sl]) - a_ref.detach().numpy()).max()
+    assert a_err < 1e-5, f"alpha error {a_err}"
+    o_err = np.abs(f64(out[sl]) - o_ref.detach().numpy())
+    assert (o_err <= 2e-2 + 1e-2 * np.abs(o_ref.detach().numpy())).all(), o_err.max()
+    errs = [_grad_close(f64(x[sl]), r.numpy(), "bf16", name)
+            for x, r, name in ((dq, rq, "dq"), (dk, rk, "dk"), (dv, rv, "dv"))]
+    log(f"  unit {(b, g)}: out {o_err.max():.2e}  dq {errs[0]:.2e}  dk {errs[1]:.2e}  dv {errs[2]:.2e}")

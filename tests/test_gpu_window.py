@@ -131,3 +131,38 @@ def test_window_import_unsupported(torch_cuda):
         cache.import_(0, K, K.clone(), lens, z)
     assert e.value.status == P.binding.DMC_ERR_UNSUPPORTED
     cache.check()
+
+
+def test_window_prompt_sampled_7b_layer(torch_cuda):
+    """Llama-2-7B layer shape (B=2, n=4096, 32 heads, d=128, CR per head in
+    {1, 2, 4, 8}) with w = 12, in the bench's launch configuration: every
+    output row of 4 sampled units against a per-unit windowed oracle, then 4
+    decode steps with those units' outputs checked."""
+    import torch
+    import oracle
+    import paper_2403_09636_amd as P
+    import workloads as W
+    from tests.gpu_helpers import assert_close, f64
+    log("case window prompt 7b layer sampled")
+    w = W.scaled(W.WORKLOADS["llama7b_layer"], batch=2)
+    k, v, q = W.prompt_full_torch(w, 0, "cuda")
+    n = w.prompt_len
+    cfg = P.make_config(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                        w.page_size, n + 8, max_prompt_len=n, window=12)
+    cache = P.DMCCache(cfg, device="cuda")
+    out = cache.prefill_attend(0, k, v, q)
+    steps = [W.decode_inputs_torch(w, s, 0, "cuda") for s in range(4)]
+    outs = [cache.decode_step(0, *x) for x in steps]
+    torch.cuda.synchronize()
+    cache.check()
+    units = [(0, 0), (1, 31), (0, 17), (1, 6)]
+    for b, g in units:
+        orc = oracle.DMCOracle(1, 1, 1, 1, w.head_dim, max_slots=n + 8, window=12)
+        o_ref, _ = orc.prefill_attend(0, f64(q[b:b + 1, :, g:g + 1]), f64(k[b:b + 1, :, g:g + 1]),
+                                      f64(v[b:b + 1, :, g:g + 1]))
+        err = assert_close(f64(out[b, :, g]), o_ref[0, :, 0], "bf16", f"prompt unit {(b, g)}")
+        for (qs, ks, vs), o in zip(steps, outs):
+            o_ref, _ = orc.decode_step(0, f64(qs[b:b + 1, g:g + 1]), f64(ks[b:b + 1, g:g + 1]),
+                                       f64(vs[b:b + 1, g:g + 1]))
+            err = max(err, assert_close(f64(o[b, g]), o_ref[0, 0], "bf16", f"decode unit {(b, g)}"))
+        log(f"  unit {(b, g)} max abs err {err:.3e}")
