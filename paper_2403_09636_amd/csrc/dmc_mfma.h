@@ -25,6 +25,15 @@ __device__ __forceinline__ int v_swizzle(int row) {
   return CPR == 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
 }
 __device__ __forceinline__ int vt_swizzle(int dim) { return (dim >> 2) & 3; }
+// Rows read both ways (as 16-byte row slices and transposed): for 256-byte
+// rows the two 2-bit halves of the row's low nibble are swapped -- distinct
+// over any 16 consecutive rows (row reads) and, shifted right by one, over
+// any 4 consecutive rows (transposed reads take chunk pairs 2c, 2c + 1).
+// Shorter rows keep the value swizzle.
+template <int CPR>
+__device__ __forceinline__ int dual_swizzle(int row) {
+  return CPR == 16 ? (((row & 3) << 2) | ((row >> 2) & 3)) : v_swizzle<CPR>(row);
+}
 __device__ __forceinline__ int score_slot(int m) {   // pi(m): bits 2 and 3 swapped
   return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1);
 }

@@ -587,35 +587,46 @@ __global__ __launch_bounds__(kThreads) void train_neurons_kernel(TrainParams p) 
 // swizzle.
 // ---------------------------------------------------------------------------
 
-// Transposed operand: A or B slice "rows r0 + 8 half + 0..7 of dim 32 t + col"
-// from a 32-row block stored with the value swizzle (vaddr per tile t).
+// Swizzle of a block's rows: 0 key (row reads), 1 value (transposed reads),
+// 2 dual (both).
+template <int CPR, int SW>
+__device__ __forceinline__ int block_swizzle(int row) {
+  return SW == 0 ? k_swizzle<CPR>(row) : SW == 1 ? v_swizzle<CPR>(row) : dual_swizzle<CPR>(row);
+}
+
+// Transposed operand: A or B slice "rows 16 kk + 8 half + 0..7 of dim 32 t +
+// col" of a 32-row block (vaddr[t][h]: offsets of the two 4-row halves).
 template <int RB>
-__device__ __forceinline__ uint4 tr_operand(const char *blk, uint32_t vaddr, int kk) {
-  const uint2 h0 = ds_read_tr16(blk + vaddr + 16 * kk * RB);
-  const uint2 h1 = ds_read_tr16(blk + vaddr + (16 * kk + 4) * RB);
+__device__ __forceinline__ uint4 tr_operand(const char *blk, const uint32_t (&vaddr)[2], int kk) {
+  const uint2 h0 = ds_read_tr16(blk + vaddr[0] + 16 * kk * RB);
+  const uint2 h1 = ds_read_tr16(blk + vaddr[1] + 16 * kk * RB);
   return make_uint4(h0.x, h0.y, h1.x, h1.y);
 }
 
-// Per-lane offsets of the transposed reads (one per 32-dim tile).
-template <int D>
-__device__ __forceinline__ void tr_offsets(int lane, uint32_t (&vaddr)[D / 32]) {
+// Per-lane offsets of the transposed reads (per 32-dim tile and 4-row half)
+// for a block stored with swizzle SW (1 or 2): a 16-lane group points at
+// four 8-byte pieces of each of 4 rows.
+template <int D, int SW>
+__device__ __forceinline__ void tr_offsets(int lane, uint32_t (&vaddr)[D / 32][2]) {
   constexpr int RB = D * 2, CPR = D / 8;
   const int g16 = lane >> 4, r16 = lane & 15;
-  const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
 #pragma unroll
-  for (int t = 0; t < D / 32; ++t) {
-    const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
-    vaddr[t] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+  for (int h = 0; h < 2; ++h) {
+    const int row = 8 * (g16 >> 1) + 4 * h + (r16 >> 2);
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) {
+      const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+      vaddr[t][h] = row * RB + ((lc ^ block_swizzle<CPR, SW>(row)) * 16) + (r16 & 1) * 8;
+    }
   }
 }
 
 // Row-read offsets: 16 bytes (dims 16 ks + 8 half .. + 8) of row `row` of a
-// block stored with swizzle SW (0: key swizzle, 1: value swizzle).
+// block stored with swizzle SW.
 template <int D, int SW>
 __device__ __forceinline__ uint32_t row_offset(int row, int ks, int hb) {
   constexpr int RB = D * 2, CPR = D / 8;
-  const int sw = SW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row);
-  return row * RB + (((2 * ks + hb) ^ sw) * 16);
+  return row * RB + (((2 * ks + hb) ^ block_swizzle<CPR, SW>(row)) * 16);
 }
 
 // Query-major kernels: MODE 0 = forward, 1 = dq.
@@ -630,7 +641,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   constexpr int CPR = D / 8;
   constexpr int BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
-  constexpr int KSW = MODE == 0 ? 0 : 1;   // dq also reads keys transposed
+  constexpr int KSW = MODE == 0 ? 0 : 2;   // dq also reads keys transposed
   constexpr int VSW = MODE == 0 ? 1 : 0;   // forward reads values transposed
   static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
   __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
@@ -704,8 +715,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   for (int i = 0; i < DPW; ++i) {
     const int c = (i * kWaves + wave) * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
-    koff[i] = row * RB + (pc ^ (KSW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row))) * 16;
-    voff[i] = row * RB + (pc ^ (VSW == 0 ? k_swizzle<CPR>(row) : v_swizzle<CPR>(row))) * 16;
+    koff[i] = row * RB + (pc ^ block_swizzle<CPR, KSW>(row)) * 16;
+    voff[i] = row * RB + (pc ^ block_swizzle<CPR, VSW>(row)) * 16;
   }
   const char *kst = static_cast<const char *>(p.ks) + int64_t(u) * p.n * RB;
   const char *vst = static_cast<const char *>(p.vs) + int64_t(u) * p.n * RB;
@@ -725,8 +736,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
     kaddr[ks] = row_offset<D, KSW>(krow, ks, hb);
     if constexpr (MODE == 1) vrow[ks] = row_offset<D, VSW>(krow, ks, hb);
   }
-  uint32_t traddr[NTL];
-  tr_offsets<D>(lane, traddr);
+  uint32_t traddr[NTL][2];
+  tr_offsets<D, MODE == 0 ? VSW : KSW>(lane, traddr);
 
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
@@ -901,7 +912,7 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
     const int c = (i * kWaves + wave) * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     loff[i] = row;
-    qoff[i] = (pc ^ v_swizzle<CPR>(row)) * 16;
+    qoff[i] = (pc ^ dual_swizzle<CPR>(row)) * 16;
   }
   // Statistics of rows 8 wave .. 8 wave + 7 of a block: lanes 0, 1 move their
   // L (32 bytes), lanes 2, 3 their D ([U][n][G] is row-contiguous and padded
@@ -923,9 +934,9 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
   const int qrow = score_slot(col);
   uint32_t raddr[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) raddr[ks] = row_offset<D, 1>(qrow, ks, hb);
-  uint32_t traddr[NTL];
-  tr_offsets<D>(lane, traddr);
+  for (int ks = 0; ks < KS; ++ks) raddr[ks] = row_offset<D, 2>(qrow, ks, hb);
+  uint32_t traddr[NTL][2];
+  tr_offsets<D, 2>(lane, traddr);
 
   f32x16_t dk[NTL], dv[NTL];
 #pragma unroll
