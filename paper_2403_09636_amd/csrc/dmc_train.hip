@@ -60,6 +60,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+
 // log(1 - sigmoid(x)) = -softplus(x), without cancellation.
 __device__ __forceinline__ float log_one_minus_sigmoid(float x) {
   return -(fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x))));
@@ -855,9 +856,13 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
 
 // State-major kernel: dK~, dV~ and the mask gradient of 128 states per
 // workgroup (32 per wave); query rows (token-major, G per token) stream
-// through LDS in blocks of 32 rows.
-template <int D, int G>
-__global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams p, int ntiles) {
+// through LDS in blocks of 32 rows.  PART 1 computes dV~ (S, P), PART 2 dK~
+// and the mask gradient (S, dP, dS): each holds half the accumulators of a
+// combined kernel and runs at least two waves per SIMD (measured slightly
+// faster than the combined kernel at one wave per SIMD).
+template <int D, int G, int PART>
+__global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams p, int ntiles) {
+  static_assert(PART == 1 || PART == 2, "dV part or dK part");
   constexpr int kSt = 3;
   constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
@@ -890,7 +895,8 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       kop[ks] = sv_ok ? ld16(static_cast<const char *>(p.ks) + so + ks * 32 + hb * 16) : zero4;
-      vop[ks] = sv_ok ? ld16(static_cast<const char *>(p.vs) + so + ks * 32 + hb * 16) : zero4;
+      vop[ks] = (sv_ok && PART != 1) ? ld16(static_cast<const char *>(p.vs) + so + ks * 32 + hb * 16)
+                                     : zero4;
     }
     if (hb == 0) kop[0].x &= 0xffff0000u;
     // the mask entry as the forward used it: bf16 of mask * sqrt(d), back to log2 units
@@ -958,28 +964,33 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(qd + raddr[ks]), kop[ks], sc);
-      dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
+      if constexpr (PART != 1)
+        dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
     }
     // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
     // 8 hb + q (pi-permuted rows), from the block's LDS statistics area
     // ([4][8 L, 8 D] floats).
     const float *sd = reinterpret_cast<const float *>(qd + 2 * BLK);
-    float Lr[16], Dr[16];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const float *e8 = sd + (2 * kk + hb) * 16;
-      const float4 l0 = *reinterpret_cast<const float4 *>(e8);
-      const float4 l1 = *reinterpret_cast<const float4 *>(e8 + 4);
-      const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 8);
-      const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 12);
-      Lr[8 * kk + 0] = l0.x; Lr[8 * kk + 1] = l0.y; Lr[8 * kk + 2] = l0.z; Lr[8 * kk + 3] = l0.w;
-      Lr[8 * kk + 4] = l1.x; Lr[8 * kk + 5] = l1.y; Lr[8 * kk + 6] = l1.z; Lr[8 * kk + 7] = l1.w;
-      Dr[8 * kk + 0] = d0.x; Dr[8 * kk + 1] = d0.y; Dr[8 * kk + 2] = d0.z; Dr[8 * kk + 3] = d0.w;
-      Dr[8 * kk + 4] = d1.x; Dr[8 * kk + 5] = d1.y; Dr[8 * kk + 6] = d1.z; Dr[8 * kk + 7] = d1.w;
-    }
     uint4 pa[2], da[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
+      float Lr[16], Dr[16];   // indexed by register 8 kk + q: only this kk's half is loaded
+      {
+        const float *e8 = sd + (2 * kk + hb) * 16;
+        const float4 l0 = *reinterpret_cast<const float4 *>(e8);
+        const float4 l1 = *reinterpret_cast<const float4 *>(e8 + 4);
+        Lr[8 * kk + 0] = l0.x; Lr[8 * kk + 1] = l0.y; Lr[8 * kk + 2] = l0.z; Lr[8 * kk + 3] = l0.w;
+        Lr[8 * kk + 4] = l1.x; Lr[8 * kk + 5] = l1.y; Lr[8 * kk + 6] = l1.z; Lr[8 * kk + 7] = l1.w;
+        if constexpr (PART != 1) {
+          const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 8);
+          const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 12);
+          Dr[8 * kk + 0] = d0.x; Dr[8 * kk + 1] = d0.y; Dr[8 * kk + 2] = d0.z; Dr[8 * kk + 3] = d0.w;
+          Dr[8 * kk + 4] = d1.x; Dr[8 * kk + 5] = d1.y; Dr[8 * kk + 6] = d1.z; Dr[8 * kk + 7] = d1.w;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) Dr[8 * kk + q] = 0.0f;
+        }
+      }
       uint32_t wp[4], wd[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -1005,8 +1016,8 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
     for (int i = 0; i < NTL; ++i)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        dv[i] = mfma_32x32x16(pa[kk], tr_operand<RB>(dd, traddr[i], kk), dv[i]);
-        dk[i] = mfma_32x32x16(da[kk], tr_operand<RB>(qd, traddr[i], kk), dk[i]);
+        if constexpr (PART != 2) dv[i] = mfma_32x32x16(pa[kk], tr_operand<RB>(dd, traddr[i], kk), dv[i]);
+        if constexpr (PART != 1) dk[i] = mfma_32x32x16(da[kk], tr_operand<RB>(qd, traddr[i], kk), dk[i]);
       }
   };
 
@@ -1019,8 +1030,10 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
 
   // Outputs: C[state][dim] -- lane holds dim 32 i + col of states
   // s0 + 8 (j / 4) + 4 hb + j % 4.
-  dm += __shfl_xor(dm, 32, 64);
-  if (hb == 0 && sv_ok) p.dmask[int64_t(u) * p.n + js] = dm;
+  if constexpr (PART != 1) {
+    dm += __shfl_xor(dm, 32, 64);
+    if (hb == 0 && sv_ok) p.dmask[int64_t(u) * p.n + js] = dm;
+  }
   const float sc_k = sl2 / kLog2e;
 #pragma unroll
   for (int i = 0; i < NTL; ++i)
@@ -1030,8 +1043,8 @@ __global__ __launch_bounds__(kThreads, 1) void train_dkv_mfma_kernel(TrainParams
       if (st >= p.n) continue;
       const int dim = 32 * i + col;
       const int64_t o = (int64_t(u) * p.n + st) * D + dim;
-      p.dks[o] = dim == 0 ? 0.0f : dk[i][j] * sc_k;
-      p.dvs[o] = dv[i][j];
+      if constexpr (PART != 1) p.dks[o] = dim == 0 ? 0.0f : dk[i][j] * sc_k;
+      if constexpr (PART != 2) p.dvs[o] = dv[i][j];
     }
 }
 
@@ -1071,7 +1084,9 @@ hipError_t train_backward_impl(const TrainParams &p, hipStream_t s) {
     hipLaunchKernelGGL((train_qmajor_kernel<D, G, 1>), dim3(8 * ((U + 7) / 8) * ntiles),
                        dim3(kThreads), 0, s, p, ntiles);
     const int stiles = (p.n + 127) / 128;
-    hipLaunchKernelGGL((train_dkv_mfma_kernel<D, G>), dim3(8 * ((U + 7) / 8) * stiles),
+    hipLaunchKernelGGL((train_dkv_mfma_kernel<D, G, 1>), dim3(8 * ((U + 7) / 8) * stiles),
+                       dim3(kThreads), 0, s, p, stiles);
+    hipLaunchKernelGGL((train_dkv_mfma_kernel<D, G, 2>), dim3(8 * ((U + 7) / 8) * stiles),
                        dim3(kThreads), 0, s, p, stiles);
   } else {
     const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
