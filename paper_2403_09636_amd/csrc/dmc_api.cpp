@@ -627,7 +627,6 @@ dmc_status train_params(const dmc_train_config *cfg, const void *q, const void *
   p->noise = noise;
   p->ks = w + L.ks;
   p->vs = w + L.vs;
-  p->x = reinterpret_cast<float *>(w + L.x);
   p->alpha = reinterpret_cast<float *>(w + L.alpha);
   p->omega = reinterpret_cast<float *>(w + L.omega);
   p->z = reinterpret_cast<float *>(w + L.z);

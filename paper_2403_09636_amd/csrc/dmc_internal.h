@@ -155,7 +155,7 @@ struct TrainParams {
   // workspace
   void *ks, *vs;             // unrolled states [U][n][d] (+ 32 zero rows), config dtype;
                              // key element 0 holds the state's mask entry * sqrt(d)
-  float *x, *alpha, *omega;  // per token [U][n]: Gumbel-sigmoid logit, alpha, omega
+  float *alpha, *omega;      // per token [U][n]
   float *z;                  // state normalisers [U][n]
   float *mask;               // [U][n]: log(1 - alpha_{j+1}) for state j < n - 1
   float *lse;                // [U][n][G]: log2-sum-exp of each query row (log2 domain)
@@ -169,7 +169,7 @@ struct TrainParams {
 
 // Workspace layout of a training configuration.
 struct TrainLayout {
-  size_t ks, vs, x, alpha, omega, z, mask, lse, dsum, dks, dvs, dmask, e, total;
+  size_t ks, vs, alpha, omega, z, mask, lse, dsum, dks, dvs, dmask, e, total;
 };
 TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int elem_bytes, int window);
 

@@ -20,8 +20,8 @@
 //
 // Vector-ALU kernels (lanes own head-dim elements, one wave per group of
 // rows) serve every dtype; bf16 attention runs on the matrix cores
-// (v_mfma_f32_32x32x16_bf16) in three kernels: forward, dq, and the state
-// gradients dK~, dV~ with the mask gradient.
+// (v_mfma_f32_32x32x16_bf16) in four kernels: forward, dq, dV~, and dK~ with
+// the mask gradient.
 #include <type_traits>
 
 #include "dmc_mfma.h"
@@ -41,7 +41,6 @@ TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int el
   // states: 32 rows of (zeroed) padding so that 32-row blocks never leave the buffer
   L.ks = take((U * N + 32) * D * elem_bytes);
   L.vs = take((U * N + 32) * D * elem_bytes);
-  L.x = take(U * N * 4);
   L.alpha = take(U * N * 4);
   L.omega = take(U * N * 4);
   L.z = take(U * N * 4);
@@ -79,8 +78,9 @@ __device__ __forceinline__ int64_t row_k(const TrainParams &p, int b, int t, int
   return ((int64_t(b) * p.n + t) * p.hkv + g) * D;
 }
 
-// Per token: Gumbel-sigmoid logit, alpha, omega; the mask entry of the
-// previous state (log(1 - alpha_t) belongs to state t - 1).
+// Per token: alpha and omega from the Gumbel-sigmoid logit and the query
+// neuron; the mask entry of the previous state (log(1 - alpha_t) belongs to
+// state t - 1).
 template <int ES, int D>
 __global__ __launch_bounds__(kThreads) void train_decide_kernel(TrainParams p) {
   const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
@@ -94,7 +94,6 @@ __global__ __launch_bounds__(kThreads) void train_decide_kernel(TrainParams p) {
   const float al = 1.0f / (1.0f + expf(-x));
   float om = 1.0f;
   if (p.omega_src == 0) om = sigmoid_floor(load_elem<ES>(p.q, row_q(p, b, t, g * G, D)));
-  p.x[i] = x;
   p.alpha[i] = al;
   p.omega[i] = om;
   if (p.alpha_out) p.alpha_out[(int64_t(b) * p.n + t) * p.hkv + g] = al;
