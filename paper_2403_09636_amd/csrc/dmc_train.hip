@@ -427,7 +427,10 @@ __global__ __launch_bounds__(kThreads) void train_dkv_kernel(TrainParams p, int 
 // time: token t feeds states j = t .. t + w - 1 with weight c_tj / z_j; its
 // key and value gradients gather those states' gradients, and e_tj = d loss /
 // d c_tj = ((k^_t - K~_j) . dK~_j + (v_t - V~_j) . dV~_j) / z_j is kept for
-// part 2.  The NT tokens share their states, which are loaded in batches.
+// part 2.  The NT tokens share their states, which are loaded in batches;
+// per state, 1 / z_j and (K~_j . dK~_j + V~_j . dV~_j) are formed once, and
+// a token's e values collect in one lane each (lane j - t) for a single
+// store.
 template <int ES, int D>
 __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
   constexpr int E = D / 64, NT = 8, kB = 4;
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
   const int W = p.window;
   for (int tg = t0; tg < t1; tg += NT) {
     const int nt = min(NT, t1 - tg);
-    float kt[NT][E], vt[NT][E], dk[NT][E], dv[NT][E], P[NT], wt[NT];
+    float kt[NT][E], vt[NT][E], dk[NT][E], dv[NT][E], P[NT], wt[NT], ereg[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
       const int t = tg + min(i, nt - 1);
@@ -450,24 +453,29 @@ __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
       if (lane == 0) kt[i][0] = 0.0f;
       wt[i] = om[t];
       P[i] = 1.0f;
+      ereg[i] = 0.0f;
 #pragma unroll
       for (int e = 0; e < E; ++e) dk[i][e] = dv[i][e] = 0.0f;
     }
     const int jl = min(tg + nt - 1 + W - 1, p.n - 1);   // last state any of them feeds
     for (int jb = tg; jb <= jl; jb += kB) {
-      float ks[kB][E], vs[kB][E], dks[kB][E], dvs[kB][E], zj[kB], aj[kB];
+      float dks[kB][E], dvs[kB][E], qs[kB], iz[kB], aj[kB];
 #pragma unroll
       for (int q = 0; q < kB; ++q) {
         const int j = min(jb + q, jl);
         const int64_t so = (int64_t(u) * p.n + j) * D + lane * E;
-        load_e<ES, E>(static_cast<const char *>(p.ks) + so * ES, ks[q]);
-        load_e<ES, E>(static_cast<const char *>(p.vs) + so * ES, vs[q]);
+        float ks[E], vs[E];
+        load_e<ES, E>(static_cast<const char *>(p.ks) + so * ES, ks);
+        load_e<ES, E>(static_cast<const char *>(p.vs) + so * ES, vs);
+        qs[q] = 0.0f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           dks[q][e] = p.dks[so + e];
           dvs[q][e] = p.dvs[so + e];
+          qs[q] = fmaf(ks[e], dks[q][e], qs[q]);   // this lane's part of K~ . dK~ + V~ . dV~
+          qs[q] = fmaf(vs[e], dvs[q][e], qs[q]);
         }
-        zj[q] = zz[j];
+        iz[q] = 1.0f / zz[j];
         aj[q] = al[j];
       }
 #pragma unroll
@@ -479,24 +487,26 @@ __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
           const int t = tg + i;
           if (i >= nt || j < t || j > t + W - 1) continue;
           if (j > t) P[i] *= aj[q];            // prod_{r = t+1 .. j} alpha_r
-          const float cz = wt[i] * P[i] / zj[q];
-          float ev = 0.0f;
+          const float cz = wt[i] * P[i] * iz[q];
+          float ev = -qs[q];
 #pragma unroll
           for (int e = 0; e < E; ++e) {
             dk[i][e] = fmaf(cz, dks[q][e], dk[i][e]);
             dv[i][e] = fmaf(cz, dvs[q][e], dv[i][e]);
-            ev = fmaf(kt[i][e] - ks[q][e], dks[q][e], ev);
-            ev = fmaf(vt[i][e] - vs[q][e], dvs[q][e], ev);
+            ev = fmaf(kt[i][e], dks[q][e], ev);
+            ev = fmaf(vt[i][e], dvs[q][e], ev);
           }
-          ev = wsum(ev) / zj[q];
-          if (lane == 0) p.e[(int64_t(u) * p.n + t) * W + (j - t)] = ev;
+          ev = wsum(ev) * iz[q];
+          if (lane == j - t) ereg[i] = ev;
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
       if (i >= nt) break;
-      const int64_t ro = row_k(p, b, tg + i, g, D) + lane * E;
+      const int t = tg + i;
+      if (lane < min(W, p.n - t)) p.e[(int64_t(u) * p.n + t) * W + lane] = ereg[i];
+      const int64_t ro = row_k(p, b, t, g, D) + lane * E;
       if (lane == 0) dk[i][0] = 0.0f;   // element 0 gets the decision gradient in part 2
       store_e<ES, E>(static_cast<char *>(p.dk) + ro * ES, dk[i]);
       store_e<ES, E>(static_cast<char *>(p.dv) + ro * ES, dv[i]);
