@@ -125,23 +125,19 @@ def profiled_traffic(workload):
     return int(kv["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(w, lens_layers, seconds):
-    """Time the float64 oracle (single thread) on a sample of units.
-
-    Each sampled (layer, kv head) unit gets a random compressed cache of its
-    real length and runs decode steps (Algorithm 1 + attention) until the
-    time budget is spent.  tokens/s = 1 / (mean unit-step time * units per
-    token), units per token = layers * kv heads.
-    """
+def _oracle_unit_steps(job):
+    """Decode unit-steps of the float64 oracle (one thread) on random (layer,
+    kv head) units with the workload's real compressed lengths, until the
+    time budget is spent.  Returns (unit-steps, seconds spent in them, units)."""
+    seed, seconds, L, H, d, G, lens_layers, prompt_len = job
     from threadpoolctl import threadpool_limits
 
     import oracle
     from workloads import decision_logits
 
-    rng = np.random.default_rng(77)
-    L, H, d, G = w.num_layers, w.num_kv_heads, w.head_dim, w.group
-    cr = w.prompt_len / np.maximum(lens_layers, 1)
-    times, n_steps, n_units = [], 0, 0
+    rng = np.random.default_rng(seed)
+    cr = prompt_len / np.maximum(lens_layers, 1)
+    spent, n_steps, n_units = 0.0, 0, 0
     with threadpool_limits(limits=1):
         t_end = time.perf_counter() + seconds
         while time.perf_counter() < t_end:
@@ -156,15 +152,67 @@ def cpu_baseline(w, lens_layers, seconds):
                 k[0] = decision_logits(rng.uniform(size=1), cr[layer, g])[0]
                 t0 = time.perf_counter()
                 u.step(q, k, v)
-                times.append(time.perf_counter() - t0)
+                spent += time.perf_counter() - t0
                 n_steps += 1
             n_units += 1
-    per_unit_step = float(np.mean(times))
-    tok_s = 1.0 / (per_unit_step * L * H)
-    return {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n_steps} unit-steps on {n_units} random (layer, kv-head) units of the "
-                      f"workload's length distribution, float64 NumPy, 1 thread; tokens/s = "
-                      f"1 / (mean unit-step time x {L} layers x {H} kv heads)"}
+    return n_steps, spent, n_units
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        return ""
+
+
+def cpu_pool(imports_torch=False):
+    """Worker processes for the oracle timing, one per host core (at most 16,
+    a GPU's share of its host).  Start them before this process touches the
+    GPU: they are fresh interpreters.  Workers that import torch (the
+    training oracle) open the GPU device as a side effect, so they are kept
+    to 15: with this process, at most 16 hold it."""
+    import multiprocessing as mp
+
+    procs = max(1, min(os.cpu_count() or 1, 15 if imports_torch else 16))
+    return mp.get_context("spawn").Pool(procs)
+
+
+def cpu_baseline(w, lens_layers, seconds, pool=None):
+    """Time the float64 oracle on a sample of units, on one thread and then in
+    one single-threaded process per host core (independent units, as the
+    paper states every head is).
+
+    tokens/s = unit-steps per second / units per token, units per token =
+    layers * kv heads.  The reported value is the all-cores figure; the
+    one-thread figure is kept beside it.
+    """
+    L, H, d, G = w.num_layers, w.num_kv_heads, w.head_dim, w.group
+    job = (77, seconds / 2, L, H, d, G, lens_layers, w.prompt_len)
+    n1, spent1, units1 = _oracle_unit_steps(job)
+    one = n1 / spent1 / (L * H)
+    own = pool is None
+    if own:
+        pool = cpu_pool()
+    procs = pool._processes
+    jobs = [(1000 + i,) + job[1:] for i in range(procs)]
+    t0 = time.perf_counter()
+    try:
+        res = pool.map(_oracle_unit_steps, jobs, chunksize=1)
+    finally:
+        if own:
+            pool.close()
+            pool.join()
+    wall = time.perf_counter() - t0
+    steps = sum(r[0] for r in res)
+    # throughput of the pool: every worker's steps over its own busy time, summed
+    rate = sum(r[0] / r[1] for r in res if r[1] > 0)
+    return {"value": rate / (L * H), "unit": "tokens/s", "cores": procs, "kind": "oracle",
+            "single_thread_value": one, "cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": f"random (layer, kv-head) units of the workload's length distribution, "
+                      f"float64 NumPy, one thread per process: {n1} unit-steps on {units1} units "
+                      f"in one process, then {steps} unit-steps in {procs} processes "
+                      f"({wall:.1f} s wall); tokens/s = unit-steps/s / ({L} layers x {H} kv heads)"}
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
@@ -241,21 +289,18 @@ def bench_prompt(args):
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline_train(w, seconds):
-    """The float64 training oracle (autograd backward), one thread, on
-    (batch row, kv head) units over the first 512 tokens of a sequence (a
-    4096-token unit alone takes minutes in the oracle): tokens/s = 512 /
-    (time per unit x kv heads).  Its cost is dominated by the per-position
-    window recurrence, linear in n; the attention part grows with n, so at
-    the full length the oracle is slower than this figure."""
+def _oracle_train_units(job):
+    """Forward + autograd backward of the float64 training oracle (one thread)
+    on (batch row, kv head) units until the time budget is spent.  Returns
+    the seconds each unit took."""
+    seed, seconds, n, d, G = job
     import torch
     from threadpoolctl import threadpool_limits
 
     import oracle.dmc_train as T
     import workloads as W
 
-    rng = np.random.default_rng(11)
-    n, d, G = min(512, w.prompt_len), w.head_dim, w.group
+    rng = np.random.default_rng(seed)
     times = []
     with threadpool_limits(limits=1):
         torch.set_num_threads(1)
@@ -270,15 +315,42 @@ def cpu_baseline_train(w, seconds):
             t0 = time.perf_counter()
             T.train_backward(q, k, v, noise, dout, None, W.TRAIN_C, W.TRAIN_TAU, W.TRAIN_WINDOW)
             times.append(time.perf_counter() - t0)
-    per_unit = float(np.mean(times))
-    return {"value": n / (per_unit * w.num_kv_heads), "unit": "tokens/s", "cores": 1,
-            "kind": "oracle",
-            "sample": f"{len(times)} units (one kv head x the first {n} tokens, forward + "
-                      f"autograd backward, float64 torch, 1 thread); tokens/s = {n} / (time per "
-                      f"unit x {w.num_kv_heads} kv heads)"}
+    return times
 
 
-def bench_train(args):
+def cpu_baseline_train(w, seconds, pool=None):
+    """The float64 training oracle (autograd backward) on (batch row, kv head)
+    units over the first 512 tokens of a sequence (a 4096-token unit alone
+    takes minutes in the oracle), first on one thread, then in one
+    single-threaded process per host core: tokens/s = units per second x 512
+    / kv heads.  Its cost is dominated by the per-position window
+    recurrence, linear in n; the attention part grows with n, so at the full
+    length the oracle is slower than this figure."""
+    n, d, G = min(512, w.prompt_len), w.head_dim, w.group
+    one = _oracle_train_units((11, seconds / 2, n, d, G))
+    one_rate = n / (float(np.mean(one)) * w.num_kv_heads)
+    own = pool is None
+    if own:
+        pool = cpu_pool(imports_torch=True)
+    procs = pool._processes
+    try:
+        res = pool.map(_oracle_train_units, [(500 + i, seconds / 2, n, d, G) for i in range(procs)],
+                       chunksize=1)
+    finally:
+        if own:
+            pool.close()
+            pool.join()
+    units_per_s = sum(len(t) / sum(t) for t in res)
+    return {"value": units_per_s * n / w.num_kv_heads, "unit": "tokens/s", "cores": procs,
+            "kind": "oracle", "single_thread_value": one_rate, "cpu_count": os.cpu_count(),
+            "cpu_model": cpu_model(),
+            "sample": f"units of one kv head x the first {n} tokens, forward + autograd "
+                      f"backward, float64 torch, one thread per process: {len(one)} units in "
+                      f"one process, then {sum(len(t) for t in res)} units in {procs} processes; "
+                      f"tokens/s = units/s x {n} / {w.num_kv_heads} kv heads"}
+
+
+def bench_train(args, pool=None):
     """Training-time DMC attention of one layer: dmc_train_forward and
     dmc_train_backward, each timed per call with HIP events on the launch
     stream (median).  Algorithmic flops per (query row, visible state): 4 d
@@ -348,7 +420,7 @@ def bench_train(args):
         "backward_TFLOPs": round(f_bwd / (t_bwd * 1e-3) / 1e12, 1),
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline_train(w, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline_train(w, args.cpu_seconds, pool)
     print(json.dumps(res), flush=True)
 
 
@@ -362,10 +434,20 @@ def main():
     if args.prompt:
         bench_prompt(args)
         return
-    if args.train:
-        bench_train(args)
-        return
+    # oracle workers are started before anything touches the GPU
+    pool = None if args.no_cpu_baseline else cpu_pool(imports_torch=args.train)
+    try:
+        if args.train:
+            bench_train(args, pool)
+        else:
+            bench_decode(args, pool)
+    finally:
+        if pool is not None:
+            pool.close()
+            pool.join()
 
+
+def bench_decode(args, pool):
     import torch
 
     import paper_2403_09636_amd as P
@@ -504,7 +586,7 @@ def main():
         res["prefill"] = {"avg_layer_ms": round(float(np.mean(prefill_ms)), 3),
                           "alg_GBps": round((rd + wr) / (np.mean(prefill_ms) * 1e-3) / 1e9, 1)}
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, lens0[:, 0, :], args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, lens0[:, 0, :], args.cpu_seconds, pool)
     print(json.dumps(res), flush=True)
     if args.calib_copy:
         # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings give

@@ -123,3 +123,14 @@ def test_bench_window_bookkeeping():
                 ref_reads += sum(min(w, e - s) for s, e in zip(starts, ends))
         assert (bench.segment_lengths_after_prompt(k0, n) == ref_sl).all()
         assert bench.windowed_prompt_reads(k0, w) == ref_reads
+
+
+def test_cpu_baseline_worker_counts_unit_steps():
+    """The oracle-timing worker runs whole units (four decode steps each) on
+    the workload's lengths and reports the time spent inside the steps."""
+    import bench
+    w = W.scaled(W.WORKLOADS["llama7b_stack"], num_layers=2, num_kv_heads=2, num_q_heads=2)
+    lens = np.full((2, 2), 40)
+    steps, spent, units = bench._oracle_unit_steps((3, 0.05, 2, 2, w.head_dim, w.group, lens,
+                                                    w.prompt_len))
+    assert units >= 1 and steps == 4 * units and spent > 0
