@@ -229,6 +229,172 @@ __device__ __forceinline__ void walk_window_state(const PromptParams &p, int u, 
 constexpr int kStages = DMC_PROMPT_STAGES;
 constexpr int kPtabLds = kPromptMaxPages;   // page-table entries of a unit cached in LDS
 
+// Open states of a wave's columns on the matrix cores (exact Algorithm 1).
+// The wave's tokens lie in one 32-token block starting at bs = a & ~31, and
+// the open state of token t is the omega-weighted mean of its segment's
+// tokens up to t: those of the block from the segment start (or from bs,
+// plus the carry record at bs, when the segment began earlier).  With
+// W[t][j] = omega_{bs+j} over that range of block rows j and 0 elsewhere:
+//   score(t) = (sum_j W[t][j] (q_t . k_{bs+j}) + q_t . carry_k) / z_t
+//   value(t) = (sum_j W[t][j] v_{bs+j} + carry_v) / z_t
+//   z_t      =  sum_j W[t][j] + carry_z
+// q_t . k_j comes from the same score product as the closed slots (raw key
+// rows as A operands, straight from global memory; q[0] is already zeroed,
+// which leaves k[0] out).  The value sum is V^T[dim][j] W^T[j][col] on the
+// matrix cores with W split into a bf16 head and tail (W = hi + lo to about
+// 2^-17), the raw value rows staged in LDS (value swizzle) for transposed
+// reads.  Results go into the online softmax state as in the vector walk:
+// max = score, weight 1 (counted in one half), accumulator = value mean.
+template <int D, int G>
+__device__ __forceinline__ void open_state_mfma(const PromptParams &p, int u, int b, int g, int a,
+                                                int nb, int col, int hb, int tok,
+                                                bool colv, const uint4 (&qop)[D / 16],
+                                                char *vstage, float &m, float &ls,
+                                                f32x16_t (&acc)[D / 32]) {
+  constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8;
+  constexpr int NDMA = 32 * RB / 1024;   // 16-byte transfers per lane for 32 value rows
+  const int lane = threadIdx.x & 63;
+  const int bs = a & ~31;
+  const int last = nb - 1;               // rows past the prompt read its last row (weight 0)
+  const uint8_t *al = p.alpha + int64_t(u) * p.max_prompt;
+  const float *om = p.omega + int64_t(u) * p.max_prompt;
+  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2]) * 2;
+  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2]) * 2;
+  const int64_t kst = p.ks[1] * 2, vst = p.vs[1] * 2;
+
+  // Raw value rows bs .. bs + 31 into this wave's staging block.
+  const uint32_t vdst = lds_offset(vstage);
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int c = i * 64 + lane;
+    const int row = c / CPR, pc = c - row * CPR;
+    const int trow = min(bs + row, last);
+    dma16(vdst + i * 1024, vbase + trow * vst + (pc ^ v_swizzle<CPR>(row)) * 16);
+  }
+  // Raw key row bs + pi(col) as this lane's A operand.
+  uint4 kop[KS];
+  {
+    const char *kr = kbase + min(bs + score_slot(col), last) * kst + hb * 16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kop[ks] = ld16(kr + ks * 32);
+  }
+  // Segment starts of the block (bit j: token bs + j opens a segment).
+  const int ta = min(bs + (lane & 31), last);
+  const uint32_t starts = static_cast<uint32_t>(__ballot(lane < 32 && bs + lane <= last && al[ta] == 0));
+  // This column's token and the first block row of its open segment.
+  const int tr = colv ? a + tok - bs : -1;
+  const uint32_t upto = tr >= 0 ? starts & (0xffffffffu >> (31 - tr)) : 0u;
+  const int first = upto ? 31 - __clz(upto) : 0;
+  const bool carried = colv && upto == 0 && bs > 0;
+  // Weights of the lane's rows j = 16 kk + 8 hb + e (register 8 kk + e of the
+  // score product holds row j, as in the closed-slot blocks).
+  float w[16];
+  float zs = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int j = 16 * (i >> 3) + 8 * hb + (i & 7);
+    const float wj = om[min(bs + j, last)];
+    w[i] = (j >= first && j <= tr) ? wj : 0.0f;
+    zs += w[i];
+  }
+
+  f32x16_t sc = f32x16_t{};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) sc = mfma_32x32x16(kop[ks], qop[ks], sc);
+  float part = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) part = fmaf(w[i], sc[i], part);
+
+  // W^T operands, head and tail.
+  uint4 whi[2], wlo[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float w0 = w[8 * kk + 2 * q], w1 = w[8 * kk + 2 * q + 1];
+      h[q] = cvt_pk_bf16(w0, w1);
+      const float h0 = __uint_as_float(h[q] << 16), h1 = __uint_as_float(h[q] & 0xffff0000u);
+      l[q] = cvt_pk_bf16(w0 - h0, w1 - h1);
+    }
+    whi[kk] = make_uint4(h[0], h[1], h[2], h[3]);
+    wlo[kk] = make_uint4(l[0], l[1], l[2], l[3]);
+  }
+
+  // Carry record of the block when some column's segment began before bs.
+  float cz = 0.0f;
+  f32x16_t cv[NTL];
+#pragma unroll
+  for (int t = 0; t < NTL; ++t) cv[t] = f32x16_t{};
+  if (__any(carried)) {
+    const float *cr = p.carry + (int64_t(u) * p.carry_blocks + (bs >> 5)) * carry_stride(D);
+    if (carried) {
+      float qk = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        float qf[8];
+        V16<2>::unpack(qop[ks], qf);
+        const float4 k0 = *reinterpret_cast<const float4 *>(cr + 16 * ks + 8 * hb);
+        const float4 k1 = *reinterpret_cast<const float4 *>(cr + 16 * ks + 8 * hb + 4);
+        qk = fmaf(qf[0], k0.x, qk);
+        qk = fmaf(qf[1], k0.y, qk);
+        qk = fmaf(qf[2], k0.z, qk);
+        qk = fmaf(qf[3], k0.w, qk);
+        qk = fmaf(qf[4], k1.x, qk);
+        qk = fmaf(qf[5], k1.y, qk);
+        qk = fmaf(qf[6], k1.z, qk);
+        qk = fmaf(qf[7], k1.w, qk);
+      }
+      part += qk;
+#pragma unroll
+      for (int t = 0; t < NTL; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 x = *reinterpret_cast<const float4 *>(cr + D + 32 * t + 8 * i + 4 * hb);
+          cv[t][4 * i + 0] = x.x;
+          cv[t][4 * i + 1] = x.y;
+          cv[t][4 * i + 2] = x.z;
+          cv[t][4 * i + 3] = x.w;
+        }
+      cz = cr[2 * D];
+    }
+  }
+  part += __shfl_xor(part, 32, 64);
+  zs += __shfl_xor(zs, 32, 64) + cz;
+
+  // Value sums: A = V^T[dim 32 t + col][rows 16 kk + 8 hb .. + 8] (transposed reads).
+  wait_vmcnt<0>();
+  wave_lds_sync();
+  uint32_t vaddr[NTL];
+  {
+    const int g16 = lane >> 4, r16 = lane & 15;
+    const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
+#pragma unroll
+    for (int t = 0; t < NTL; ++t) {
+      const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+      vaddr[t] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NTL; ++t) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const uint2 h0 = ds_read_tr16(vstage + vaddr[t] + 16 * kk * RB);
+      const uint2 h1 = ds_read_tr16(vstage + vaddr[t] + (16 * kk + 4) * RB);
+      const uint4 va = make_uint4(h0.x, h0.y, h1.x, h1.y);
+      cv[t] = mfma_32x32x16(va, whi[kk], cv[t]);
+      cv[t] = mfma_32x32x16(va, wlo[kk], cv[t]);
+    }
+  }
+  if (colv) {
+    const float inv = 1.0f / zs;
+    m = part * inv * p.scale_log2;
+    ls = hb == 0 ? 1.0f : 0.0f;   // the open state's weight, counted once per column
+#pragma unroll
+    for (int t = 0; t < NTL; ++t) acc[t] = cv[t] * inv;
+  }
+}
+
 template <int D, int G, bool VT>
 __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p, int ntiles) {
   constexpr int T = 32 / G;            // tokens per wave
@@ -288,11 +454,15 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
 #pragma unroll
   for (int t = 0; t < NTL; ++t) acc[t] = f32x16_t{};
 
-  // Open state of each column's token.  The walk stages key and value means
-  // of 8 tokens at a time (fp32, this wave's part of the block ring); then
-  // every lane takes its column's score (dot with its Q^T slice, summed over
-  // the two halves) and its slice of the value mean.
-  if (cnt > 0) {
+  // Open state of each column's token.
+  if (cnt > 0 && p.window == 0) {
+    open_state_mfma<D, G>(p, u, b, g, a, nb, col, hb, tok, colv, qop,
+                          reinterpret_cast<char *>(smem) + wave * BLK, m, ls, acc);
+  } else if (cnt > 0) {
+    // Window grouping: the walk stages key and value means of 8 tokens at a
+    // time (fp32, this wave's part of the block ring); then every lane takes
+    // its column's score (dot with its Q^T slice, summed over the two halves)
+    // and its slice of the value mean.
     float *stage = reinterpret_cast<float *>(smem) + wave * STAGE;
     constexpr int E = D / 64;
     auto snap = [&](int t, const float *ak, const float *av, float zs) {
@@ -346,10 +516,7 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
           }
           wave_lds_sync();
         };
-    if (p.window > 0)
-      walk_window_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
-    else
-      walk_open_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
+    walk_window_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
   }
   __syncthreads();   // slot limits published; staging area free again
 
