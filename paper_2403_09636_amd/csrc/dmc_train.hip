@@ -183,6 +183,141 @@ __global__ __launch_bounds__(64) void train_states_kernel(TrainParams p) {
   }
 }
 
+// Unrolled states on the matrix cores (bf16), one wave per (unit, 32
+// positions j0 .. j0 + 31).  The wave stages the raw key and value rows of
+// tokens tb = j0 - 16 (NK - 2) .. j0 + 31 in LDS (direct transfers, value
+// swizzle) and forms, per position (lane column), the closed-form weights
+// c_tj = omega_t prod_{r=t+1..j} alpha_r of its window in registers, walking
+// the tokens downwards from j exactly as the vector kernel does (so z_j is
+// the same fp32 sum).  Then, per 32-dim tile,
+//   S^T[dim][j] = sum_t K^T[dim][t] C^T[t][j]   (A: transposed LDS reads,
+//                                                B: the lane's weights)
+// with each weight split into a bf16 head and tail (c = hi + lo to about
+// 2^-17 relative), and the same for the values.  NK 16-token k-steps cover
+// the 31 + w tokens that the 32 positions need.
+template <int D, int NK>
+__global__ __launch_bounds__(64) void train_states_mfma_kernel(TrainParams p) {
+  constexpr int RB = D * 2, CPR = D / 8, NTL = D / 32, ROWS = 16 * NK;
+  constexpr int NDMA = ROWS * CPR / 64;   // 16-byte transfers per lane and matrix
+  static_assert(ROWS * CPR % 64 == 0, "row staging split");
+  __shared__ __align__(16) unsigned char smem[2 * ROWS * RB];
+  const int u = blockIdx.y, lane = threadIdx.x;
+  const int col = lane & 31, hb = lane >> 5;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int j0 = blockIdx.x * 32;
+  const int tb = j0 - 16 * (NK - 2);
+  const int W = p.window, last = p.n - 1;
+
+  // Raw rows of tokens tb .. tb + ROWS - 1 (clamped into the sequence; the
+  // rows outside it get weight 0).
+  const char *kb = static_cast<const char *>(p.k) + row_k(p, b, 0, g, D) * 2;
+  const char *vb = static_cast<const char *>(p.v) + row_k(p, b, 0, g, D) * 2;
+  const int64_t rs = int64_t(p.hkv) * D * 2;
+  const uint32_t kst = lds_offset(smem), vst = kst + ROWS * RB;
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int c = i * 64 + lane;
+    const int row = c / CPR, pc = c - row * CPR;
+    const int64_t src = min(max(tb + row, 0), last) * rs + (pc ^ v_swizzle<CPR>(row)) * 16;
+    dma16(kst + i * 1024, kb + src);
+    dma16(vst + i * 1024, vb + src);
+  }
+
+  // Weights of position j for staged rows 0 .. ROWS - 1, from the top down.
+  const float *al = p.alpha + int64_t(u) * p.n;
+  const float *om = p.omega + int64_t(u) * p.n;
+  const int j = j0 + col;
+  float cw[ROWS];
+  float zs = 0.0f, P = 1.0f;
+#pragma unroll
+  for (int r = ROWS - 1; r >= 0; --r) {
+    const int t = tb + r;
+    const int tc = min(max(t, 0), last);
+    const float a = al[tc], o = om[tc];
+    const bool in = t <= j && t > j - W && t >= 0;
+    const float c = in ? o * P : 0.0f;
+    cw[r] = c;
+    zs += c;
+    if (in) P *= a;
+  }
+  // This lane's half (rows 16 ks + 8 hb + e) as packed bf16 head and tail.
+  uint4 whi[NK], wlo[NK];
+#pragma unroll
+  for (int ks = 0; ks < NK; ++ks) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float w0 = hb ? cw[16 * ks + 8 + 2 * q] : cw[16 * ks + 2 * q];
+      const float w1 = hb ? cw[16 * ks + 9 + 2 * q] : cw[16 * ks + 1 + 2 * q];
+      h[q] = cvt_pk_bf16(w0, w1);
+      l[q] = cvt_pk_bf16(w0 - __uint_as_float(h[q] << 16), w1 - __uint_as_float(h[q] & 0xffff0000u));
+    }
+    whi[ks] = make_uint4(h[0], h[1], h[2], h[3]);
+    wlo[ks] = make_uint4(l[0], l[1], l[2], l[3]);
+  }
+
+  uint32_t vaddr[NTL];
+  {
+    const int g16 = lane >> 4, r16 = lane & 15;
+    const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
+#pragma unroll
+    for (int t = 0; t < NTL; ++t) {
+      const int lc = 4 * t + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+      vaddr[t] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+    }
+  }
+  wait_vmcnt<0>();
+  wave_lds_sync();
+
+  const float inv = 1.0f / zs;
+  const float sqrt_d = kLog2e / p.scale_log2;
+  if (j < p.n && hb == 0) p.z[int64_t(u) * p.n + j] = zs;
+  const float mask_j = j < p.n ? p.mask[int64_t(u) * p.n + j] * sqrt_d : 0.0f;
+  const int nrow = min(32, p.n - j0);   // positions of this block inside the sequence
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    char *buf = reinterpret_cast<char *>(smem) + m * ROWS * RB;
+    f32x16_t acc[NTL];
+#pragma unroll
+    for (int t = 0; t < NTL; ++t) {
+      acc[t] = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < NK; ++ks) {
+        const uint2 h0 = ds_read_tr16(buf + vaddr[t] + 16 * ks * RB);
+        const uint2 h1 = ds_read_tr16(buf + vaddr[t] + (16 * ks + 4) * RB);
+        const uint4 a = make_uint4(h0.x, h0.y, h1.x, h1.y);
+        acc[t] = mfma_32x32x16(a, whi[ks], acc[t]);
+        acc[t] = mfma_32x32x16(a, wlo[ks], acc[t]);
+      }
+    }
+    // The 32 state rows back into this matrix's staging rows 0 .. 31 (its
+    // inputs are consumed), 16-byte chunks XOR-swizzled by row; lane holds
+    // dims 32 t + 8 i + 4 hb .. + 4 of position j0 + col.
+#pragma unroll
+    for (int t = 0; t < NTL; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float x0 = acc[t][4 * i] * inv;
+        if (m == 0 && t == 0 && i == 0 && hb == 0) x0 = mask_j;   // the mask carrier
+        const uint32_t lo = cvt_pk_bf16(x0, acc[t][4 * i + 1] * inv);
+        const uint32_t hi = cvt_pk_bf16(acc[t][4 * i + 2] * inv, acc[t][4 * i + 3] * inv);
+        *reinterpret_cast<uint2 *>(buf + col * RB + (((4 * t + i) ^ k_swizzle<CPR>(col)) * 16) + hb * 8) =
+            make_uint2(lo, hi);
+      }
+    wave_lds_sync();
+    // Whole rows out: 64 / CPR rows per pass, 16 bytes per lane.
+    char *dst = static_cast<char *>(m == 0 ? p.ks : p.vs) + (int64_t(u) * p.n + j0) * RB;
+    constexpr int RPP = 64 / CPR;
+#pragma unroll
+    for (int r0 = 0; r0 < 32; r0 += RPP) {
+      const int row = r0 + lane / CPR, ch = lane % CPR;
+      if (row < nrow)
+        *reinterpret_cast<uint4 *>(dst + row * RB + ch * 16) =
+            *reinterpret_cast<const uint4 *>(buf + row * RB + ((ch ^ k_swizzle<CPR>(row)) * 16));
+    }
+  }
+}
+
 // Rows handled by one wave of the attention kernels: TG tokens x G heads.
 template <int G>
 struct Rows {
@@ -1070,13 +1205,21 @@ hipError_t train_forward_impl(const TrainParams &p, hipStream_t s) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((train_decide_kernel<ES, D>), dim3(blocks_for(int64_t(U) * p.n)), dim3(kThreads),
                      0, s, p);
-  hipLaunchKernelGGL((train_states_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
   if constexpr (ES == 2) {
+    const dim3 grid((p.n + 31) / 32, U);
+    switch (2 + (p.window + 14) / 16) {   // 16-token k-steps for 31 + w tokens
+      case 2: hipLaunchKernelGGL((train_states_mfma_kernel<D, 2>), grid, dim3(64), 0, s, p); break;
+      case 3: hipLaunchKernelGGL((train_states_mfma_kernel<D, 3>), grid, dim3(64), 0, s, p); break;
+      case 4: hipLaunchKernelGGL((train_states_mfma_kernel<D, 4>), grid, dim3(64), 0, s, p); break;
+      case 5: hipLaunchKernelGGL((train_states_mfma_kernel<D, 5>), grid, dim3(64), 0, s, p); break;
+      default: hipLaunchKernelGGL((train_states_mfma_kernel<D, 6>), grid, dim3(64), 0, s, p); break;
+    }
     constexpr int TW = kWaves * (32 / G);
     const int ntiles = (p.n + TW - 1) / TW;
     hipLaunchKernelGGL((train_qmajor_kernel<D, G, 0>), dim3(8 * ((U + 7) / 8) * ntiles),
                        dim3(kThreads), 0, s, p, ntiles);
   } else {
+    hipLaunchKernelGGL((train_states_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
     const int ngroups = (p.n + Rows<G>::TG - 1) / Rows<G>::TG;
     hipLaunchKernelGGL((train_fwd_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * ngroups * 64)),
                        dim3(kThreads), 0, s, p, ngroups);

@@ -57,6 +57,11 @@ CASES = [
     ("bf16", 128, 1, 1, 2, 300, 12, 5.0, 0.1, [1.0, 8.0], "lead", True),
     ("bf16", 64, 4, 1, 2, 201, 12, 5.0, 0.1, [2.0, 4.0], "uniform", False),
     ("bf16", 128, 2, 2, 1, 161, 64, 5.0, 0.2, [16.0], "lead", True),
+    # every width class of the matrix-core states pass (w = 1, 17, 18, 40)
+    ("bf16", 64, 1, 1, 2, 90, 1, 5.0, 0.1, [3.0, 1.0], "lead", True),
+    ("bf16", 128, 1, 1, 1, 70, 17, 3.0, 0.2, [6.0], "lead", False),
+    ("bf16", 128, 4, 1, 2, 120, 18, 5.0, 0.1, [8.0, 2.0], "uniform", True),
+    ("bf16", 64, 1, 1, 1, 150, 40, 5.0, 0.3, [30.0], "lead", True),
 ]
 
 
