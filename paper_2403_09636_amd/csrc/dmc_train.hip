@@ -1104,6 +1104,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     if (rb + 31 < s0 * G) return;                    // every row precedes this wave's states
     const char *qd = reinterpret_cast<const char *>(smem) + ST * SLOT;
     const char *dd = qd + BLK;
+    const bool interior = rb / G > s0 + 31 && rb + 32 <= nrows && s0 + 32 <= p.n;
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -1136,22 +1137,38 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
         }
       }
       uint32_t wp[4], wd[4];
+      if (interior) {   // every row's token is past every state of the wave
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float pv[2], dsv[2];
+        for (int q = 0; q < 4; ++q) {
+          float pv[2], dsv[2];
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int i = 8 * kk + 2 * q + e;
-          const int rg = rb + 16 * kk + 8 * hb + 2 * q + e;
-          const int tq = rg / G;
-          const bool vis = sv_ok && rg < nrows && tq >= js;
-          const float x = sc[i] * sl2 + (tq > js ? bias : 0.0f);
-          pv[e] = vis ? fast_exp2(x - Lr[i]) : 0.0f;
-          dsv[e] = vis ? pv[e] * (dp[i] - Dr[i]) : 0.0f;   // statistics past the rows are not read
-          if (vis && tq > js) dm += dsv[e];
+          for (int e = 0; e < 2; ++e) {
+            const int i = 8 * kk + 2 * q + e;
+            pv[e] = fast_exp2(fmaf(sc[i], sl2, bias - Lr[i]));
+            dsv[e] = pv[e] * (dp[i] - Dr[i]);
+            dm += dsv[e];
+          }
+          wp[q] = cvt_pk_bf16(pv[0], pv[1]);
+          wd[q] = cvt_pk_bf16(dsv[0], dsv[1]);
         }
-        wp[q] = cvt_pk_bf16(pv[0], pv[1]);
-        wd[q] = cvt_pk_bf16(dsv[0], dsv[1]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float pv[2], dsv[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int i = 8 * kk + 2 * q + e;
+            const int rg = rb + 16 * kk + 8 * hb + 2 * q + e;
+            const int tq = rg / G;
+            const bool vis = sv_ok && rg < nrows && tq >= js;
+            const float x = sc[i] * sl2 + (tq > js ? bias : 0.0f);
+            pv[e] = vis ? fast_exp2(x - Lr[i]) : 0.0f;
+            dsv[e] = vis ? pv[e] * (dp[i] - Dr[i]) : 0.0f;   // statistics past the rows are not read
+            if (vis && tq > js) dm += dsv[e];
+          }
+          wp[q] = cvt_pk_bf16(pv[0], pv[1]);
+          wd[q] = cvt_pk_bf16(dsv[0], dsv[1]);
+        }
       }
       pa[kk] = make_uint4(wp[0], wp[1], wp[2], wp[3]);
       da[kk] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
