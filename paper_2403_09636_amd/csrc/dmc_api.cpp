@@ -636,6 +636,7 @@ dmc_status train_params(const dmc_train_config *cfg, const void *q, const void *
   p->dks = reinterpret_cast<float *>(w + L.dks);
   p->dvs = reinterpret_cast<float *>(w + L.dvs);
   p->dmask = reinterpret_cast<float *>(w + L.dmask);
+  p->qs = reinterpret_cast<float *>(w + L.qs);
   p->e = reinterpret_cast<float *>(w + L.e);
   p->c = cfg->decision_bias;
   p->tau = cfg->temperature;

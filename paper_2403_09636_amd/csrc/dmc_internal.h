@@ -160,8 +160,11 @@ struct TrainParams {
   float *mask;               // [U][n]: log(1 - alpha_{j+1}) for state j < n - 1
   float *lse;                // [U][n][G]: log2-sum-exp of each query row (log2 domain)
   float *dsum;               // [U][n][G]: sum(dout * out) of each query row
-  float *dks, *dvs;          // [U][n][d] fp32: gradients of the states
+  float *dks, *dvs;          // gradients of the states: [U][n][d] fp32 (vector passes) or,
+                             // in the same bytes, bf16 head and tail planes [2][U][n][d]
+                             // (matrix-core passes)
   float *dmask;              // [U][n]
+  float *qs;                 // [U][n]: K~_j . dK~_j + V~_j . dV~_j (matrix-core passes)
   float *e;                  // [U][n][w]: d loss / d weight of token t in state t + i
   float c, tau, scale_log2;
   int32_t batch, n, hq, hkv, window, omega_src;
@@ -169,7 +172,7 @@ struct TrainParams {
 
 // Workspace layout of a training configuration.
 struct TrainLayout {
-  size_t ks, vs, alpha, omega, z, mask, lse, dsum, dks, dvs, dmask, e, total;
+  size_t ks, vs, alpha, omega, z, mask, lse, dsum, dks, dvs, dmask, qs, e, total;
 };
 TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int elem_bytes, int window);
 

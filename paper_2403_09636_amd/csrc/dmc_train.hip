@@ -50,6 +50,7 @@ TrainLayout train_layout(int batch, int n, int hq, int hkv, int head_dim, int el
   L.dks = take(U * N * D * 4);
   L.dvs = take(U * N * D * 4);
   L.dmask = take(U * N * 4);
+  L.qs = take(U * N * 4);
   L.e = take(U * N * size_t(window) * 4);
   L.total = off;
   return L;
@@ -649,6 +650,215 @@ __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
   }
 }
 
+// States -> tokens, part 1, on the matrix cores (bf16): one wave per (unit,
+// 32 tokens t0 .. t0 + 31), which feed states t0 .. t0 + 30 + w (staged
+// rows r = j - t0, NK 16-row k-steps).  Per matrix (keys, then values) the
+// states' gradients, which the matrix-core state-gradient pass leaves as
+// bf16 head and tail planes (dX~ = hi + lo to about 2^-17), are copied into
+// LDS by direct transfers (value swizzle), and
+//   E[t][j]  += X^_t . dX~_j      (A: token rows from global memory)
+//   dX^T[dim][t] = sum_j dX~^T[dim][j] C^T[j][t],  C[t][j] = c_tj / z_j
+// (A: transposed plane reads; B: the lane's weights, formed as in the vector
+// pass, split into head and tail; hi.hi + hi.lo + lo.hi).  Then e_tj =
+// (E[t][j] - K~_j . dK~_j - V~_j . dV~_j) / z_j over the window, the dot
+// products left per state by the state-gradient pass.  The token gradients go out as
+// whole rows through LDS.
+template <int D, int NK>
+__global__ __launch_bounds__(64, 2) void train_tokens_mfma_kernel(TrainParams p) {
+  constexpr int RB = D * 2, CPR = D / 8, NTL = D / 32, KS = D / 16, ROWS = 16 * NK;
+  constexpr int NCT = (ROWS + 31) / 32;   // 32-state column tiles of E and Q
+  constexpr int PLANE = ROWS * RB;
+  constexpr int NAL = (ROWS + 63) / 64;
+  __shared__ __align__(16) unsigned char smem[2 * PLANE];
+  __shared__ __align__(16) float s_al[ROWS], s_iz[ROWS];
+  const int u = blockIdx.y, lane = threadIdx.x;
+  const int col = lane & 31, hb = lane >> 5;
+  const int b = u / p.hkv, g = u - b * p.hkv;
+  const int t0 = blockIdx.x * 32;
+  const int W = p.window, last = p.n - 1;
+  const int64_t un = int64_t(u) * p.n;
+  const int64_t plane_bytes = int64_t(p.batch) * p.hkv * p.n * RB;
+
+  // What a phase reads from global memory, issued at once after the
+  // weights are formed: the states' gradient planes (direct to LDS) and the
+  // token rows (A of E).
+  uint4 xa[KS];
+  auto issue = [&](int m) {
+    const char *hp = reinterpret_cast<const char *>(m == 0 ? p.dks : p.dvs);
+    const uint32_t dst = lds_offset(smem);
+#pragma unroll
+    for (int i = 0; i < ROWS * CPR / 64; ++i) {
+      const int c = i * 64 + lane;
+      const int row = c / CPR, pc = c - row * CPR;
+      const int64_t src = (un + min(t0 + row, last)) * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
+      dma16(dst + i * 1024, hp + src);
+      dma16(dst + PLANE + i * 1024, hp + plane_bytes + src);
+    }
+    const char *xr = static_cast<const char *>(m == 0 ? p.k : p.v) +
+                     row_k(p, b, min(t0 + col, last), g, D) * 2 + hb * 16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) xa[ks] = ld16(xr + ks * 32);
+  };
+
+  // alpha_j and 1 / z_j of the staged states (through LDS, read as float4),
+  // omega of this lane's token, 1 / z and X~ . dX~ of its E columns.
+  float alv[NAL], zv[NAL], izc[NCT], qsc[NCT];
+#pragma unroll
+  for (int k = 0; k < NAL; ++k) {
+    const int j = min(t0 + 64 * k + lane, last);
+    alv[k] = p.alpha[un + j];
+    zv[k] = p.z[un + j];
+  }
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    izc[c] = p.z[un + min(t0 + 32 * c + col, last)];
+    qsc[c] = p.qs[un + min(t0 + 32 * c + col, last)];
+  }
+  const int t = t0 + col;
+  const float wt = p.omega[un + min(t, last)];
+#pragma unroll
+  for (int k = 0; k < NAL; ++k)
+    if (64 * k + lane < ROWS) {
+      s_al[64 * k + lane] = alv[k];
+      s_iz[64 * k + lane] = 1.0f / zv[k];
+    }
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) izc[c] = 1.0f / izc[c];
+  wave_lds_sync();
+
+  // Weights C[t][t0 + r] of this lane's token, ascending in j as in the
+  // vector pass: (omega_t prod_{r=t+1..j} alpha_r) / z_j.
+  uint4 chi[NK], clo[NK];
+  {
+    float cw[ROWS];
+    float P = 1.0f;
+#pragma unroll
+    for (int r4 = 0; r4 < ROWS; r4 += 4) {
+      const float4 a4 = *reinterpret_cast<const float4 *>(s_al + r4);
+      const float4 z4 = *reinterpret_cast<const float4 *>(s_iz + r4);
+      const float av[4] = {a4.x, a4.y, a4.z, a4.w}, iv[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = t0 + r4 + q;
+        const bool in = j >= t && j < t + W && j <= last;
+        if (in && j > t) P *= av[q];
+        cw[r4 + q] = in ? wt * P * iv[q] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) {
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float w0 = hb ? cw[16 * ks + 8 + 2 * q] : cw[16 * ks + 2 * q];
+        const float w1 = hb ? cw[16 * ks + 9 + 2 * q] : cw[16 * ks + 1 + 2 * q];
+        h[q] = cvt_pk_bf16(w0, w1);
+        l[q] = cvt_pk_bf16(w0 - __uint_as_float(h[q] << 16), w1 - __uint_as_float(h[q] & 0xffff0000u));
+      }
+      chi[ks] = make_uint4(h[0], h[1], h[2], h[3]);
+      clo[ks] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+  }
+
+  uint32_t vaddr[NTL];
+  {
+    const int g16 = lane >> 4, r16 = lane & 15;
+    const int row0 = 8 * (g16 >> 1) + (r16 >> 2);
+#pragma unroll
+    for (int i = 0; i < NTL; ++i) {
+      const int lc = 4 * i + 2 * (g16 & 1) + ((r16 & 3) >> 1);
+      vaddr[i] = row0 * RB + ((lc ^ v_swizzle<CPR>(row0)) * 16) + (r16 & 1) * 8;
+    }
+  }
+
+  f32x16_t ae[NCT];
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) ae[c] = f32x16_t{};
+  const int ntok = min(32, p.n - t0);   // tokens of this block inside the sequence
+
+#pragma unroll 1
+  for (int m = 0; m < 2; ++m) {
+    issue(m);
+    wait_vmcnt<0>();
+    wave_lds_sync();
+    if (m == 0 && hb == 0) xa[0].x &= 0xffff0000u;   // k^_t: element 0 is not part of a key
+
+    // E.
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      const int srow = 32 * c + col;
+      const bool sok = srow < ROWS;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 bh = make_uint4(0, 0, 0, 0), bl = bh;
+        if (sok) {
+          const uint32_t off = srow * RB + (((2 * ks + hb) ^ v_swizzle<CPR>(srow)) * 16);
+          bh = *reinterpret_cast<const uint4 *>(smem + off);
+          bl = *reinterpret_cast<const uint4 *>(smem + PLANE + off);
+        }
+        ae[c] = mfma_32x32x16(xa[ks], bh, ae[c]);
+        ae[c] = mfma_32x32x16(xa[ks], bl, ae[c]);
+      }
+    }
+
+    // Token gradients: lane holds dims 32 i + 8 q + 4 hb .. + 4 of token t0 + col.
+    f32x16_t acc[NTL];
+#pragma unroll
+    for (int i = 0; i < NTL; ++i) {
+      acc[i] = f32x16_t{};
+#pragma unroll
+      for (int ks = 0; ks < NK; ++ks) {
+        const uint2 h0 = ds_read_tr16(smem + vaddr[i] + 16 * ks * RB);
+        const uint2 h1 = ds_read_tr16(smem + vaddr[i] + (16 * ks + 4) * RB);
+        const uint2 l0 = ds_read_tr16(smem + PLANE + vaddr[i] + 16 * ks * RB);
+        const uint2 l1 = ds_read_tr16(smem + PLANE + vaddr[i] + (16 * ks + 4) * RB);
+        const uint4 ah = make_uint4(h0.x, h0.y, h1.x, h1.y), alo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+        acc[i] = mfma_32x32x16(ah, chi[ks], acc[i]);
+        acc[i] = mfma_32x32x16(ah, clo[ks], acc[i]);
+        acc[i] = mfma_32x32x16(alo, chi[ks], acc[i]);
+      }
+    }
+    // Rows out through the head plane (its reads are done), chunks XOR-swizzled by row.
+#pragma unroll
+    for (int i = 0; i < NTL; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float x0 = acc[i][4 * q];
+        if (m == 0 && i == 0 && q == 0 && hb == 0) x0 = 0.0f;   // dk[0]: the decision gradient, part 2
+        const uint32_t lo = cvt_pk_bf16(x0, acc[i][4 * q + 1]);
+        const uint32_t hi = cvt_pk_bf16(acc[i][4 * q + 2], acc[i][4 * q + 3]);
+        *reinterpret_cast<uint2 *>(smem + col * RB + (((4 * i + q) ^ k_swizzle<CPR>(col)) * 16) + hb * 8) =
+            make_uint2(lo, hi);
+      }
+    wave_lds_sync();
+    char *dst = static_cast<char *>(m == 0 ? p.dk : p.dv);
+    constexpr int RPP = 64 / CPR;
+#pragma unroll
+    for (int r0 = 0; r0 < 32; r0 += RPP) {
+      const int row = r0 + lane / CPR, ch = lane % CPR;
+      if (row < ntok)
+        *reinterpret_cast<uint4 *>(dst + row_k(p, b, t0 + row, g, D) * 2 + ch * 16) =
+            *reinterpret_cast<const uint4 *>(smem + row * RB + ((ch ^ k_swizzle<CPR>(row)) * 16));
+    }
+    wave_lds_sync();   // the planes are restaged next
+  }
+
+  // e_tj = (E[t][j] - X~_j . dX~_j) / z_j; register r of a tile is row
+  // (token) t0 + 8 (r / 4) + 4 hb + r % 4, column (state) t0 + 32 c + col.
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    const int j = t0 + 32 * c + col;
+    const float dq = qsc[c];
+    if (j > last) continue;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int tt = t0 + 8 * (r >> 2) + 4 * hb + (r & 3);
+      const int dl = j - tt;
+      if (dl >= 0 && dl < W && tt <= last) p.e[(un + tt) * W + dl] = (ae[c][r] - dq) * izc[c];
+    }
+  }
+}
+
 // States -> tokens, part 2, one thread per (unit, token r): the weight
 // gradients e give d omega_r = sum_j e_rj prod_{r+1..j} alpha and
 // d alpha_r = sum_j prod_{r+1..j} alpha * sum_{t = a_j .. r-1} e_tj omega_t
@@ -1195,7 +1405,12 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     dm += __shfl_xor(dm, 32, 64);
     if (hb == 0 && sv_ok) p.dmask[int64_t(u) * p.n + js] = dm;
   }
+  // dK~ and dV~ leave as bf16 head and tail planes ([U][n][D] each, in the
+  // fp32 array's bytes): x = hi + lo to about 2^-17, the operand form the
+  // token pass stages straight into LDS.
   const float sc_k = sl2 / kLog2e;
+  const int64_t plane = int64_t(U) * p.n * D;
+  uint16_t *out = reinterpret_cast<uint16_t *>(PART == 1 ? p.dvs : p.dks);
 #pragma unroll
   for (int i = 0; i < NTL; ++i)
 #pragma unroll
@@ -1204,9 +1419,41 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       if (st >= p.n) continue;
       const int dim = 32 * i + col;
       const int64_t o = (int64_t(u) * p.n + st) * D + dim;
-      if constexpr (PART != 1) p.dks[o] = dim == 0 ? 0.0f : dk[i][j] * sc_k;
-      if constexpr (PART != 2) p.dvs[o] = dv[i][j];
+      const float x = PART == 1 ? dv[i][j] : (dim == 0 ? 0.0f : dk[i][j] * sc_k);
+      const uint32_t h = bf16_bits(x);
+      out[o] = static_cast<uint16_t>(h);
+      out[plane + o] = static_cast<uint16_t>(bf16_bits(x - __uint_as_float(h << 16)));
     }
+  // X~_j . dX~_j of the wave's states for the token pass (the value part
+  // here, the key part added by the second kernel): per state, the lanes of
+  // a half hold its 32-dim slices.
+  {
+    const uint16_t *xs = reinterpret_cast<const uint16_t *>(PART == 1 ? p.vs : p.ks);
+    float part[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int st = min(s0 + 8 * (j >> 2) + 4 * hb + (j & 3), p.n - 1);
+      part[j] = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NTL; ++i) {
+        const int dim = 32 * i + col;
+        const float xv = __uint_as_float(uint32_t(xs[(int64_t(u) * p.n + st) * D + dim]) << 16);
+        const float x = PART == 1 ? dv[i][j] : (dim == 0 ? 0.0f : dk[i][j] * sc_k);
+        part[j] = fmaf(xv, x, part[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) part[j] = row_sum<32>(part[j]);
+    if (col == 0) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int st = s0 + 8 * (j >> 2) + 4 * hb + (j & 3);
+        if (st >= p.n) continue;
+        float *q = p.qs + int64_t(u) * p.n + st;
+        *q = PART == 1 ? part[j] : *q + part[j];
+      }
+    }
+  }
 }
 
 int blocks_for(int64_t threads) {
@@ -1265,7 +1512,18 @@ hipError_t train_backward_impl(const TrainParams &p, hipStream_t s) {
     hipLaunchKernelGGL((train_dkv_kernel<ES, D, G>), dim3(blocks_for(int64_t(U) * nblocks * 64)),
                        dim3(kThreads), 0, s, p, nblocks);
   }
-  hipLaunchKernelGGL((train_tokens_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
+  if constexpr (ES == 2) {
+    const dim3 grid((p.n + 31) / 32, U);
+    switch (2 + (p.window + 14) / 16) {   // 16-row k-steps for the 31 + w states
+      case 2: hipLaunchKernelGGL((train_tokens_mfma_kernel<D, 2>), grid, dim3(64), 0, s, p); break;
+      case 3: hipLaunchKernelGGL((train_tokens_mfma_kernel<D, 3>), grid, dim3(64), 0, s, p); break;
+      case 4: hipLaunchKernelGGL((train_tokens_mfma_kernel<D, 4>), grid, dim3(64), 0, s, p); break;
+      case 5: hipLaunchKernelGGL((train_tokens_mfma_kernel<D, 5>), grid, dim3(64), 0, s, p); break;
+      default: hipLaunchKernelGGL((train_tokens_mfma_kernel<D, 6>), grid, dim3(64), 0, s, p); break;
+    }
+  } else {
+    hipLaunchKernelGGL((train_tokens_kernel<ES, D>), dim3((p.n + 63) / 64, U), dim3(64), 0, s, p);
+  }
   hipLaunchKernelGGL((train_neurons_kernel<ES, D>), dim3(blocks_for(int64_t(U) * p.n)),
                      dim3(kThreads), 0, s, p);
   return hipGetLastError();
