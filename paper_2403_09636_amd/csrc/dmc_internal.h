@@ -164,7 +164,7 @@ struct TrainParams {
                              // in the same bytes, bf16 head and tail planes [2][U][n][d]
                              // (matrix-core passes)
   float *dmask;              // [U][n]
-  float *qs;                 // [U][n]: K~_j . dK~_j + V~_j . dV~_j (matrix-core passes)
+  float *qs;                 // [2][U][n]: V~_j . dV~_j, then K~_j . dK~_j (matrix-core passes)
   float *e;                  // [U][n][w]: d loss / d weight of token t in state t + i
   float c, tau, scale_log2;
   int32_t batch, n, hq, hkv, window, omega_src;
