@@ -699,11 +699,13 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   };
 
   for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
-  static_assert(kStages == 3, "the block loop below is unrolled for a 3-slot ring");
-  for (int kb = 0; kb < nblk; kb += 3) {
+  static_assert(kStages == 3 || kStages == 4, "the block loop below is unrolled for 3 or 4 slots");
+  for (int kb = 0; kb < nblk; kb += kStages) {
     step(std::integral_constant<int, 0>{}, kb);
     if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
     if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+    if constexpr (kStages > 3)
+      if (kb + 3 < nblk) step(std::integral_constant<int, kStages - 1>{}, kb + 3);
   }
 
   // Normalise and store: lane holds dims 32 t + 8 i + 4 hb .. + 4 of its column.

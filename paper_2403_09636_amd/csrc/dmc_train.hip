@@ -918,7 +918,7 @@ __global__ __launch_bounds__(kThreads) void train_neurons_kernel(TrainParams p) 
 // Query-major kernels (forward, dq): one workgroup = 4 waves = 128 query
 // columns of one unit, token-major (column c = token c / G, head c % G); a
 // wave owns 32 columns.  The unit's states stream through LDS in blocks of 32
-// rows (direct global -> LDS transfers, a 3-slot ring two blocks ahead), and
+// rows (direct global -> LDS transfers, a 4-slot ring three blocks ahead), and
 // per block and wave, lane l holding column l % 32 and half l / 32:
 //   S^T[state][col] = K'[state] . Q'[col]     (A = K' rows, B = Q'^T)
 // Score row m is state pi(m) (bits 2 and 3 of m swapped), so a lane's score
@@ -933,7 +933,8 @@ __global__ __launch_bounds__(kThreads) void train_neurons_kernel(TrainParams p) 
 //
 // State-major kernel (dK~, dV~, mask gradient): one workgroup = 4 waves =
 // 128 states of one unit, a wave owning 32 (its K~, V~ rows are operands in
-// registers); query rows (token, head) stream through LDS in blocks of 32:
+// registers); query rows (token, head) stream through LDS in blocks of 32
+// (a 3-slot ring):
 //   S[row][state] = Q[row] . K~[state],  dP[row][state] = dO[row] . V~[state]
 // with rows pi-permuted so that P^T and dS^T come out as A operands of
 //   dV~[state][dim] += P^T[state][row] dO[row][dim]
@@ -942,6 +943,20 @@ __global__ __launch_bounds__(kThreads) void train_neurons_kernel(TrainParams p) 
 // transposed LDS read ds_read_b64_tr_b16 on rows stored with the value
 // swizzle.
 // ---------------------------------------------------------------------------
+
+// Ring slots (blocks in flight + 1) of the query-major kernels (64 KiB of
+// LDS per workgroup, two per CU) and of the state-major ones (three per CU
+// at 3 slots; 4 slots measured slower there, faster for forward and dq).
+constexpr int kQMajorStages = 4, kDkvStages = 3;
+
+// Waits until the ring block of step kb has landed: `after` blocks were
+// issued behind it, PER transfers each.
+template <int PER>
+__device__ __forceinline__ void wait_block(int after) {
+  if (after >= 2) wait_vmcnt<2 * PER>();
+  else if (after == 1) wait_vmcnt<PER>();
+  else wait_vmcnt<0>();
+}
 
 // Swizzle of a block's rows: 0 key (row reads), 1 value (transposed reads),
 // 2 dual (both).
@@ -988,7 +1003,7 @@ __device__ __forceinline__ uint32_t row_offset(int row, int ks, int hb) {
 // Query-major kernels: MODE 0 = forward, 1 = dq.
 template <int D, int G, int MODE>
 __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p, int ntiles) {
-  constexpr int kSt = 3;               // ring slots
+  constexpr int kSt = kQMajorStages;   // ring slots
   constexpr int T = 32 / G;            // tokens per wave
   constexpr int TW = kWaves * T;       // tokens per workgroup
   constexpr int KS = D / 16;           // 16-dim k-steps of the score product
@@ -1097,9 +1112,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
 
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
-    const int after = min(nblk - 1 - kb, kSt - 2);
-    if (after >= 1) wait_vmcnt<2 * DPW>();
-    else wait_vmcnt<0>();
+    wait_block<2 * DPW>(min(nblk - 1 - kb, kSt - 2));
     __syncthreads();   // block kb is in LDS for every wave; the slot of kb - 1 is free
     if (kb + kSt - 1 < nblk) issue(kb + kSt - 1, (ST + kSt - 1) % kSt);
     if (kb * 32 >= wave_hi) return;
@@ -1180,10 +1193,12 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   };
 
   for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(kb, kb);
-  for (int kb = 0; kb < nblk; kb += 3) {
+  for (int kb = 0; kb < nblk; kb += kSt) {
     step(std::integral_constant<int, 0>{}, kb);
     if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
     if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+    if constexpr (kSt > 3)
+      if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
   }
 
   // Lane holds dims 32 i + 8 j + 4 hb .. + 4 of its column.
@@ -1218,7 +1233,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
 template <int D, int G, int PART>
 __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams p, int ntiles) {
   static_assert(PART == 1 || PART == 2, "dV part or dK part");
-  constexpr int kSt = 3;
+  constexpr int kSt = kDkvStages;
   constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
   constexpr int SLOT = 2 * BLK + 256;   // query rows, dO rows, 32 x (L, D) statistics
@@ -1306,9 +1321,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
 
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
-    const int after = min(nblk - 1 - kb, kSt - 2);
-    if (after >= 1) wait_vmcnt<2 * DPW + 1>();
-    else wait_vmcnt<0>();
+    wait_block<2 * DPW + 1>(min(nblk - 1 - kb, kSt - 2));
     __syncthreads();
     if (kb + kSt - 1 < nblk) issue(qb0 + kb + kSt - 1, (ST + kSt - 1) % kSt);
     const int rb = (qb0 + kb) * 32;                  // first row of the block
@@ -1394,10 +1407,12 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   };
 
   for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(qb0 + kb, kb);
-  for (int kb = 0; kb < nblk; kb += 3) {
+  for (int kb = 0; kb < nblk; kb += kSt) {
     step(std::integral_constant<int, 0>{}, kb);
     if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
     if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+    if constexpr (kSt > 3)
+      if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
   }
 
   // Outputs: C[state][dim] -- lane holds dim 32 i + col of states
