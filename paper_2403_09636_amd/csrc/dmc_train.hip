@@ -1256,8 +1256,10 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
   const float sl2 = p.scale_log2;
 
-  // K~ and V~ of the lane's state as B operands (dims 16 ks + 8 hb .. + 8);
-  // key element 0 (the mask carrier) is left out of the scores.
+  // K~ and V~ of the lane's state as B operands (dims 16 ks + 8 hb .. + 8).
+  // Key element 0 carries the state's mask entry (bf16 of mask * sqrt(d));
+  // the query operand's element 0 is set to 1, so every score arrives with
+  // the bias of a past row, which the diagonal takes out again.
   uint4 kop[KS], vop[KS];
   float bias = 0.0f;
   {
@@ -1268,8 +1270,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       vop[ks] = (sv_ok && PART != 1) ? ld16(static_cast<const char *>(p.vs) + so + ks * 32 + hb * 16)
                                      : zero4;
     }
-    if (hb == 0) kop[0].x &= 0xffff0000u;
-    // the mask entry as the forward used it: bf16 of mask * sqrt(d), back to log2 units
+    // the same entry in log2 units
     if (sv_ok)
       bias = __uint_as_float(bf16_bits(p.mask[int64_t(u) * p.n + js] * (kLog2e / sl2)) << 16) * sl2;
   }
@@ -1281,29 +1282,45 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   const int qb0 = row_lo >> 5, qb1 = (nrows + 31) >> 5;
   const int nblk = qb1 - qb0;
   const uint32_t ring = lds_offset(smem);
-  int64_t qoff[DPW];
-  uint32_t loff[DPW];
+  // This thread's chunks: block row loff, byte offset lofs from the block's
+  // first row (a block's rows r = t G + h are 32 / G whole tokens).
+  uint32_t qoff[DPW], loff[DPW], lofs[DPW];
 #pragma unroll
   for (int i = 0; i < DPW; ++i) {
     const int c = (i * kWaves + wave) * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     loff[i] = row;
     qoff[i] = (pc ^ dual_swizzle<CPR>(row)) * 16;
+    lofs[i] = uint32_t(((row / G) * p.hq + row % G) * D * 2) + qoff[i];
   }
+  const int64_t row0 = row_q(p, b, 0, g * G, D) * 2;   // bytes to (b, token 0, head g G)
+  const int64_t tokb = int64_t(p.hq) * D * 2;          // bytes per token
   // Statistics of rows 8 wave .. 8 wave + 7 of a block: lanes 0, 1 move their
   // L (32 bytes), lanes 2, 3 their D ([U][n][G] is row-contiguous and padded
   // by 32 rows), so every wave issues the same number of transfers.
   const char *stat_src = reinterpret_cast<const char *>(lane < 2 ? p.lse : p.dsum) +
                          (int64_t(u) * p.n * G + 8 * wave) * 4 + (lane & 1) * 16;
   auto issue = [&](int qb, int st) {
+    if (qb * 32 + 32 <= nrows) {   // whole block: one base, fixed offsets
+      const int64_t bb = row0 + int64_t(qb * (32 / G)) * tokb;
+      const char *qp = uniform_ptr(static_cast<const char *>(p.q) + bb);
+      const char *dp = uniform_ptr(static_cast<const char *>(p.dout) + bb);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
-      const int rg = min(qb * 32 + int(loff[i]), nrows - 1);   // rows past the sequence: in bounds, masked
-      const int tq = rg / G, h = rg - tq * G;
-      const int64_t ro = row_q(p, b, tq, g * G + h, D) * 2 + qoff[i];
-      dma16(dst, static_cast<const char *>(p.q) + ro);
-      dma16(dst + BLK, static_cast<const char *>(p.dout) + ro);
+      for (int i = 0; i < DPW; ++i) {
+        const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
+        dma16_s(dst, qp, lofs[i]);
+        dma16_s(dst + BLK, dp, lofs[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < DPW; ++i) {
+        const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
+        const int rg = min(qb * 32 + int(loff[i]), nrows - 1);   // rows past the sequence: in bounds, masked
+        const int tq = rg / G, h = rg - tq * G;
+        const int64_t ro = row_q(p, b, tq, g * G + h, D) * 2 + qoff[i];
+        dma16(dst, static_cast<const char *>(p.q) + ro);
+        dma16(dst + BLK, static_cast<const char *>(p.dout) + ro);
+      }
     }
     if (lane < 4) dma16(ring + st * SLOT + 2 * BLK + wave * 64, stat_src + int64_t(qb) * 128);
   };
@@ -1332,7 +1349,9 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(qd + raddr[ks]), kop[ks], sc);
+      uint4 qa = *reinterpret_cast<const uint4 *>(qd + raddr[ks]);
+      if (ks == 0 && hb == 0) qa.x = (qa.x & 0xffff0000u) | 0x3f80u;   // query element 0 <- 1
+      sc = mfma_32x32x16(qa, kop[ks], sc);
       if constexpr (PART != 1)
         dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
     }
@@ -1368,7 +1387,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
 #pragma unroll
           for (int e = 0; e < 2; ++e) {
             const int i = 8 * kk + 2 * q + e;
-            pv[e] = fast_exp2(fmaf(sc[i], sl2, bias - Lr[i]));
+            pv[e] = fast_exp2(fmaf(sc[i], sl2, -Lr[i]));
             dsv[e] = pv[e] * (dp[i] - Dr[i]);
             dm += dsv[e];
           }
@@ -1385,7 +1404,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
             const int rg = rb + 16 * kk + 8 * hb + 2 * q + e;
             const int tq = rg / G;
             const bool vis = sv_ok && rg < nrows && tq >= js;
-            const float x = sc[i] * sl2 + (tq > js ? bias : 0.0f);
+            const float x = sc[i] * sl2 - (tq > js ? 0.0f : bias);   // no bias on the diagonal
             pv[e] = vis ? fast_exp2(x - Lr[i]) : 0.0f;
             dsv[e] = vis ? pv[e] * (dp[i] - Dr[i]) : 0.0f;   // statistics past the rows are not read
             if (vis && tq > js) dm += dsv[e];
