@@ -166,16 +166,20 @@ def cpu_model():
         return ""
 
 
+def cpu_workers(imports_torch=False):
+    """Oracle worker processes: one per host core, at most 16 (a GPU's share
+    of its host).  Workers that import torch (the training oracle) open the
+    GPU device as a side effect, so they are kept to 15: with this process,
+    at most 16 hold it."""
+    return max(1, min(os.cpu_count() or 1, 15 if imports_torch else 16))
+
+
 def cpu_pool(imports_torch=False):
-    """Worker processes for the oracle timing, one per host core (at most 16,
-    a GPU's share of its host).  Start them before this process touches the
-    GPU: they are fresh interpreters.  Workers that import torch (the
-    training oracle) open the GPU device as a side effect, so they are kept
-    to 15: with this process, at most 16 hold it."""
+    """The oracle workers, started before this process touches the GPU (they
+    are fresh interpreters)."""
     import multiprocessing as mp
 
-    procs = max(1, min(os.cpu_count() or 1, 15 if imports_torch else 16))
-    return mp.get_context("spawn").Pool(procs)
+    return mp.get_context("spawn").Pool(cpu_workers(imports_torch))
 
 
 def cpu_baseline(w, lens_layers, seconds, pool=None):
@@ -194,7 +198,7 @@ def cpu_baseline(w, lens_layers, seconds, pool=None):
     own = pool is None
     if own:
         pool = cpu_pool()
-    procs = pool._processes
+    procs = cpu_workers()
     jobs = [(1000 + i,) + job[1:] for i in range(procs)]
     t0 = time.perf_counter()
     try:
@@ -332,7 +336,7 @@ def cpu_baseline_train(w, seconds, pool=None):
     own = pool is None
     if own:
         pool = cpu_pool(imports_torch=True)
-    procs = pool._processes
+    procs = cpu_workers(imports_torch=True)
     try:
         res = pool.map(_oracle_train_units, [(500 + i, seconds / 2, n, d, G) for i in range(procs)],
                        chunksize=1)
@@ -445,6 +449,34 @@ def main():
         if pool is not None:
             pool.close()
             pool.join()
+
+
+def hbm_context(torch, dev):
+    """Streaming rates of two plain torch kernels on the same device, as
+    context beside the 8 TB/s spec peak: a 1 GiB device-to-device copy
+    (read + write bytes) and a sum over 2 GiB of bf16 (read bytes)."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    x = torch.ones(n, dtype=torch.bfloat16, device=dev)
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    copy_ms = timed(lambda: dst.copy_(src))
+    sum_ms = timed(lambda: x.sum())
+    del src, dst, x
+    return {"copy_GBps": round(2 * n / (copy_ms * 1e-3) / 1e9, 1),
+            "sum_read_GBps": round(2 * n / (sum_ms * 1e-3) / 1e9, 1),
+            "note": "torch copy_ and sum kernels, context only"}
 
 
 def bench_decode(args, pool):
@@ -575,6 +607,7 @@ def bench_decode(args, pool):
                      "alg_bytes_per_launch": int(alg_per_launch),
                      "avg_launch_us": round(avg_launch_ms * 1e3, 2)},
         "setup_s": round(setup_s, 1),
+        "hbm_context": hbm_context(torch, dev),
     }
     if prefill_ms:
         n = w.prompt_len
