@@ -430,6 +430,20 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   const int cnt = ok ? max(0, min(T, nb - a)) : 0;
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
+  // The tile's page-table slice, loaded now for a bound on the slots it can
+  // see (a token's slot never exceeds the token) and stored to LDS before the
+  // first barrier.
+  const int P = 1 << p.log2p;
+  const int64_t pt = int64_t(u) * p.maxpages;
+  const int npg = min(min((min(nb, tile * TW + TW) + P - 1) >> p.log2p, p.maxpages), kPtabLds);
+  constexpr int kPtPer = (kPtabLds + kThreads - 1) / kThreads;
+  int ptv[kPtPer];
+#pragma unroll
+  for (int j = 0; j < kPtPer; ++j) {
+    const int i = tid + j * kThreads;
+    ptv[j] = i < npg ? p.ptab[pt + i] : 0;
+  }
+
   const int seg = cnt > 0 ? token_slots(p, u, a, cnt) : -1;
   const int tok = col / G, head = col - tok * G;
   const bool colv = tok < cnt;
@@ -518,18 +532,18 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
         };
     walk_window_state<2, D>(p, u, b, g, a, cnt, snap, batch_end);
   }
-  __syncthreads();   // slot limits published; staging area free again
+#pragma unroll
+  for (int j = 0; j < kPtPer; ++j) {
+    const int i = tid + j * kThreads;
+    if (i < npg) s_pt[i] = ptv[j];
+  }
+  __syncthreads();   // slot limits and page table published; staging area free again
 
   int s_top = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) s_top = max(s_top, s_hi[w]);
   s_top = __builtin_amdgcn_readfirstlane(s_top);
   const int nblk = (s_top + 31) >> 5;
-  const int P = 1 << p.log2p;
-  const int64_t pt = int64_t(u) * p.maxpages;
-  const int npg = min((s_top + P - 1) >> p.log2p, kPtabLds);
-  for (int i = tid; i < npg; i += kThreads) s_pt[i] = p.ptab[pt + i];
-  __syncthreads();
 
   // Transfers of block kb into ring slot st.  This thread's chunks and their
   // byte offsets within a 32-row block (rows XOR-swizzled; LDS position =
