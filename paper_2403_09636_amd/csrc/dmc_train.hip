@@ -1013,7 +1013,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   constexpr int BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
   constexpr int KSW = MODE == 0 ? 0 : 2;   // dq also reads keys transposed
-  constexpr int VSW = MODE == 0 ? 1 : 0;   // forward reads values transposed
+  constexpr int VSW = MODE == 0 ? 1 : KSW;   // forward reads values transposed; dq as rows,
+                                             // laid out like the keys (shared offsets)
   static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
   __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
 
@@ -1081,13 +1082,13 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   // Block transfers (same chunk mapping as prompt attention; the unit's
   // states are contiguous, so one wave-uniform base per block).
   const uint32_t ring = lds_offset(smem);
-  uint32_t koff[DPW], voff[DPW];
+  uint32_t koff[DPW], voff[MODE == 0 ? DPW : 1];
 #pragma unroll
   for (int i = 0; i < DPW; ++i) {
     const int c = (i * kWaves + wave) * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     koff[i] = row * RB + (pc ^ block_swizzle<CPR, KSW>(row)) * 16;
-    voff[i] = row * RB + (pc ^ block_swizzle<CPR, VSW>(row)) * 16;
+    if constexpr (MODE == 0) voff[i] = row * RB + (pc ^ block_swizzle<CPR, VSW>(row)) * 16;
   }
   const char *kst = static_cast<const char *>(p.ks) + int64_t(u) * p.n * RB;
   const char *vst = static_cast<const char *>(p.vs) + int64_t(u) * p.n * RB;
@@ -1096,16 +1097,15 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
     for (int i = 0; i < DPW; ++i) {
       const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
       dma16_s(kdst, uniform_ptr(kst + int64_t(kb) * BLK), koff[i]);
-      dma16_s(kdst + BLK, uniform_ptr(vst + int64_t(kb) * BLK), voff[i]);
+      dma16_s(kdst + BLK, uniform_ptr(vst + int64_t(kb) * BLK), MODE == 0 ? voff[i] : koff[i]);
     }
   };
 
   const int krow = score_slot(col);
-  uint32_t kaddr[KS], vrow[MODE == 1 ? KS : 1];
+  uint32_t kaddr[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     kaddr[ks] = row_offset<D, KSW>(krow, ks, hb);
-    if constexpr (MODE == 1) vrow[ks] = row_offset<D, VSW>(krow, ks, hb);
   }
   uint32_t traddr[NTL][2];
   tr_offsets<D, MODE == 0 ? VSW : KSW>(lane, traddr);
@@ -1170,7 +1170,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
       f32x16_t dp = f32x16_t{};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(vd + vrow[ks]), dop[ks], dp);
+        dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(vd + kaddr[ks]), dop[ks], dp);
       uint4 sb[2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
