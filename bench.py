@@ -431,7 +431,7 @@ def bench_train(args, pool=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: this benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
               "the decode path shards by kv head or by sequence, see the design notes",
               file=sys.stderr)
         sys.exit(2)
