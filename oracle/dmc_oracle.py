@@ -183,10 +183,11 @@ class LayerCache:
         v = np.array(v, dtype=np.float64)
         active = np.ones(self.U, bool) if active is None else np.asarray(active, bool)
 
-        # lines 1-2: alpha_t, omega_t; reading 3: an empty cache appends
+        # Algorithm 1, the decision and the importance; reading 3: an empty cache appends
         alpha = decision(k[:, 0] if logits is None else logits, c) * (self.l > 0)
         omega = importance(q0_group, omega_src)
-        # line 3: k_t[0] <- 0  (q_t[0] is zeroed where scores are formed)
+        # the decision neuron is cleared from the key: k_t[0] <- 0 (q_t[0] is zeroed
+        # where scores are formed)
         k[:, 0] = 0.0
 
         acc = np.nonzero(active & (alpha == 1))[0]
@@ -196,7 +197,7 @@ class LayerCache:
             self._windowed(k, v, alpha, omega, acc, app)
             return alpha, np.where(active, self.l - 1, -1)
 
-        # lines 4-7: accumulate into the last slot l-1
+        # alpha = 1: omega-weighted running mean into the last slot l-1, z grows by omega
         if acc.size:
             last = self.l[acc] - 1
             z_prev = self.z[acc]
@@ -206,7 +207,7 @@ class LayerCache:
             self.V[acc, last] = (self.V[acc, last] * z_prev[:, None]
                                  + v[acc] * omega[acc, None]) / z_t[:, None]
             self.z[acc] = z_t
-        # lines 8-11: append
+        # alpha = 0: append a slot, z restarts at omega
         if app.size:
             pos = self.l[app]
             self.z[app] = omega[app]
@@ -249,7 +250,7 @@ class LayerCache:
     def attend(self, u, q_heads):
         """Softmax attention of the query heads q_heads [G, d] of unit u."""
         q = np.array(q_heads, dtype=np.float64)
-        q[:, 0] = 0.0                                  # Algorithm 1, line 3
+        q[:, 0] = 0.0                                  # Algorithm 1: q_t[0] leaves the score
         n = self.l[u]
         K, V = self.K[u, :n], self.V[u, :n]
         s = (q @ K.T) / math.sqrt(self.d)              # [G, n]

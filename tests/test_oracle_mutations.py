@@ -17,7 +17,7 @@ MUTATIONS = {
     "no_bias": ("(k0 > np.float64(np.float32(c)))", "(k0 > 0.0)"),
     "first_token_may_accumulate": ("else logits, c) * (self.l > 0)", "else logits, c)"),
     "key_not_zeroed": ("        k[:, 0] = 0.0\n", "        pass\n"),
-    "query_not_zeroed": ("        q[:, 0] = 0.0                                  # Algorithm 1, line 3",
+    "query_not_zeroed": ("        q[:, 0] = 0.0                                  # Algorithm 1: q_t[0] leaves the score",
                          "        pass"),
     "z_drops_omega": ("z_t = z_prev + omega[acc]", "z_t = z_prev + 0.5"),
     "merge_drops_old_weight": ("(self.K[acc, last] * z_prev[:, None]", "(self.K[acc, last]"),
