@@ -62,6 +62,10 @@ CASES = [
     ("bf16", 128, 1, 1, 1, 70, 17, 3.0, 0.2, [6.0], "lead", False),
     ("bf16", 128, 4, 1, 2, 120, 18, 5.0, 0.1, [8.0, 2.0], "uniform", True),
     ("bf16", 64, 1, 1, 1, 150, 40, 5.0, 0.3, [30.0], "lead", True),
+    # degenerate and block-boundary lengths on the matrix-core kernels
+    ("bf16", 128, 1, 1, 2, 1, 12, 5.0, 0.1, [2.0, 4.0], "lead", True),
+    ("bf16", 128, 4, 2, 1, 2, 12, 5.0, 0.1, [3.0], "uniform", False),
+    ("bf16", 64, 2, 1, 2, 33, 3, 5.0, 0.1, [2.0, 8.0], "lead", True),
 ]
 
 
