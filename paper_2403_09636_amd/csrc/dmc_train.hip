@@ -1110,6 +1110,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   uint32_t traddr[NTL][2];
   tr_offsets<D, MODE == 0 ? VSW : KSW>(lane, traddr);
 
+  // One block of the dq kernel.
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
     wait_block<2 * DPW>(min(nblk - 1 - kb, kSt - 2));
@@ -1134,7 +1135,80 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
         else if (st == t) sv[rr] -= diag;
       }
     }
-    if constexpr (MODE == 0) {
+    {   // dq (the forward runs the pipelined step below)
+      // dP^T = V . dO^T, with P = exp2(S - L) (the forward's statistics)
+      // formed between its MFMAs (order pinned; value rows read two ahead),
+      // then dS^T = P^T (dP^T - D).
+      f32x16_t dp = f32x16_t{};
+      float pe[16];
+      uint4 vr[3];
+      vr[0] = *reinterpret_cast<const uint4 *>(vd + kaddr[0]);
+      vr[1] = *reinterpret_cast<const uint4 *>(vd + kaddr[1]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 2 < KS) vr[(ks + 2) % 3] = *reinterpret_cast<const uint4 *>(vd + kaddr[ks + 2]);
+        dp = mfma_32x32x16(vr[ks % 3], dop[ks], dp);
+#pragma unroll
+        for (int e = 0; e < 16 / KS; ++e) {
+          const int i = ks * (16 / KS) + e;
+          pe[i] = fast_exp2(fmaf(sv[i], sl2, -Lc));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      uint4 sb[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r0 = 8 * kk + 2 * q;
+          w[q] = cvt_pk_bf16(pe[r0] * (dp[r0] - Dc), pe[r0 + 1] * (dp[r0 + 1] - Dc));
+        }
+        sb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+      for (int i = 0; i < NTL; ++i)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          acc[i] = mfma_32x32x16(tr_operand<RB>(kd, traddr[i], kk), sb[kk], acc[i]);
+    }
+  };
+
+  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(kb, kb);
+  if constexpr (MODE == 0) {
+    // Step kb runs block kb's exponentials between the score MFMAs of block
+    // kb + 1 (one accumulator chain; order pinned by scheduling barriers),
+    // then block kb's value product.
+    f32x16_t scn = f32x16_t{};
+    if (nblk > 0) {
+      wait_block<2 * DPW>(min(nblk - 1, kSt - 2));
+      __syncthreads();
+      if (wave_hi > 0) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          scn = mfma_32x32x16(*reinterpret_cast<const uint4 *>(
+                                  reinterpret_cast<const char *>(smem) + kaddr[ks]), qop[ks], scn);
+      }
+    }
+    auto step0 = [&](auto stage_c, int kb) {
+      constexpr int ST = decltype(stage_c)::value, SN = (ST + 1) % kSt;
+      if (kb + 1 < nblk) wait_block<2 * DPW>(min(kSt - 3, nblk - 2 - kb));   // block kb + 1 landed
+      __syncthreads();   // every wave is past step kb - 1: the slot of kb - 1 is free
+      if (kb + kSt - 1 < nblk) issue(kb + kSt - 1, (ST + kSt - 1) % kSt);
+      if (kb * 32 >= wave_hi) return;
+      const char *vd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK + BLK;
+      const char *kn = reinterpret_cast<const char *>(smem) + SN * 2 * BLK;   // block kb + 1's keys
+      float sv[16];
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) sv[rr] = scn[rr];
+      if (kb * 32 + 32 > a) {   // the block reaches the diagonal
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int st = kb * 32 + score_slot(8 * (rr >> 2) + 4 * hb + (rr & 3));
+          if (st > t) sv[rr] = neg_inf();
+          else if (st == t) sv[rr] -= diag;
+        }
+      }
       float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
 #pragma unroll
       for (int rr = 3; rr < 15; rr += 2) mx = fmaxf(fmaxf(mx, sv[rr]), sv[rr + 1]);
@@ -1148,14 +1222,32 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
 #pragma unroll
         for (int i = 0; i < NTL; ++i) acc[i] *= f;
       }
+      // The next block's slot always holds readable data; past the last
+      // block its scores are not used.
+      uint4 kr[3];
+      kr[0] = *reinterpret_cast<const uint4 *>(kn + kaddr[0]);
+      kr[1] = *reinterpret_cast<const uint4 *>(kn + kaddr[1]);
+      f32x16_t sc = f32x16_t{};
+      float ev[16];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 2 < KS) kr[(ks + 2) % 3] = *reinterpret_cast<const uint4 *>(kn + kaddr[ks + 2]);
+        sc = mfma_32x32x16(kr[ks % 3], qop[ks], sc);
+#pragma unroll
+        for (int e = 0; e < 16 / KS; ++e) {
+          const int i = ks * (16 / KS) + e;
+          ev[i] = fast_exp2(fmaf(sv[i], sl2, -m));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      scn = sc;
       uint4 pb[2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         uint32_t w[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          w[q] = cvt_pk_bf16(fast_exp2(fmaf(sv[8 * kk + 2 * q], sl2, -m)),
-                             fast_exp2(fmaf(sv[8 * kk + 2 * q + 1], sl2, -m)));
+          w[q] = cvt_pk_bf16(ev[8 * kk + 2 * q], ev[8 * kk + 2 * q + 1]);
           ls = add_pair(w[q], ls);
         }
         pb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
@@ -1165,40 +1257,22 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
           acc[i] = mfma_32x32x16(tr_operand<RB>(vd, traddr[i], kk), pb[kk], acc[i]);
-    } else {
-      // dP^T = V . dO^T, then dS^T = P^T (dP^T - D) with P from the forward's statistics.
-      f32x16_t dp = f32x16_t{};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(vd + kaddr[ks]), dop[ks], dp);
-      uint4 sb[2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        uint32_t w[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int r0 = 8 * kk + 2 * q;
-          const float p0 = fast_exp2(fmaf(sv[r0], sl2, -Lc));
-          const float p1 = fast_exp2(fmaf(sv[r0 + 1], sl2, -Lc));
-          w[q] = cvt_pk_bf16(p0 * (dp[r0] - Dc), p1 * (dp[r0 + 1] - Dc));
-        }
-        sb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-#pragma unroll
-      for (int i = 0; i < NTL; ++i)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-          acc[i] = mfma_32x32x16(tr_operand<RB>(kd, traddr[i], kk), sb[kk], acc[i]);
+    };
+    for (int kb = 0; kb < nblk; kb += kSt) {
+      step0(std::integral_constant<int, 0>{}, kb);
+      if (kb + 1 < nblk) step0(std::integral_constant<int, 1>{}, kb + 1);
+      if (kb + 2 < nblk) step0(std::integral_constant<int, 2>{}, kb + 2);
+      if constexpr (kSt > 3)
+        if (kb + 3 < nblk) step0(std::integral_constant<int, kSt - 1>{}, kb + 3);
     }
-  };
-
-  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(kb, kb);
-  for (int kb = 0; kb < nblk; kb += kSt) {
-    step(std::integral_constant<int, 0>{}, kb);
-    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
-    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
-    if constexpr (kSt > 3)
-      if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
+  } else {
+    for (int kb = 0; kb < nblk; kb += kSt) {
+      step(std::integral_constant<int, 0>{}, kb);
+      if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
+      if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
+      if constexpr (kSt > 3)
+        if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
+    }
   }
 
   // Lane holds dims 32 i + 8 j + 4 hb .. + 4 of its column.
