@@ -1421,6 +1421,64 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     const char *dd = qd + BLK;
     const bool interior = rb / G > s0 + 31 && rb + 32 <= nrows && s0 + 32 <= p.n;
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
+    // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
+    // 8 hb + q (pi-permuted rows), from the block's LDS statistics area
+    // ([4][8 L, 8 D] floats).
+    const float *sd = reinterpret_cast<const float *>(qd + 2 * BLK);
+    uint4 pa[2], da[2];
+    if (PART == 2 && interior) {
+      // Scores first; then dP's MFMAs with P's exponentials between them
+      // (order pinned; dO rows read two ahead).
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 qa = *reinterpret_cast<const uint4 *>(qd + raddr[ks]);
+        if (ks == 0 && hb == 0) qa.x = (qa.x & 0xffff0000u) | 0x3f80u;   // query element 0 <- 1
+        sc = mfma_32x32x16(qa, kop[ks], sc);
+      }
+      float Lr[16], Dr[16];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const float *e8 = sd + (2 * kk + hb) * 16;
+#pragma unroll
+        for (int c4 = 0; c4 < 2; ++c4) {
+          const float4 l4 = *reinterpret_cast<const float4 *>(e8 + 4 * c4);
+          const float4 d4 = *reinterpret_cast<const float4 *>(e8 + 8 + 4 * c4);
+          Lr[8 * kk + 4 * c4 + 0] = l4.x; Lr[8 * kk + 4 * c4 + 1] = l4.y;
+          Lr[8 * kk + 4 * c4 + 2] = l4.z; Lr[8 * kk + 4 * c4 + 3] = l4.w;
+          Dr[8 * kk + 4 * c4 + 0] = d4.x; Dr[8 * kk + 4 * c4 + 1] = d4.y;
+          Dr[8 * kk + 4 * c4 + 2] = d4.z; Dr[8 * kk + 4 * c4 + 3] = d4.w;
+        }
+      }
+      float pe[16];
+      uint4 dr[3];
+      dr[0] = *reinterpret_cast<const uint4 *>(dd + raddr[0]);
+      dr[1] = *reinterpret_cast<const uint4 *>(dd + raddr[1]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 2 < KS) dr[(ks + 2) % 3] = *reinterpret_cast<const uint4 *>(dd + raddr[ks + 2]);
+        dp = mfma_32x32x16(dr[ks % 3], vop[ks], dp);
+#pragma unroll
+        for (int e = 0; e < 16 / KS; ++e) {
+          const int i = ks * (16 / KS) + e;
+          pe[i] = fast_exp2(fmaf(sc[i], sl2, -Lr[i]));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        uint32_t wd[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int i = 8 * kk + 2 * q;
+          const float d0 = pe[i] * (dp[i] - Dr[i]), d1 = pe[i + 1] * (dp[i + 1] - Dr[i + 1]);
+          dm += d0;
+          dm += d1;
+          wd[q] = cvt_pk_bf16(d0, d1);
+        }
+        da[kk] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        pa[kk] = da[kk];   // unused by this part
+      }
+    } else {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       uint4 qa = *reinterpret_cast<const uint4 *>(qd + raddr[ks]);
@@ -1429,11 +1487,6 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       if constexpr (PART != 1)
         dp = mfma_32x32x16(*reinterpret_cast<const uint4 *>(dd + raddr[ks]), vop[ks], dp);
     }
-    // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
-    // 8 hb + q (pi-permuted rows), from the block's LDS statistics area
-    // ([4][8 L, 8 D] floats).
-    const float *sd = reinterpret_cast<const float *>(qd + 2 * BLK);
-    uint4 pa[2], da[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       float Lr[16], Dr[16];   // indexed by register 8 kk + q: only this kk's half is loaded
@@ -1489,6 +1542,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       }
       pa[kk] = make_uint4(wp[0], wp[1], wp[2], wp[3]);
       da[kk] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    }
     }
 #pragma unroll
     for (int i = 0; i < NTL; ++i)
