@@ -224,7 +224,7 @@ __device__ __forceinline__ void walk_window_state(const PromptParams &p, int u, 
 // sum is taken over the rounded values.
 // ---------------------------------------------------------------------------
 #ifndef DMC_PROMPT_STAGES
-#define DMC_PROMPT_STAGES 3
+#define DMC_PROMPT_STAGES 4
 #endif
 constexpr int kStages = DMC_PROMPT_STAGES;
 constexpr int kPtabLds = kPromptMaxPages;   // page-table entries of a unit cached in LDS
@@ -618,29 +618,45 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   }
 
   const float sl2 = p.scale_log2;
-  auto step = [&](auto stage_c, int kb) {
-    constexpr int ST = decltype(stage_c)::value;
-    // blocks issued after kb: min(nblk - 1 - kb, kStages - 2)
-    const int after = min(nblk - 1 - kb, kStages - 2);
+  // Waits until at most `after` blocks issued behind the awaited one are in flight.
+  auto wait_after = [&](int after) {
     if (after >= 2) wait_vmcnt<4 * DPW>();
     else if (after == 1) wait_vmcnt<2 * DPW>();
     else wait_vmcnt<0>();
-    __syncthreads();   // block kb is in LDS for every wave; the ring slot of kb - 1 is free
-    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (ST + kStages - 1) % kStages);
-    if (kb * 32 >= wave_hi) return;
-    const char *kd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
-    const char *vd = kd + BLK;
-
+  };
+  auto scores = [&](const char *kd) {
     f32x16_t sc = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       sc = mfma_32x32x16(*reinterpret_cast<const uint4 *>(kd + kaddr[ks]), qop[ks], sc);
+    return sc;
+  };
+
+  // Pipelined over blocks: step kb runs block kb's exponentials between the
+  // score MFMAs of block kb + 1 (one accumulator chain, order pinned by
+  // scheduling barriers, key operands read two ahead), then block kb's value
+  // product.
+  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
+  f32x16_t scn = f32x16_t{};
+  if (nblk > 0) {
+    wait_after(min(nblk - 1, kStages - 2));
+    __syncthreads();   // block 0 is in LDS for every wave
+    if (wave_hi > 0) scn = scores(reinterpret_cast<const char *>(smem));
+  }
+  auto step = [&](auto stage_c, int kb) {
+    constexpr int ST = decltype(stage_c)::value, SN = (ST + 1) % kStages;
+    if (kb + 1 < nblk) wait_after(min(kStages - 3, nblk - 2 - kb));   // block kb + 1 has landed
+    __syncthreads();   // every wave is past step kb - 1: the ring slot of kb - 1 is free
+    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (ST + kStages - 1) % kStages);
+    if (kb * 32 >= wave_hi) return;
+    const char *vd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK + BLK;
+    const char *kn = reinterpret_cast<const char *>(smem) + SN * 2 * BLK;   // block kb + 1's keys
 
     // Raw scores; slots past this column's limit are masked only in blocks
     // that reach the staircase.
     float sv[16];
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) sv[rr] = sc[rr];
+    for (int rr = 0; rr < 16; ++rr) sv[rr] = scn[rr];
     if (kb * 32 + 32 > wave_lo) {   // the block reaches the staircase
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
@@ -661,14 +677,32 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
 #pragma unroll
       for (int t = 0; t < NTL; ++t) acc[t] *= f;
     }
+    // The next block's slot always holds readable data; past the last block
+    // its scores are not used.
+    uint4 kr[3];
+    kr[0] = *reinterpret_cast<const uint4 *>(kn + kaddr[0]);
+    kr[1] = *reinterpret_cast<const uint4 *>(kn + kaddr[1]);
+    f32x16_t sc = f32x16_t{};
+    float ev[16];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 2 < KS) kr[(ks + 2) % 3] = *reinterpret_cast<const uint4 *>(kn + kaddr[ks + 2]);
+      sc = mfma_32x32x16(kr[ks % 3], qop[ks], sc);
+#pragma unroll
+      for (int e = 0; e < 16 / KS; ++e) {
+        const int i = ks * (16 / KS) + e;
+        ev[i] = fast_exp2(fmaf(sv[i], sl2, -m));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    scn = sc;
     uint4 pb[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       uint32_t w[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        w[q] = cvt_pk_bf16(fast_exp2(fmaf(sv[8 * kk + 2 * q], sl2, -m)),
-                           fast_exp2(fmaf(sv[8 * kk + 2 * q + 1], sl2, -m)));
+        w[q] = cvt_pk_bf16(ev[8 * kk + 2 * q], ev[8 * kk + 2 * q + 1]);
         ls = add_pair(w[q], ls);
       }
       pb[kk] = make_uint4(w[0], w[1], w[2], w[3]);
@@ -712,7 +746,6 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
       for (int kk = 0; kk < 2; ++kk) acc[t] = mfma_32x32x16(va[t][kk], pb[kk], acc[t]);
   };
 
-  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
   static_assert(kStages == 3 || kStages == 4, "the block loop below is unrolled for 3 or 4 slots");
   for (int kb = 0; kb < nblk; kb += kStages) {
     step(std::integral_constant<int, 0>{}, kb);
