@@ -57,7 +57,7 @@ class DMCError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
-                          "or python -m paper_2403_09636_amd.csrc.build")
+                          "or python paper_2403_09636_amd/csrc/build.py")
     lib = ctypes.CDLL(LIB_PATH)
     i64p = POINTER(c_int64)
     lib.dmc_cache_workspace_bytes.argtypes = [POINTER(CacheConfig)]

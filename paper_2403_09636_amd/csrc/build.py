@@ -1,6 +1,7 @@
 """Build libdmc.so (gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2403_09636_amd.csrc.build [--verbose]
+Usage: python paper_2403_09636_amd/csrc/build.py [--verbose]
+(run by path: importing the package first would load the library it builds)
 """
 from __future__ import annotations
 

@@ -141,6 +141,29 @@ def test_missing_library_fails_loudly(tmp_path):
     assert res.returncode != 0 and "not built" in res.stderr
 
 
+def test_build_runs_on_a_tree_without_the_library(tmp_path):
+    """build() must reach the compiler on a fresh checkout, where no libdmc.so exists yet.
+
+    A stand-in hipcc writes an empty file, so the build "succeeds" and only the final import
+    (loading that empty file) fails: "built" must be printed before it.
+    """
+    for item in ("__graft_entry__.py", "include", "paper_2403_09636_amd"):
+        src = os.path.join(ROOT, item)
+        if os.path.isdir(src):
+            shutil.copytree(src, tmp_path / item,
+                            ignore=shutil.ignore_patterns("*.so", "__pycache__"))
+        else:
+            shutil.copy(src, tmp_path / item)
+    fake = tmp_path / "rocm" / "bin"
+    fake.mkdir(parents=True)
+    (fake / "hipcc").write_text('#!/bin/sh\nwhile [ "$1" != "-o" ]; do shift; done\n: > "$2"\n')
+    (fake / "hipcc").chmod(0o755)
+    env = dict(os.environ, ROCM_PATH=str(tmp_path / "rocm"))
+    res = subprocess.run([sys.executable, "-c", "import __graft_entry__ as g; g.build()"],
+                         cwd=tmp_path, env=env, capture_output=True, text=True)
+    assert "built " in res.stdout, res.stdout + res.stderr
+
+
 def test_train_config_struct_matches_header(P):
     text = open(HEADER).read()
     body = re.search(r"typedef struct dmc_train_config \{(.*?)\} dmc_train_config;", text, re.S)
