@@ -18,6 +18,7 @@
 // attention, balanced by actual compressed length) plus a small combine
 // launch for units split over several pieces.
 #include "dmc_device.h"
+#include "dmc_mfma.h"
 
 namespace dmc {
 namespace {
@@ -581,17 +582,43 @@ __device__ __forceinline__ float window_mean_lds(const DecodeParams &p, int u, i
 // transposed (V^T: d rows of page_size slots) so that slice of V^T is one
 // 16-byte load.  P enters the value product rounded to bf16; its row sum is
 // taken over the same rounded values.
+//
+// Chunks stream through LDS: each wave owns one chunk-sized LDS slot (keys,
+// then V^T), filled by direct global-to-LDS transfers.  The wave copies a
+// landed chunk into its operand registers, then issues the next chunk's
+// transfers before computing on the registers, so a whole chunk (16 KB at
+// d = 128) is in flight while one is consumed.  Rows are stored with their
+// 16-byte pieces XOR-permuted so that the operand reads of 16 consecutive
+// lanes (16 rows at one column) hit distinct bank groups.
 // ---------------------------------------------------------------------------
+// Key row r of a chunk: 16-byte piece c sits at position c ^ key_perm(r).
+template <int CPR>
+__device__ __forceinline__ int key_perm(int r) {
+  return CPR == 16 ? ((r & 3) | (((r >> 3) & 3) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 3) << 1));
+}
+// V^T row r (64 bytes: 32 slots): piece c sits at position c ^ ((r >> 2) & 3).
+
+template <int D>
+constexpr int mfma_ring_bytes() { return kWaves * 2 * 32 * D * 2; }
+// Per-wave staging rows of the owner's current key and value (after the ring).
+template <int D>
+constexpr int mfma_stage_bytes() { return kWaves * 2 * D * 2; }
+
 template <int D, int G, bool WIN>
 __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
   constexpr int NT = D / 16;      // 16-dim tiles of the value product
   constexpr int RB = D * 2;       // bytes per key row
+  constexpr int CPR = RB / 16;    // 16-byte pieces per key row
+  constexpr int CH = 32 * RB;     // bytes of a chunk's keys (and of its V^T)
+  constexpr int NX = CH / 1024;   // 1-KB wave transfers per half chunk
   constexpr int REC = D + 4;      // partial record: m, l, -, -, acc[D]
   static_assert(G >= 4 && G <= 16, "query group");
+  static_assert(CPR == 8 || CPR == 16, "head dim");
 
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_wsum[kWaves];
+  __shared__ __align__(16) unsigned char s_ring[mfma_ring_bytes<D>() + mfma_stage_bytes<D>()];
   const int U = p.units;
   int *s_off = reinterpret_cast<int *>(smem);
   const size_t win_lds_off = align_up(size_t(U + 1) * 4, 16);   // windowed means, 2 D fp32 per wave
@@ -658,8 +685,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
         float mc = sv[0];
 #pragma unroll
         for (int j = 1; j < 8; ++j) mc = fmaxf(mc, sv[j]);
-        mc = fmaxf(mc, __shfl_xor(mc, 16, 64));
-        mc = fmaxf(mc, __shfl_xor(mc, 32, 64));
+        mc = max_halves(max_rows16(mc));   // lane swaps, no LDS traffic
         const float mn = fmaxf(m, mc);
         if (vbits == 0u) return;
         const float f = fast_exp2(m - mn);
@@ -690,30 +716,67 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
         }
       };
 
+      // Owner inputs are issued before the stream so that they arrive while it runs:
+      // k_t[0], q_t[0] of the deciding heads, z, the open slot's page, and the current
+      // key and value rows (copied into this wave's staging rows).
+      float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
+      int open_page = -1;
+      const unsigned char *lst = s_ring + mfma_ring_bytes<D>() + wave * 2 * RB;
+      if (owner) {
+        const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
+        k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
+        q0 = load_elem<2>(p.q, int64_t(b * p.hq + dg * G) * D);
+        if (l > 0) {
+          zold = p.z[u];
+          open_page = p.ptab[pt + ((l - 1) >> p.log2p)];
+        }
+        const uint32_t st = __builtin_amdgcn_readfirstlane(lds_offset(lst));
+        if (lane < RB / 16) {
+          dma16_s(st, uniform_ptr(static_cast<const char *>(p.k) + int64_t(u) * RB), lane * 16);
+          dma16_s(st + RB, uniform_ptr(static_cast<const char *>(p.v) + int64_t(u) * RB), lane * 16);
+        }
+      }
+
+      const unsigned char *lk = s_ring + wave * 2 * CH, *lv = lk + CH;
+      const int c_last = end > start ? (end - 1) >> 5 : -1;   // chunk left in the slot
       if (end > start) {
-        const int c0 = start >> 5, c1 = (end - 1) >> 5;
+        const int c0 = start >> 5, c1 = c_last;
         auto range_of = [&](int ch, int &rlo, int &rhi) {
           const int row0 = ch << 5;
           rlo = max(start, row0) - row0;
           rhi = min(end, row0 + 32) - row0;
         };
-        auto issue_k = [&](int ch, uint4 (&ka)[2][KS]) {
-          int rlo, rhi;
-          range_of(ch, rlo, rhi);
-          const char *pg = p.pool + int64_t(p.ptab[pt + ((ch << 5) >> p.log2p)]) * p.page_bytes;
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-            const int rr = min(max(krow + 4 * t, rlo), rhi - 1);
-            const char *kr = pg + int64_t(rr) * RB + q * 16;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) ka[t][ks] = ld16_stream(kr + ks * 64);
+        // The whole chunk (one page: P == 32) is transferred; rows outside
+        // [start, end) are page memory of this unit whose scores and values
+        // the validity bits mask.
+        const uint32_t slot_k =
+            __builtin_amdgcn_readfirstlane(lds_offset(s_ring) + wave * 2 * CH);
+        const uint32_t slot_v = slot_k + CH;
+        // Page-table entries of the piece's chunks, one per lane, 64 chunks per batch with the
+        // next batch loaded one batch ahead: no chunk transfer waits on a table lookup.
+        int cb = c0;
+        int pcur = p.ptab[pt + min(c0 + lane, c1)];
+        int pnxt = p.ptab[pt + min(c0 + 64 + lane, c1)];
+        auto page_of = [&](int ch) -> int {
+          if (ch - cb >= 64) {
+            cb += 64;
+            pcur = pnxt;
+            pnxt = p.ptab[pt + min(cb + 64 + lane, c1)];
           }
+          return __builtin_amdgcn_readlane(pcur, ch - cb);
         };
-        auto issue_v = [&](int ch, uint4 (&va)[NT]) {
-          const char *pg = p.pool + int64_t(p.ptab[pt + ((ch << 5) >> p.log2p)]) * p.page_bytes;
-          const char *vtp = pg + int64_t(P) * RB + (8 * q) * 2;
+        auto issue = [&](int ch) {
+          const char *pg = uniform_ptr(p.pool + int64_t(page_of(ch)) * p.page_bytes);
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) va[nt] = ld16_stream(vtp + int64_t(16 * nt + n) * P * 2);
+          for (int i = 0; i < NX; ++i) {
+            const int o = 1024 * i + 16 * lane, r = o / RB, c = (o % RB) / 16;
+            dma16_s(slot_k + 1024 * i, pg, uint32_t(r * RB + 16 * (c ^ key_perm<CPR>(r))));
+          }
+#pragma unroll
+          for (int i = 0; i < NX; ++i) {
+            const int r = 16 * i + (lane >> 2), c = lane & 3;
+            dma16_s(slot_v + 1024 * i, pg + CH, uint32_t(r * 64 + 16 * (c ^ ((r >> 2) & 3))));
+          }
         };
         auto bits = [&](int ch) -> uint32_t {
           int rlo, rhi;
@@ -721,46 +784,66 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
           const uint32_t hi_mask = rhi >= 32 ? 0xffffffffu : ((1u << rhi) - 1u);
           return hi_mask & ~((1u << rlo) - 1u);
         };
-        // One operand set; the next chunk's keys load during this chunk's
-        // softmax and value product, its values during the next score product.
         uint4 ka[2][KS], va[NT];
-        issue_k(c0, ka);
-        issue_v(c0, va);
+        issue(c0);
         for (int ch = c0; ch <= c1; ++ch) {
+          wait_vmcnt<0>();     // this chunk has landed in the slot
+          wave_lds_sync();
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const int rr = krow + 4 * t;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+              ka[t][ks] = *reinterpret_cast<const uint4 *>(
+                  lk + rr * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(rr)));
+          }
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            va[nt] = *reinterpret_cast<const uint4 *>(lv + (16 * nt + n) * 64 +
+                                                      16 * (q ^ ((n >> 2) & 3)));
+          if (ch < c1) {
+            wave_lds_sync();   // the slot's reads are done before it is refilled
+            issue(ch + 1);
+          }
           float sraw[8];
           scores(ka, sraw);
-          if (ch < c1) issue_k(ch + 1, ka);
           values(sraw, va, bits(ch));
-          if (ch < c1) issue_v(ch + 1, va);
         }
       }
 
-      // Owner: Algorithm 1 loads (issued after the stream to keep registers free).
-      float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
-      int open_page = -1, seg_len = 0;
+      // Owner: the current rows from the staging area; the open slot from the chunk
+      // left in the slot when it is the open slot's page, else from its page.
+      int seg_len = 0;
       uint4 kt[KS], ko[KS];
       uint16_t vt[NT], vo[NT];
       if (owner) {
-        const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
         if (WIN && l > 0) seg_len = p.win.seg_len[u];
-        k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
-        q0 = load_elem<2>(p.q, int64_t(b * p.hq + dg * G) * D);
-        const char *kp = static_cast<const char *>(p.k) + int64_t(u) * RB;
-        const uint16_t *vp = static_cast<const uint16_t *>(p.v) + int64_t(u) * D;
+        wait_vmcnt<0>();
+        wave_lds_sync();
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kt[ks] = ld16(kp + ks * 64 + q * 16);
+        for (int ks = 0; ks < KS; ++ks) kt[ks] = *reinterpret_cast<const uint4 *>(lst + ks * 64 + q * 16);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) vt[nt] = vp[16 * nt + n];
+        for (int nt = 0; nt < NT; ++nt)
+          vt[nt] = *reinterpret_cast<const uint16_t *>(lst + RB + (16 * nt + n) * 2);
         if (l > 0) {
-          zold = p.z[u];
-          open_page = p.ptab[pt + ((l - 1) >> p.log2p)];
-          const char *pg = p.pool + int64_t(open_page) * p.page_bytes;
           const int so = (l - 1) & (P - 1);
+          if (((l - 1) >> 5) == c_last) {
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) ko[ks] = ld16(pg + int64_t(so) * RB + ks * 64 + q * 16);
-          const uint16_t *vtp = reinterpret_cast<const uint16_t *>(pg + int64_t(P) * RB);
+            for (int ks = 0; ks < KS; ++ks)
+              ko[ks] = *reinterpret_cast<const uint4 *>(
+                  lk + so * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(so)));
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) vo[nt] = vtp[(16 * nt + n) * P + so];
+            for (int nt = 0; nt < NT; ++nt)
+              vo[nt] = *reinterpret_cast<const uint16_t *>(
+                  lv + (16 * nt + n) * 64 + 16 * ((so >> 3) ^ ((n >> 2) & 3)) + (so & 7) * 2);
+          } else {
+            const char *pg = p.pool + int64_t(open_page) * p.page_bytes;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) ko[ks] = ld16(pg + int64_t(so) * RB + ks * 64 + q * 16);
+            const uint16_t *vtp = reinterpret_cast<const uint16_t *>(pg + int64_t(P) * RB);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) vo[nt] = vtp[(16 * nt + n) * P + so];
+          }
         } else {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) ko[ks] = zero4;
@@ -1573,6 +1656,12 @@ template <int ES, int D, int G>
 hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) {
   const size_t lds = decode_lds_bytes(p.units, G, D, p.win.window > 0);
   if (vt && !(ES == 2 && G >= 4)) return hipErrorInvalidValue;
+  // The matrix-core kernel adds its chunk ring to the LDS of a workgroup.  When
+  // two such workgroups no longer fit a compute unit (large unit counts), the
+  // grid is halved so that every workgroup is resident at once.
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  if (vt && 2 * (lds + mfma_ring_bytes<D>() + mfma_stage_bytes<D>() + 64) > kLdsPerCu && grid > 1)
+    grid /= 2;
   if (p.win.window > 0)
     launch_decode_kernel<ES, D, G, true>(p, grid, vt, lds, s);
   else

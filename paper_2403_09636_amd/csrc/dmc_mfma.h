@@ -101,6 +101,15 @@ __device__ __forceinline__ float max_halves(float x) {
                __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
 }
 
+// Maximum of x over lanes l and l ^ 16 (v_permlane16_swap of x with itself
+// leaves rows 0/2 in one result and rows 1/3 in the other).  No LDS access.
+__device__ __forceinline__ float max_rows16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x),
+                                                  __builtin_bit_cast(unsigned, x), false, false);
+  return fmaxf(__builtin_bit_cast(float, static_cast<unsigned>(r[0])),
+               __builtin_bit_cast(float, static_cast<unsigned>(r[1])));
+}
+
 // Two floats -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
   typedef float f2_t __attribute__((ext_vector_type(2)));
