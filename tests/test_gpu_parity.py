@@ -207,6 +207,34 @@ def test_import_export_roundtrip(torch_cuda, G, d):
     pr.ok()
 
 
+@pytest.mark.parametrize("G", [1, 8])
+def test_decode_many_pieces_per_unit(torch_cuda, G):
+    """About 100 slots per wave of the full decode grid (512 units of 260-560
+    slots), so most units are cut into four or five pieces whose partial
+    records the combine merges.  Every unit's output, slot index, length and
+    slots are checked over several steps.  G = 1 runs the vector-ALU kernel,
+    G = 8 the matrix-core kernel."""
+    import torch
+    B, Hkv, d = (16, 32, 64) if G == 1 else (64, 8, 64)
+    log(f"case many pieces per unit G={G} units={B * Hkv}")
+    rng = np.random.default_rng(77 + G)
+    lens = rng.integers(260, 560, size=(B, Hkv)).astype(np.int32)
+    lens[0, 0], lens[-1, -1] = 1, 0                     # a one-slot and an empty unit
+    dense, steps = int(lens.max()), 4
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=dense + steps)
+    K = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    V = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    K[..., 0] = 0                                        # stored keys have element 0 cleared
+    z = torch.rand((B, Hkv)).cuda() * 3 + 0.1
+    pr.gpu.import_(0, K, V, torch.from_numpy(lens).cuda(), z)
+    pr.orc.load(0, f64(K), f64(V), lens, f64(z))
+    cr = rng.choice([1.0, 2.0, 4.0], size=Hkv)
+    for _ in range(steps):
+        pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, cr, "bf16", "cuda"))
+    pr.compare_cache(0)
+    pr.ok()
+
+
 def test_pool_exhaustion_sets_flag(torch_cuda):
     """A pool too small for the appends: the device flag reports
     DMC_ERR_CAPACITY, every page is used, nothing is written out of bounds
