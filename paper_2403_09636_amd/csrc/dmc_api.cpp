@@ -64,6 +64,7 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 constexpr int kDecodeWgPerCu = DMC_DECODE_WG_PER_CU;
 constexpr int64_t kMaxDecodeWaves = 8192;
 constexpr size_t kMaxDecodeLds = 64 * 1024;
+constexpr size_t kMaxLdsPerWorkgroup = 160 * 1024;   // gfx950
 
 int elem_bytes(const dmc_cache_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
 
@@ -103,7 +104,10 @@ dmc_status validate_config(const dmc_cache_config *c) {
     return fail(DMC_ERR_INVALID_ARG, "max_prompt_len must be in [0, max_slots_per_seq]");
   const int64_t units = int64_t(c->batch) * c->num_kv_heads;
   if (units > (int64_t(1) << 20)) return fail(DMC_ERR_UNSUPPORTED, "too many units per layer");
-  if (dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim, c->window > 0) > kMaxDecodeLds)
+  const size_t dyn_lds = dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim, c->window > 0);
+  const bool v_trans = c->dtype == DMC_BF16 && G >= 4 && c->page_size == 32;
+  if (dyn_lds > kMaxDecodeLds ||
+      dyn_lds + dmc::decode_static_lds_bytes(c->head_dim, v_trans) > kMaxLdsPerWorkgroup)
     return fail(DMC_ERR_UNSUPPORTED,
                 "batch * num_kv_heads = %lld units exceed the decode kernel's LDS tile table",
                 static_cast<long long>(units));

@@ -209,5 +209,8 @@ hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt
 // Dynamic LDS bytes of the decode kernel for a unit count / group / head dim
 // (and whether the cache has a window).
 size_t decode_lds_bytes(int units, int group, int head_dim, bool window);
+// Static LDS of the decode kernel that runs such a cache (matrix-core kernel:
+// its chunk ring and staging rows).
+size_t decode_static_lds_bytes(int head_dim, bool v_trans);
 
 }  // namespace dmc

@@ -583,13 +583,15 @@ __device__ __forceinline__ float window_mean_lds(const DecodeParams &p, int u, i
 // 16-byte load.  P enters the value product rounded to bf16; its row sum is
 // taken over the same rounded values.
 //
-// Chunks stream through LDS: each wave owns one chunk-sized LDS slot (keys,
+// Chunks stream through LDS: each wave owns two chunk-sized LDS slots (keys,
 // then V^T), filled by direct global-to-LDS transfers.  The wave copies a
-// landed chunk into its operand registers, then issues the next chunk's
-// transfers before computing on the registers, so a whole chunk (16 KB at
-// d = 128) is in flight while one is consumed.  Rows are stored with their
-// 16-byte pieces XOR-permuted so that the operand reads of 16 consecutive
-// lanes (16 rows at one column) hit distinct bank groups.
+// landed chunk into its operand registers and refills that slot with the
+// chunk two ahead before computing on the registers, so two chunks (32 KB at
+// d = 128) are in flight while one is consumed.  The ring takes 128 KB of LDS
+// at d = 128, so one workgroup (one wave per SIMD) runs on a compute unit.
+// Rows are stored with their 16-byte pieces XOR-permuted so that the operand
+// reads of 16 consecutive lanes (16 rows at one column) hit distinct bank
+// groups.
 // ---------------------------------------------------------------------------
 // Key row r of a chunk: 16-byte piece c sits at position c ^ key_perm(r).
 template <int CPR>
@@ -599,7 +601,7 @@ __device__ __forceinline__ int key_perm(int r) {
 // V^T row r (64 bytes: 32 slots): piece c sits at position c ^ ((r >> 2) & 3).
 
 template <int D>
-constexpr int mfma_ring_bytes() { return kWaves * 2 * 32 * D * 2; }
+constexpr int mfma_ring_bytes() { return kWaves * 2 * 2 * 32 * D * 2; }   // 2 slots per wave
 // Per-wave staging rows of the owner's current key and value (after the ring).
 template <int D>
 constexpr int mfma_stage_bytes() { return kWaves * 2 * D * 2; }
@@ -722,6 +724,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
       float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
       int open_page = -1;
       const unsigned char *lst = s_ring + mfma_ring_bytes<D>() + wave * 2 * RB;
+      const int c_first = start >> 5;
       if (owner) {
         const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
         k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
@@ -737,8 +740,8 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
         }
       }
 
-      const unsigned char *lk = s_ring + wave * 2 * CH, *lv = lk + CH;
       const int c_last = end > start ? (end - 1) >> 5 : -1;   // chunk left in the slot
+      const unsigned char *lk = s_ring + (wave * 2 + ((c_last - c_first) & 1)) * 2 * CH, *lv = lk + CH;
       if (end > start) {
         const int c0 = start >> 5, c1 = c_last;
         auto range_of = [&](int ch, int &rlo, int &rhi) {
@@ -749,9 +752,8 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
         // The whole chunk (one page: P == 32) is transferred; rows outside
         // [start, end) are page memory of this unit whose scores and values
         // the validity bits mask.
-        const uint32_t slot_k =
-            __builtin_amdgcn_readfirstlane(lds_offset(s_ring) + wave * 2 * CH);
-        const uint32_t slot_v = slot_k + CH;
+        const uint32_t slot_k0 =
+            __builtin_amdgcn_readfirstlane(lds_offset(s_ring) + wave * 4 * CH);
         // Page-table entries of the piece's chunks, one per lane, 64 chunks per batch with the
         // next batch loaded one batch ahead: no chunk transfer waits on a table lookup.
         int cb = c0;
@@ -765,7 +767,8 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
           }
           return __builtin_amdgcn_readlane(pcur, ch - cb);
         };
-        auto issue = [&](int ch) {
+        auto issue = [&](int ch, int sl) {
+          const uint32_t slot_k = slot_k0 + sl * 2 * CH, slot_v = slot_k + CH;
           const char *pg = uniform_ptr(p.pool + int64_t(page_of(ch)) * p.page_bytes);
 #pragma unroll
           for (int i = 0; i < NX; ++i) {
@@ -785,25 +788,29 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
           return hi_mask & ~((1u << rlo) - 1u);
         };
         uint4 ka[2][KS], va[NT];
-        issue(c0);
+        issue(c0, 0);
+        if (c0 < c1) issue(c0 + 1, 1);
         for (int ch = c0; ch <= c1; ++ch) {
-          wait_vmcnt<0>();     // this chunk has landed in the slot
+          const int sl = (ch - c0) & 1;
+          if (ch < c1) wait_vmcnt<2 * NX>();   // this chunk has landed; the next may be in flight
+          else wait_vmcnt<0>();
           wave_lds_sync();
+          const unsigned char *ck = s_ring + (wave * 2 + sl) * 2 * CH, *cv = ck + CH;
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             const int rr = krow + 4 * t;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
               ka[t][ks] = *reinterpret_cast<const uint4 *>(
-                  lk + rr * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(rr)));
+                  ck + rr * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(rr)));
           }
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt)
-            va[nt] = *reinterpret_cast<const uint4 *>(lv + (16 * nt + n) * 64 +
+            va[nt] = *reinterpret_cast<const uint4 *>(cv + (16 * nt + n) * 64 +
                                                       16 * (q ^ ((n >> 2) & 3)));
-          if (ch < c1) {
+          if (ch + 2 <= c1) {
             wave_lds_sync();   // the slot's reads are done before it is refilled
-            issue(ch + 1);
+            issue(ch + 2, sl);
           }
           float sraw[8];
           scores(ka, sraw);
@@ -1657,8 +1664,8 @@ hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) 
   const size_t lds = decode_lds_bytes(p.units, G, D, p.win.window > 0);
   if (vt && !(ES == 2 && G >= 4)) return hipErrorInvalidValue;
   // The matrix-core kernel adds its chunk ring to the LDS of a workgroup.  When
-  // two such workgroups no longer fit a compute unit (large unit counts), the
-  // grid is halved so that every workgroup is resident at once.
+  // two such workgroups do not fit a compute unit (always at d = 128), the grid
+  // is halved so that every workgroup is resident at once.
   constexpr size_t kLdsPerCu = 160 * 1024;
   if (vt && 2 * (lds + mfma_ring_bytes<D>() + mfma_stage_bytes<D>() + 64) > kLdsPerCu && grid > 1)
     grid /= 2;
@@ -1745,6 +1752,12 @@ size_t decode_lds_bytes(int units, int group, int head_dim, bool window) {
   // slot-space prefix [units + 1]; with a window, 2 * head_dim fp32 per wave
   // for the matrix-core decode's windowed means
   return align_up(size_t(units + 1) * 4, 16) + (window ? size_t(kWaves) * 2 * head_dim * 4 : 0);
+}
+
+size_t decode_static_lds_bytes(int head_dim, bool v_trans) {
+  if (!v_trans) return 64;
+  return head_dim == 128 ? mfma_ring_bytes<128>() + mfma_stage_bytes<128>() + 64
+                         : mfma_ring_bytes<64>() + mfma_stage_bytes<64>() + 64;
 }
 
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s) {

@@ -79,6 +79,19 @@ def test_too_many_units_for_decode_table(P):
     assert "units" in P.binding.last_error()
 
 
+def test_matrix_core_cache_unit_limit(P):
+    """bf16 grouped-query caches (G >= 4, 32-slot pages) decode with a 128 KB
+    chunk ring in LDS at d = 128, which leaves room for the slot-space table of
+    about 7600 units; the same shapes in fp32 run the vector kernel."""
+    ok = P.make_config(1, 950, 64, 8, 128, "bf16")        # 7600 units
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(ok)) > 0
+    big = P.make_config(1, 1024, 64, 8, 128, "bf16")      # 8192 units
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(big)) == 0
+    assert "units" in P.binding.last_error()
+    vec = P.make_config(1, 1024, 64, 8, 128, "fp32")
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(vec)) > 0
+
+
 def test_alloc_rejects_before_hip(P):
     lib = P.binding.lib
     cfg = P.make_config(1, 2, 2, 2, 64, max_slots_per_seq=64)
