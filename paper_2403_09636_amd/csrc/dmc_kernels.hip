@@ -1036,6 +1036,42 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int b
   const int u = b * p.hkv + g;
   const int first = p.meta[2 * u], nt = p.meta[2 * u + 1];   // records first .. first+nt-1
   if (nt <= 1) return;
+  if (nt <= 4) {
+    // Few records (the usual case): every load is issued at once, one round trip.
+    float mi[4], li[4], a[4][E];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      mi[i] = neg_inf();
+      li[i] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) a[i][e] = 0.0f;
+      if (i < nt) {
+        const float *rec = p.partials + (int64_t(first + i) * G + hg) * REC;
+        mi[i] = rec[0];
+        li[i] = rec[1];
+#pragma unroll
+        for (int e = 0; e < E; ++e) a[i][e] = rec[4 + lane * E + e];
+      }
+    }
+    const float M = fmaxf(fmaxf(mi[0], mi[1]), fmaxf(mi[2], mi[3]));
+    float L = 0.0f, A[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) A[e] = 0.0f;
+    if (M != neg_inf()) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float w = mi[i] == neg_inf() ? 0.0f : fast_exp2(mi[i] - M);
+        L = fmaf(w, li[i], L);
+#pragma unroll
+        for (int e = 0; e < E; ++e) A[e] = fmaf(w, a[i][e], A[e]);
+      }
+    }
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) A[e] *= inv;
+    store_e<ES, E>(static_cast<char *>(p.out) + (int64_t(bh) * D + lane * E) * ES, A);
+    return;
+  }
   float L = 0.0f, A[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) A[e] = 0.0f;
