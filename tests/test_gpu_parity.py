@@ -277,6 +277,30 @@ def test_bad_import_length_sets_flag(torch_cuda):
     assert pr.gpu.lengths(0).cpu().numpy().tolist() == [[3, 0]]
 
 
+def test_largest_matrix_core_unit_table(torch_cuda):
+    """Grouped-query bf16 caches decode on matrix cores with a 128 KB chunk ring
+    in LDS at d = 128; the largest accepted slot-space table (7600 units) fills
+    the rest of the compute unit's LDS.  Imported caches of 40-70 slots (two or
+    three pages per unit), three steps, every unit against the oracle."""
+    import torch
+    log("case largest matrix-core unit table")
+    B, Hkv, G, d, steps = 950, 8, 8, 128, 3
+    rng = np.random.default_rng(78)
+    lens = rng.integers(40, 71, size=(B, Hkv)).astype(np.int32)
+    dense = int(lens.max())
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=dense + steps)
+    K = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    V = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    K[..., 0] = 0
+    z = torch.rand((B, Hkv)).cuda() * 3 + 0.1
+    pr.gpu.import_(0, K, V, torch.from_numpy(lens).cuda(), z)
+    pr.orc.load(0, f64(K), f64(V), lens, f64(z))
+    for _ in range(steps):
+        pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, np.full(Hkv, 2.0), "bf16", "cuda"))
+    pr.compare_cache(0)
+    pr.ok()
+
+
 def test_largest_unit_table(torch_cuda):
     """batch * kv heads near the decode kernel's LDS slot-table limit (64 KB):
     16000 units of one query head each, a few steps from empty, against the
