@@ -773,12 +773,12 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
 #pragma unroll
           for (int i = 0; i < NX; ++i) {
             const int o = 1024 * i + 16 * lane, r = o / RB, c = (o % RB) / 16;
-            dma16_s(slot_k + 1024 * i, pg, uint32_t(r * RB + 16 * (c ^ key_perm<CPR>(r))));
+            dma16_s_nt(slot_k + 1024 * i, pg, uint32_t(r * RB + 16 * (c ^ key_perm<CPR>(r))));
           }
 #pragma unroll
           for (int i = 0; i < NX; ++i) {
             const int r = 16 * i + (lane >> 2), c = lane & 3;
-            dma16_s(slot_v + 1024 * i, pg + CH, uint32_t(r * 64 + 16 * (c ^ ((r >> 2) & 3))));
+            dma16_s_nt(slot_v + 1024 * i, pg + CH, uint32_t(r * 64 + 16 * (c ^ ((r >> 2) & 3))));
           }
         };
         auto bits = [&](int ch) -> uint32_t {

@@ -62,6 +62,15 @@ __device__ __forceinline__ void dma16_s(uint32_t lds_base, const char *sbase, ui
                : "memory");
 }
 
+// dma16_s with the nontemporal policy, for data streamed once (no reuse
+// through the caches).
+__device__ __forceinline__ void dma16_s_nt(uint32_t lds_base, const char *sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory");
+}
+
 // A wave-uniform pointer, made visibly uniform (SGPRs) for dma16_s.
 __device__ __forceinline__ const char *uniform_ptr(const char *ptr) {
   const uint64_t x = reinterpret_cast<uint64_t>(ptr);
