@@ -132,6 +132,25 @@ __device__ __forceinline__ void load_e(const char *p, float *f) {
     f[0] = load_elem<ES>(p, 0);
   }
 }
+// load_e with the nontemporal policy, for data read once (prompt rows).
+template <int ES, int E>
+__device__ __forceinline__ void load_e_nt(const char *p, float *f) {
+  if constexpr (ES == 2 && E == 2) {
+    const uint32_t w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+    f[0] = __uint_as_float(w << 16);
+    f[1] = __uint_as_float(w & 0xffff0000u);
+  } else if constexpr (ES == 4 && E == 2) {
+    typedef float f2_t __attribute__((ext_vector_type(2)));
+    const f2_t w = __builtin_nontemporal_load(reinterpret_cast<const f2_t *>(p));
+    f[0] = w.x;
+    f[1] = w.y;
+  } else if constexpr (ES == 2) {
+    f[0] = __uint_as_float(uint32_t(__builtin_nontemporal_load(reinterpret_cast<const uint16_t *>(p)))
+                           << 16);
+  } else {
+    f[0] = __builtin_nontemporal_load(reinterpret_cast<const float *>(p));
+  }
+}
 template <int ES, int E>
 __device__ __forceinline__ void store_e(char *p, const float *f) {
   if constexpr (ES == 2 && E == 2) {

@@ -1355,8 +1355,8 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
 #pragma unroll
     for (int j = 0; j < kRows; ++j) {
       const int tj = t2 + min(j, cnt - 1);
-      load_e<ES, E>(kbase + tj * kst, kk[j]);
-      load_e<ES, E>(vbase + tj * vst, vv[j]);
+      load_e_nt<ES, E>(kbase + tj * kst, kk[j]);   // prompt rows are read once
+      load_e_nt<ES, E>(vbase + tj * vst, vv[j]);
       ww[j] = om[tj];
     }
 #pragma unroll
