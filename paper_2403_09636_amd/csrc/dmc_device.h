@@ -164,6 +164,17 @@ __device__ __forceinline__ void store_e(char *p, const float *f) {
   }
 }
 
+// store_e with the nontemporal policy, for rows written once and read much later.
+template <int ES, int E>
+__device__ __forceinline__ void store_e_nt(char *p, const float *f) {
+  if constexpr (ES == 2 && E == 2) {
+    __builtin_nontemporal_store(bf16_bits(f[0]) | (bf16_bits(f[1]) << 16),
+                                reinterpret_cast<uint32_t *>(p));
+  } else {
+    store_e<ES, E>(p, f);
+  }
+}
+
 __device__ __forceinline__ float sigmoid_floor(float x) {
   // omega = sigmoid(x), floored at 2^-100 so a running sum never reaches 0.
   return fmaxf(1.0f / (1.0f + expf(-x)), 0x1p-100f);

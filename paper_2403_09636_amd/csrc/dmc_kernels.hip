@@ -1344,8 +1344,8 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
     }
     char *row = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB +
                 lane * E * ES;
-    store_e<ES, E>(row, kq);
-    store_e<ES, E>(row + int64_t(P) * RB, vq);
+    store_e_nt<ES, E>(row, kq);
+    store_e_nt<ES, E>(row + int64_t(P) * RB, vq);
     if (lane == 0 && (s & (P - 1)) == 0)
       p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)] = pb + (s >> p.log2p);
   };
