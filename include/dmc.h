@@ -190,7 +190,12 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer,
  *   k_dev, v_dev: [B, Hkv, d] contiguous, 16-byte aligned.
  *   out_dev: [B, Hq, d] contiguous, 16-byte aligned, written.
  *   slot_index_dev: optional int32 [B, Hkv]: slot index the token went to
- *     (-1 when it was dropped for lack of capacity). */
+ *     (-1 when it was dropped for lack of capacity).
+ * The call only enqueues kernels on `stream` (no allocation, no host
+ * synchronisation), so it can be captured in a HIP graph.  Each call reads the
+ * layer's lengths from one of two buffers and writes the other, and a captured
+ * call keeps the buffers of its capture, so a graph meant for repeated replay
+ * holds an even number of steps per layer. */
 dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q_dev,
                            const void *k_dev, const void *v_dev, void *out_dev,
                            int32_t *slot_index_dev, dmc_stream_t stream);
