@@ -1501,8 +1501,8 @@ __global__ __launch_bounds__(kThreads) void prefill_window_kernel(PrefillParams 
     }
     char *row = p.pool + int64_t(pb + (sl >> p.log2p)) * p.page_bytes + int64_t(sl & (P - 1)) * RB +
                 lane * E * ES;
-    store_e<ES, E>(row, kq);
-    store_e<ES, E>(row + int64_t(P) * RB, vq);
+    store_e_nt<ES, E>(row, kq);
+    store_e_nt<ES, E>(row + int64_t(P) * RB, vq);
     if (lane == 0 && (sl & (P - 1)) == 0)
       p.ptab[int64_t(u) * p.maxpages + (sl >> p.log2p)] = pb + (sl >> p.log2p);
   };
@@ -1513,8 +1513,8 @@ __global__ __launch_bounds__(kThreads) void prefill_window_kernel(PrefillParams 
 #pragma unroll
     for (int j = 0; j < kRows; ++j) {
       tk[j] = s_list[wave][i0 + min(j, cnt - 1)];
-      load_e<ES, E>(kbase + tk[j] * kst, kk[j]);
-      load_e<ES, E>(vbase + tk[j] * vst, vv[j]);
+      load_e_nt<ES, E>(kbase + tk[j] * kst, kk[j]);   // prompt rows are read once
+      load_e_nt<ES, E>(vbase + tk[j] * vst, vv[j]);
       ww[j] = om[tk[j]];
     }
 #pragma unroll
