@@ -47,6 +47,8 @@ def parse():
                     help="window-grouping width (Sec. 3.3); prefilled workloads only")
     ap.add_argument("--calib-copy", action="store_true",
                     help="finish with plain 1 GiB device copies (counter calibration)")
+    ap.add_argument("--sources-digest", action="store_true",
+                    help="print the digest of the decode kernels' sources and exit")
     return ap.parse_args()
 
 
@@ -106,12 +108,27 @@ def windowed_prompt_reads(k0, window):
     return int((pos_from_end < window).sum())
 
 
-def profiled_traffic(workload):
-    """Calibrated HBM bytes per launch from the committed rocprofv3 counter
-    summary, or None when the kernel source changed since it was taken."""
+# Every source the decode kernels are compiled from: the counter figures in
+# profiles/ hold for this exact set of files.
+KERNEL_SOURCES = ("dmc_kernels.hip", "dmc_device.h", "dmc_mfma.h", "dmc_internal.h")
+
+
+def kernel_sources_digest():
+    """sha256 over the decode kernels' sources (name, then bytes, in order)."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload}_counters.txt")
-    src = os.path.join(ROOT, "paper_2403_09636_amd", "csrc", "dmc_kernels.hip")
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(name.encode() + b"\0")
+        h.update(open(os.path.join(ROOT, "paper_2403_09636_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload, window=0):
+    """Calibrated HBM bytes per launch from the committed rocprofv3 counter
+    summary of this workload (and window), or None when any kernel source
+    changed since the counters were taken."""
+    suffix = f"_w{window}" if window else ""
+    path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload}{suffix}_counters.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -119,8 +136,7 @@ def profiled_traffic(workload):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if kv.get("kernel_source_sha256") != sha:
+    if kv.get("kernel_sources_sha256") != kernel_sources_digest():
         return None
     return int(kv["traffic_bytes_per_launch"])
 
@@ -430,6 +446,9 @@ def bench_train(args, pool=None):
 
 def main():
     args = parse()
+    if args.sources_digest:
+        print(kernel_sources_digest())
+        return
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
               "the decode path shards by kv head or by sequence, see the design notes",
@@ -602,7 +621,7 @@ def bench_decode(args, pool):
                    "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": profiled_traffic(w.name),
+                     "traffic": profiled_traffic(w.name, args.window),
                      "kernel": "dmc_decode_step (decode_kernel + combine_kernel)",
                      "alg_bytes_per_launch": int(alg_per_launch),
                      "avg_launch_us": round(avg_launch_ms * 1e3, 2)},

@@ -107,19 +107,31 @@ typedef struct dmc_cache_config {
 
 typedef struct dmc_cache dmc_cache; /* opaque host handle */
 
-/* Bytes of device workspace a cache with this configuration needs (page pool,
- * page tables, lengths, z, control words, decode split-K partials and prefill
- * staging).  Returns 0 for an invalid configuration (see dmc_last_error). */
+/* Bytes of device workspace a cache with this configuration needs.  The cache
+ * is the paged storage of Sec. 3.3 (Practical considerations): every
+ * (layer, batch row, kv head) keeps its own variable-length sequence of
+ * slots, held in fixed-size pages taken from one shared pool on demand, with
+ * a per-unit page table -- so the workspace is the page pool, the page
+ * tables, the slot counts and running importance sums z of Algorithm 1, the
+ * control words of the page allocator, and the decode split-K partials and
+ * prefill staging.  Returns 0 for an invalid configuration (see
+ * dmc_last_error). */
 size_t dmc_cache_workspace_bytes(const dmc_cache_config *cfg);
 
-/* Create a cache inside the caller-owned device buffer `workspace_dev` of
+/* Create a cache (the paged per-head storage of Sec. 3.3, every unit empty:
+ * Algorithm 1 starts from an empty cache, so the first token of a unit opens
+ * its first slot) inside the caller-owned device buffer `workspace_dev` of
  * `bytes` bytes (>= dmc_cache_workspace_bytes(cfg), 256-byte aligned, on the
  * current HIP device).  Enqueues the initialisation (all lengths and z zero,
- * empty pool, flags clear) on `stream`.  *out receives the host handle. */
+ * empty pool, flags clear) on `stream`.  *out receives the host handle.
+ * Errors: DMC_ERR_INVALID_ARG for a bad configuration, a NULL or misaligned
+ * workspace, or one smaller than needed (nothing enqueued); DMC_ERR_HIP if
+ * the device query or the initialisation launch fails (*out stays NULL). */
 dmc_status dmc_cache_alloc(const dmc_cache_config *cfg, void *workspace_dev, size_t bytes,
                            dmc_stream_t stream, dmc_cache **out);
 
-/* Release the host handle (the workspace stays the caller's). */
+/* Release the host handle of a paged cache (Sec. 3.3); the workspace and the
+ * pages in it stay the caller's, untouched.  DMC_ERR_INVALID_ARG for NULL. */
 dmc_status dmc_cache_free(dmc_cache *cache);
 
 /* Empty every layer: lengths, z, page pool and flags back to the initial state. */
@@ -192,10 +204,10 @@ dmc_status dmc_prefill_attend(dmc_cache *cache, int32_t layer,
  *   slot_index_dev: optional int32 [B, Hkv]: slot index the token went to
  *     (-1 when it was dropped for lack of capacity).
  * The call only enqueues kernels on `stream` (no allocation, no host
- * synchronisation), so it can be captured in a HIP graph.  Each call reads the
- * layer's lengths from one of two buffers and writes the other, and a captured
- * call keeps the buffers of its capture, so a graph meant for repeated replay
- * holds an even number of steps per layer. */
+ * synchronisation, no memset), so it can be captured in a HIP graph.  Every
+ * call on a layer uses the same device buffers (its last kernel copies the
+ * post-step lengths back into the layer's current-lengths buffer), so a
+ * captured step can be replayed any number of times. */
 dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q_dev,
                            const void *k_dev, const void *v_dev, void *out_dev,
                            int32_t *slot_index_dev, dmc_stream_t stream);

@@ -149,13 +149,6 @@ class LayerCache:
             self.wa = np.zeros((self.U, w), dtype=np.int64)
             self.wn = np.zeros(self.U, dtype=np.int64)   # tokens seen by the unit
 
-    def copy(self):
-        assert not self.window, "copy of a windowed cache is not needed"
-        other = LayerCache(self.U, self.d, self.cap)
-        other.K[:], other.V[:] = self.K, self.V
-        other.l[:], other.z[:] = self.l, self.z
-        return other
-
     def load(self, K, V, lengths, z):
         """Install an existing compressed cache (dense [U, >=max l, d])."""
         assert not self.window, "a windowed cache needs its token window; it is not imported"

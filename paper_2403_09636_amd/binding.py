@@ -136,23 +136,180 @@ def _ptr(t):
     return None if t is None else c_void_p(t.data_ptr())
 
 
+# -- argument validation ------------------------------------------------------
+# The C ABI receives raw pointers and cannot see shapes, dtypes or devices, so
+# everything the header requires of a tensor is checked here, before any call
+# into the library.  Checks run in a fixed order (dtype, shape, layout,
+# alignment, then device), so each rejection can be exercised with CPU tensors.
+
+def _fail(msg):
+    raise DMCError(DMC_ERR_INVALID_ARG, msg)
+
+
+def cache_dtype(cfg):
+    import torch
+    return torch.float32 if cfg.dtype == DMC_FP32 else torch.bfloat16
+
+
+def _check(name, t, dtype, shape=None, contiguous=True, align16=True,
+           last_dim_contiguous=False, stride_mult=None):
+    """Validate one tensor argument (not its device, see _on_device); shape
+    entries of None match any size."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        _fail(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        _fail(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(w is not None and g != w for g, w in zip(t.shape, shape)):
+            want = "[" + ", ".join("*" if w is None else str(w) for w in shape) + "]"
+            _fail(f"{name} has shape {list(t.shape)}, expected {want}")
+    if contiguous and not t.is_contiguous():
+        _fail(f"{name} must be contiguous")
+    if last_dim_contiguous and t.dim() > 0 and t.shape[-1] > 1 and t.stride(-1) != 1:
+        _fail(f"{name} must have a contiguous last dimension")
+    if stride_mult and any(st % stride_mult for st in t.stride()[:-1]):
+        _fail(f"{name} strides {tuple(t.stride())} must be multiples of {stride_mult} elements")
+    if align16 and t.numel() > 0 and t.data_ptr() % 16:
+        _fail(f"{name} must be 16-byte aligned")
+
+
+def _on_device(device, **tensors):
+    """Last check of every entry point: all tensors on the cache's device."""
+    for name, t in tensors.items():
+        if t is not None and t.device != device:
+            _fail(f"{name} is on {t.device}, the cache is on {device}")
+
+
+def check_decode_args(cfg, device, q, k, v, out, slot_index=None):
+    """dmc_decode_step: q, out [B, Hq, d]; k, v [B, Hkv, d]; contiguous, cache
+    dtype, 16-byte aligned; slot_index int32 [B, Hkv]."""
+    import torch
+    dt = cache_dtype(cfg)
+    B, Hq, Hkv, d = cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    _check("q", q, dt, (B, Hq, d))
+    _check("k", k, dt, (B, Hkv, d))
+    _check("v", v, dt, (B, Hkv, d))
+    _check("out", out, dt, (B, Hq, d))
+    if slot_index is not None:
+        _check("slot_index", slot_index, torch.int32, (B, Hkv), align16=False)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if _overlap(out, t):
+            _fail(f"out overlaps {name}")
+    _on_device(device, q=q, k=k, v=v, out=out, slot_index=slot_index)
+
+
+def _overlap(x, y):
+    if x.numel() == 0 or y.numel() == 0:
+        return False
+    x0, x1 = x.data_ptr(), x.data_ptr() + x.numel() * x.element_size()
+    y0, y1 = y.data_ptr(), y.data_ptr() + y.numel() * y.element_size()
+    return x0 < y1 and y0 < x1
+
+
+def check_prefill_args(cfg, device, k, v, q, n, prompt_lens=None, slot_index=None,
+                       full_q=False, out=None):
+    """dmc_prefill_compress / dmc_prefill_attend: k, v [B, >= n, Hkv, d] with a
+    contiguous last dimension and strides that are multiples of 8 elements,
+    16-byte aligned; q [B, >= n, Hq, d] likewise when every element is read
+    (prompt attention, full_q), else [B, >= n, Hq] or [B, >= n, Hq, *] (only
+    element 0 is read); out like q; prompt_lens int32 [B]; slot_index int32
+    [B, Hkv, n] contiguous."""
+    import torch
+    dt = cache_dtype(cfg)
+    B, Hq, Hkv, d = cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    maxn = cfg.max_prompt_len if cfg.max_prompt_len > 0 else cfg.max_slots_per_seq
+    if not 0 <= n <= maxn:
+        _fail(f"prompt length {n} outside [0, {maxn}]")
+    for name, t in (("k", k), ("v", v)):
+        _check(name, t, dt, (B, None, Hkv, d), contiguous=False, last_dim_contiguous=True,
+               stride_mult=8)
+        if t.shape[1] < n:
+            _fail(f"{name} holds {t.shape[1]} tokens, fewer than n = {n}")
+    if full_q:
+        _check("q", q, dt, (B, None, Hq, d), contiguous=False, last_dim_contiguous=True,
+               stride_mult=8)
+    else:
+        if q.dim() == 3:
+            _check("q", q, dt, (B, None, Hq), contiguous=False, align16=False)
+        else:
+            _check("q", q, dt, (B, None, Hq, None), contiguous=False, align16=False)
+    if q.shape[1] < n:
+        _fail(f"q holds {q.shape[1]} tokens, fewer than n = {n}")
+    if out is not None:
+        _check("out", out, dt, (B, None, Hq, d), contiguous=False,
+               last_dim_contiguous=True, stride_mult=8)
+        if out.shape[1] < n:
+            _fail(f"out holds {out.shape[1]} tokens, fewer than n = {n}")
+        for name, t in (("q", q), ("k", k), ("v", v)):
+            if _overlap(out, t):
+                _fail(f"out overlaps {name}")
+    if prompt_lens is not None:
+        _check("prompt_lens", prompt_lens, torch.int32, (B,), align16=False)
+    if slot_index is not None:
+        _check("slot_index", slot_index, torch.int32, (B, Hkv, n), align16=False)
+    _on_device(device, k=k, v=v, q=q, out=out, prompt_lens=prompt_lens, slot_index=slot_index)
+
+
+def check_import_args(cfg, device, K, V, lengths, z):
+    """dmc_cache_import: K, V [B, Hkv, dense_slots, d] contiguous cache dtype,
+    16-byte aligned; lengths int32 [B, Hkv]; z float32 [B, Hkv]."""
+    import torch
+    dt = cache_dtype(cfg)
+    B, Hkv, d = cfg.batch, cfg.num_kv_heads, cfg.head_dim
+    _check("K", K, dt, (B, Hkv, None, d))
+    _check("V", V, dt, (B, Hkv, K.shape[2], d))
+    _check("lengths", lengths, torch.int32, (B, Hkv), align16=False)
+    _check("z", z, torch.float32, (B, Hkv), align16=False)
+    _on_device(device, K=K, V=V, lengths=lengths, z=z)
+
+
+def check_train_args(cfg, device, q, k, v, noise, extra=()):
+    """dmc_train_forward / dmc_train_backward: q-shaped [B, n, Hq, d] and
+    k-shaped [B, n, Hkv, d] tensors contiguous in the config dtype and 16-byte
+    aligned; noise and the per-token fp32 arrays [B, n, Hkv] contiguous.
+    extra: (name, tensor, kind) with kind 'q', 'k' or 'tok' (None tensors skip)."""
+    import torch
+    dt = torch.float32 if cfg.dtype == DMC_FP32 else torch.bfloat16
+    B, n, Hq, Hkv, d = cfg.batch, cfg.seq_len, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    shapes = {"q": (dt, (B, n, Hq, d), True), "k": (dt, (B, n, Hkv, d), True),
+              "tok": (torch.float32, (B, n, Hkv), False)}
+    items = [("q", q, "q"), ("k", k, "k"), ("v", v, "k"), ("noise", noise, "tok"), *extra]
+    for name, t, kind in items:
+        if t is None:
+            continue
+        dtype, shape, a16 = shapes[kind]
+        _check(name, t, dtype, shape, align16=a16)
+    _on_device(device, **{name: t for name, t, _ in items})
+
+
 def _stream(stream):
     import torch
     s = torch.cuda.current_stream() if stream is None else stream
     return c_void_p(s.cuda_stream)
 
 
+def _cuda_device(device):
+    import torch
+    dev = torch.device(device)
+    if dev.type == "cuda" and dev.index is None:
+        dev = torch.device("cuda", torch.cuda.current_device())
+    return dev
+
+
 class DMCCache:
     """A paged DMC cache in one torch-allocated workspace on the current GPU.
 
-    Thin wrapper over the C ABI: shapes and dtypes are checked here only to
-    give Python errors; the library validates everything again.
+    Thin wrapper over the C ABI.  The library checks pointers, alignment,
+    strides, layer and prompt length; the shapes, dtypes, devices and layouts
+    of the tensors, which it cannot see, are checked here before each call
+    (check_*_args), raising DMCError.
     """
 
     def __init__(self, cfg: CacheConfig, device="cuda", stream=None):
         import torch
         self.cfg = cfg
-        self.device = torch.device(device)
+        self.device = _cuda_device(device)
         self.dtype = torch.float32 if cfg.dtype == DMC_FP32 else torch.bfloat16
         self.G = cfg.num_q_heads // cfg.num_kv_heads
         nbytes = workspace_bytes(cfg)
@@ -181,6 +338,7 @@ class DMCCache:
         """Algorithm 1 update + attention for one layer; returns out [B, Hq, d]."""
         if out is None:
             out = torch_empty_like(q)
+        check_decode_args(self.cfg, self.device, q, k, v, out, slot_index)
         check(lib.dmc_decode_step(self.handle, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                   _ptr(slot_index), _stream(stream)))
         return out
@@ -188,6 +346,7 @@ class DMCCache:
     def prefill(self, layer, k, v, q, n=None, prompt_lens=None, slot_index=None, stream=None):
         """Compress a prompt: k, v [B, n, Hkv, d] (strided), q [B, n, Hq, (d)]."""
         n = k.shape[1] if n is None else n
+        check_prefill_args(self.cfg, self.device, k, v, q, n, prompt_lens, slot_index)
         ks = (c_int64 * 3)(k.stride(0), k.stride(1), k.stride(2))
         vs = (c_int64 * 3)(v.stride(0), v.stride(1), v.stride(2))
         qs = (c_int64 * 3)(q.stride(0), q.stride(1), q.stride(2))
@@ -203,6 +362,8 @@ class DMCCache:
             import torch
             out = torch.empty((q.shape[0], n, q.shape[2], q.shape[3]), dtype=q.dtype,
                               device=q.device)
+        check_prefill_args(self.cfg, self.device, k, v, q, n, prompt_lens, slot_index,
+                           full_q=True, out=out)
         ks = (c_int64 * 3)(k.stride(0), k.stride(1), k.stride(2))
         vs = (c_int64 * 3)(v.stride(0), v.stride(1), v.stride(2))
         qs = (c_int64 * 3)(q.stride(0), q.stride(1), q.stride(2))
@@ -232,6 +393,7 @@ class DMCCache:
         return K, V, z
 
     def import_(self, layer, K, V, lengths, z, stream=None):
+        check_import_args(self.cfg, self.device, K, V, lengths, z)
         check(lib.dmc_cache_import(self.handle, layer, _ptr(K), _ptr(V), K.shape[2],
                                    _ptr(lengths), _ptr(z), _stream(stream)))
 
@@ -273,7 +435,8 @@ class DMCTrainer:
         n = lib.dmc_train_workspace_bytes(ctypes.byref(cfg))
         if n == 0:
             raise DMCError(DMC_ERR_INVALID_ARG, last_error())
-        self.workspace = torch.empty(n + 256, dtype=torch.uint8, device=device)
+        self.device = _cuda_device(device)
+        self.workspace = torch.empty(n + 256, dtype=torch.uint8, device=self.device)
         self._ws = c_void_p((self.workspace.data_ptr() + 255) // 256 * 256)
         self._ws_bytes = n
 
@@ -281,6 +444,8 @@ class DMCTrainer:
         """out [B, n, Hq, d] (and alpha [B, n, Hkv] fp32 if given)."""
         if out is None:
             out = torch_empty_like(q)
+        check_train_args(self.cfg, self.device, q, k, v, noise,
+                         (("out", out, "q"), ("alpha", alpha, "tok")))
         check(lib.dmc_train_forward(ctypes.byref(self.cfg), _ptr(q), _ptr(k), _ptr(v), _ptr(noise),
                                     _ptr(out), _ptr(alpha), self._ws, self._ws_bytes,
                                     _stream(stream)))
@@ -292,6 +457,9 @@ class DMCTrainer:
         dq = torch_empty_like(q) if dq is None else dq
         dk = torch_empty_like(k) if dk is None else dk
         dv = torch_empty_like(v) if dv is None else dv
+        check_train_args(self.cfg, self.device, q, k, v, noise,
+                         (("out", out, "q"), ("dout", dout, "q"), ("dalpha", dalpha, "tok"),
+                          ("dq", dq, "q"), ("dk", dk, "k"), ("dv", dv, "k")))
         check(lib.dmc_train_backward(ctypes.byref(self.cfg), _ptr(q), _ptr(k), _ptr(v),
                                      _ptr(noise), _ptr(out), _ptr(dout), _ptr(dalpha), _ptr(dq),
                                      _ptr(dk), _ptr(dv), self._ws, self._ws_bytes,

@@ -27,7 +27,6 @@ struct dmc_cache {
   size_t ws_bytes;
   int device;
   int cu_count;
-  std::vector<uint8_t> parity;  // per layer: which lengths buffer is current
 };
 
 namespace {
@@ -184,8 +183,12 @@ T *at(const dmc_cache *c, size_t off) {
   return reinterpret_cast<T *>(c->ws + off);
 }
 
-int32_t *lens_of(const dmc_cache *c, int layer, int parity) {
-  return at<int32_t>(c, c->lay.lens) + (size_t(parity) * c->cfg.num_layers + layer) * c->lay.units;
+// Lengths of one layer: buffer 0 holds the current slot counts (read by every
+// kernel); buffer 1 receives the post-step counts of a decode step, which the
+// step's combine launch copies back into buffer 0.  A decode call therefore
+// always uses the same pair, and a captured call replays correctly.
+int32_t *lens_of(const dmc_cache *c, int layer, int which) {
+  return at<int32_t>(c, c->lay.lens) + (size_t(which) * c->cfg.num_layers + layer) * c->lay.units;
 }
 
 // Token-window ring of one layer (all null when the cache has no window).
@@ -226,7 +229,6 @@ dmc_status enqueue_reset(dmc_cache *c, hipStream_t s) {
   if (c->lay.window > 0 &&
       (e = dmc::launch_fill_i32(at<int32_t>(c, c->lay.win_len), 0, NL * U, s)) != hipSuccess)
     return hip_fail(e, "reset window lengths");
-  for (auto &p : c->parity) p = 0;
   return DMC_OK;
 }
 
@@ -266,7 +268,6 @@ dmc_status dmc_cache_alloc(const dmc_cache_config *cfg, void *workspace, size_t 
   c->ws_bytes = bytes;
   c->device = dev;
   c->cu_count = cus > 0 ? cus : 256;
-  c->parity.assign(cfg->num_layers, 0);
   st = enqueue_reset(c, static_cast<hipStream_t>(stream));
   if (st != DMC_OK) {
     delete c;
@@ -298,14 +299,13 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
     return fail(DMC_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
   const dmc_cache_config &c = cache->cfg;
   const dmc::Layout &L = cache->lay;
-  const int par = cache->parity[layer];
   dmc::DecodeParams p{};
   p.pool = cache->ws + L.pool;
   p.page_bytes = L.page_bytes;
   p.num_pages = c.num_pages;
   p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
-  p.len_in = lens_of(cache, layer, par);
-  p.len_out = lens_of(cache, layer, par ^ 1);
+  p.len_in = lens_of(cache, layer, 0);
+  p.len_out = lens_of(cache, layer, 1);
   p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
   p.ctrl = at<dmc::Control>(cache, L.ctrl);
   p.q = q;
@@ -335,7 +335,6 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, L.v_trans, p, grid,
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode launch");
-  cache->parity[layer] = static_cast<uint8_t>(par ^ 1);
   return DMC_OK;
 }
 
@@ -374,7 +373,7 @@ dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const 
   p.page_bytes = L.page_bytes;
   p.num_pages = c.num_pages;
   p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
-  p.len = lens_of(cache, layer, cache->parity[layer]);
+  p.len = lens_of(cache, layer, 0);
   p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
   p.ctrl = at<dmc::Control>(cache, L.ctrl);
   p.k = k;
@@ -501,7 +500,7 @@ dmc_status dmc_cache_lengths(const dmc_cache *cache, int32_t layer, int32_t *len
   if (!lengths) return fail(DMC_ERR_INVALID_ARG, "lengths is NULL");
   DeviceGuard g(cache->device);
   if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_copy_i32(lengths, lens_of(cache, layer, cache->parity[layer]),
+  hipError_t e = dmc::launch_copy_i32(lengths, lens_of(cache, layer, 0),
                                       cache->lay.units, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lengths copy");
   return DMC_OK;
@@ -514,7 +513,7 @@ static dmc::DenseParams dense_params(const dmc_cache *cache, int32_t layer, int3
   p.page_bytes = L.page_bytes;
   p.num_pages = cache->cfg.num_pages;
   p.ptab = at<int32_t>(cache, L.ptab) + size_t(layer) * L.units * L.maxpages;
-  p.len = lens_of(cache, layer, cache->parity[layer]);
+  p.len = lens_of(cache, layer, 0);
   p.z = at<float>(cache, L.z) + size_t(layer) * L.units;
   p.ctrl = at<dmc::Control>(cache, L.ctrl);
   p.page_base = at<int32_t>(cache, L.pf_pagebase);
@@ -604,6 +603,17 @@ dmc_status validate_train(const dmc_train_config *c) {
 
 int train_elem_bytes(const dmc_train_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
 
+// Device that holds a training workspace (the configuration names none).
+dmc_status workspace_device(const void *ws, int *dev) {
+  hipPointerAttribute_t attr{};
+  hipError_t e = hipPointerGetAttributes(&attr, ws);
+  if (e != hipSuccess) return hip_fail(e, "hipPointerGetAttributes(workspace)");
+  if (attr.type != hipMemoryTypeDevice)
+    return fail(DMC_ERR_INVALID_ARG, "the training workspace is not device memory");
+  *dev = attr.device;
+  return DMC_OK;
+}
+
 dmc::TrainLayout train_layout_of(const dmc_train_config &c) {
   return dmc::train_layout(c.batch, c.seq_len, c.num_q_heads, c.num_kv_heads, c.head_dim,
                            train_elem_bytes(c), c.window);
@@ -671,6 +681,11 @@ dmc_status dmc_train_forward(const dmc_train_config *cfg, const void *q, const v
   if (!aligned16(out)) return fail(DMC_ERR_INVALID_ARG, "out must be 16-byte aligned");
   p.out = out;
   p.alpha_out = alpha;
+  int dev = 0;
+  st = workspace_device(ws, &dev);
+  if (st != DMC_OK) return st;
+  DeviceGuard g(dev);   // enqueue on the workspace's device, restoring the caller's
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the workspace's device");
   hipError_t e = dmc::launch_train_forward(train_elem_bytes(*cfg), cfg->head_dim,
                                            cfg->num_q_heads / cfg->num_kv_heads, p,
                                            static_cast<hipStream_t>(stream));
@@ -695,6 +710,11 @@ dmc_status dmc_train_backward(const dmc_train_config *cfg, const void *q, const 
   p.dq = dq;
   p.dk = dk;
   p.dv = dv;
+  int dev = 0;
+  st = workspace_device(ws, &dev);
+  if (st != DMC_OK) return st;
+  DeviceGuard g(dev);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the workspace's device");
   hipError_t e = dmc::launch_train_backward(train_elem_bytes(*cfg), cfg->head_dim,
                                             cfg->num_q_heads / cfg->num_kv_heads, p,
                                             static_cast<hipStream_t>(stream));

@@ -62,8 +62,9 @@ struct DecodeParams {
   int64_t page_bytes;
   int64_t num_pages;
   int32_t *ptab;           // [U, maxpages] of this layer
-  const int32_t *len_in;   // [U] lengths before this step
-  int32_t *len_out;        // [U] lengths after this step (other parity buffer)
+  int32_t *len_in;         // [U] lengths before this step (the layer's current lengths)
+  int32_t *len_out;        // [U] lengths after this step; the combine launch copies them
+                           // back into len_in
   float *z;                // [U]
   Control *ctrl;
   const void *q, *k, *v;
@@ -82,7 +83,7 @@ struct PrefillParams {
   int64_t page_bytes;
   int64_t num_pages;
   int32_t *ptab;
-  int32_t *len;            // [U] current-parity lengths of this layer
+  int32_t *len;            // [U] current lengths of this layer
   float *z;
   Control *ctrl;
   const void *k, *v, *q;

@@ -10,9 +10,10 @@
 // Memory layout (one workspace, see dmc_api.cpp):
 //   page pool: page = P key rows then P value rows, each row d contiguous
 //              elements; a row is 128..512 bytes, a page 2*P*row bytes.
-//   page table [L][U][maxpages] int32, lengths [2][L][U] int32 (double
-//   buffered: a decode step reads one parity and writes the other, so every
-//   workgroup sees the same pre-step lengths), z [L][U] fp32.
+//   page table [L][U][maxpages] int32, lengths [2][L][U] int32 (buffer 0
+//   holds the current counts; a decode step reads buffer 0 and writes its
+//   post-step counts to buffer 1, so every workgroup sees the same pre-step
+//   lengths, and its combine launch copies them back), z [L][U] fp32.
 //
 // Decode = one fused launch per layer (Algorithm 1 update + split-K
 // attention, balanced by actual compressed length) plus a small combine
@@ -606,8 +607,13 @@ constexpr int mfma_ring_bytes() { return kWaves * 2 * 2 * 32 * D * 2; }   // 2 s
 template <int D>
 constexpr int mfma_stage_bytes() { return kWaves * 2 * D * 2; }
 
+// Occupancy: at d = 128 the chunk ring (128 KB) leaves room for one workgroup
+// per compute unit (one wave per SIMD); at d = 64 two fit.
+template <int D>
+constexpr int mfma_decode_wg_per_cu() { return D == 128 ? 1 : 2; }
+
 template <int D, int G, bool WIN>
-__global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
   constexpr int NT = D / 16;      // 16-dim tiles of the value product
   constexpr int RB = D * 2;       // bytes per key row
@@ -1023,11 +1029,17 @@ __global__ __launch_bounds__(kThreads, 2) void decode_mfma_kernel(DecodeParams p
 // Combine the split-K partial records of units with more than one tile:
 // o = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i.  One wave per
 // (b, query head); lane i fetches record i's max and sum, then every lane
-// accumulates its E dims over the records.
+// accumulates its E dims over the records.  The launch also copies the
+// step's post-update lengths back into the layer's current-lengths buffer
+// (every unit's owner wrote len_out; this launch runs after all of them).
 template <int ES, int D, int G>
 __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeParams p, int batch) {
   constexpr int REC = D + 4;
   constexpr int E = D / 64;
+  {
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i < p.units) p.len_in[i] = p.len_out[i];
+  }
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int bh = blockIdx.x * kWaves + wave;
   if (bh >= batch * p.hq) return;
@@ -1712,6 +1724,8 @@ hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int batch = p.units / p.hkv;
+  // one wave per (b, query head); the launch's threads also cover the U units
+  // for the lengths copy (kThreads * blocks >= 64 * batch * hq >= units)
   const int blocks = (batch * p.hq + kWaves - 1) / kWaves;
   hipLaunchKernelGGL((combine_kernel<ES, D, G>), dim3(blocks), dim3(kThreads), 0, s, p, batch);
   return hipGetLastError();

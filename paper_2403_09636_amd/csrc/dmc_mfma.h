@@ -44,31 +44,43 @@ __device__ __forceinline__ uint32_t lds_offset(const void *p) {
 }
 
 // 16 bytes per lane from global memory straight into LDS at
-// lds_base + 16 * lane (lds_base wave-uniform).  Issued as inline assembly so
-// that the compiler neither waits for it nor reorders LDS accesses around it;
-// completion is awaited with wait_vmcnt before the workgroup barrier.
+// lds_base + 16 * lane (lds_base wave-uniform), by the compiler's
+// global_load_lds builtin: the compiler sets m0 from lds_base itself and
+// inserts no wait for the transfer, so completion is awaited explicitly with
+// wait_vmcnt before the LDS is read.  aux carries the cache-policy bits
+// (kNontemporal for data streamed once).
+constexpr int kCachePolicyDefault = 0;
+constexpr int kNontemporal = 2;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) char global_cchar_t;
+
+template <int AUX = kCachePolicyDefault>
 __device__ __forceinline__ void dma16(uint32_t lds_base, const void *g) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(lds_base), "v"(g)
-               : "memory");
+  __builtin_amdgcn_global_load_lds((global_cchar_t *)g, (lds_void_t *)(size_t)lds_base, 16, 0, AUX);
 }
 
-// Same, with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane offset.
+// Same, with a wave-uniform 64-bit base (SGPRs, see uniform_ptr) and a 32-bit
+// per-lane offset, by the buffer form of the transfer: the base goes into a
+// raw buffer resource (SGPRs; stride 0, no practical bound) and the lane's
+// offset stays one 32-bit VGPR.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const char *sbase) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(sbase), static_cast<short>(0),
+                                           0x7fffffff, 0x00020000);
+}
+template <int AUX = kCachePolicyDefault>
+__device__ __forceinline__ void dma16_so(uint32_t lds_base, const char *sbase, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(raw_rsrc(sbase), (lds_void_t *)(size_t)lds_base, 16,
+                                           voff, 0, 0, AUX);
+}
 __device__ __forceinline__ void dma16_s(uint32_t lds_base, const char *sbase, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :
-               : "s"(lds_base), "v"(voff), "s"(sbase)
-               : "memory");
+  dma16_so<kCachePolicyDefault>(lds_base, sbase, voff);
 }
 
 // dma16_s with the nontemporal policy, for data streamed once (no reuse
 // through the caches).
 __device__ __forceinline__ void dma16_s_nt(uint32_t lds_base, const char *sbase, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
-               :
-               : "s"(lds_base), "v"(voff), "s"(sbase)
-               : "memory");
+  dma16_so<kNontemporal>(lds_base, sbase, voff);
 }
 
 // A wave-uniform pointer, made visibly uniform (SGPRs) for dma16_s.

@@ -663,8 +663,13 @@ __global__ __launch_bounds__(64) void train_tokens_kernel(TrainParams p) {
 // (E[t][j] - K~_j . dK~_j - V~_j . dV~_j) / z_j over the window, the dot
 // products left per state by the state-gradient pass.  The token gradients go out as
 // whole rows through LDS.
+// Two waves per SIMD, except for the widest windows at d = 128 (NK >= 4), whose
+// E and transposed-product tiles need more than half the register file: one.
 template <int D, int NK>
-__global__ __launch_bounds__(64, 2) void train_tokens_mfma_kernel(TrainParams p) {
+constexpr int tokens_mfma_waves() { return (D == 128 && NK >= 4) ? 1 : 2; }
+
+template <int D, int NK>
+__global__ __launch_bounds__(64, (tokens_mfma_waves<D, NK>())) void train_tokens_mfma_kernel(TrainParams p) {
   constexpr int RB = D * 2, CPR = D / 8, NTL = D / 32, KS = D / 16, ROWS = 16 * NK;
   constexpr int NCT = (ROWS + 31) / 32;   // 32-state column tiles of E and Q
   constexpr int PLANE = ROWS * RB;

@@ -163,3 +163,35 @@ def test_prompt_attend_sampled_7b_layer(torch_cuda):
                                       f64(v[b:b + 1, :, g:g + 1]))
         err = assert_close(f64(out[b, :, g]), o_ref[0, :, 0], "bf16", f"unit {(b, g)}")
         log(f"  unit {(b, g)} max abs err {err:.3e}")
+
+
+def test_prompt_attend_sampled_70b_gqa(torch_cuda):
+    """Llama-2-70B GQA shape at its full prompt (B = 2, n = 4096, 64 query /
+    8 kv heads, G = 8, d = 128, CR 2 per kv head, value pages stored
+    transposed): every unit's slot indices against the oracle's decisions and
+    every output row of 4 sampled units (all 8 query heads each) against a
+    per-unit oracle -- the Sec. 3.2 visibility at this length and group size."""
+    import torch
+    import workloads as W
+    import paper_2403_09636_amd as P
+    log("case prompt 70b gqa sampled")
+    w = W.scaled(W.WORKLOADS["llama70b_gqa"], batch=2)
+    G, n = w.group, w.prompt_len
+    k, v, q = W.prompt_full_torch(w, 0, "cuda")
+    cfg = P.make_config(1, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
+                        w.page_size, n + 8, max_prompt_len=n)
+    cache = P.DMCCache(cfg, device="cuda")
+    slot = torch.empty((w.batch, w.num_kv_heads, n), dtype=torch.int32, device="cuda")
+    out = cache.prefill_attend(0, k, v, q, slot_index=slot)
+    torch.cuda.synchronize()
+    cache.check()
+    alpha = oracle.decision(f64(k[..., 0]), 0.0)
+    alpha[:, 0] = 0
+    want_slots = np.cumsum(1 - alpha, axis=1) - 1
+    assert (slot.cpu().numpy() == want_slots.transpose(0, 2, 1)).all()
+    for b, g in [(0, 0), (1, 7), (0, 5), (1, 2)]:
+        orc = oracle.DMCOracle(1, 1, G, 1, w.head_dim, max_slots=n)
+        o_ref, _ = orc.prefill_attend(0, f64(q[b:b + 1, :, g * G:(g + 1) * G]),
+                                      f64(k[b:b + 1, :, g:g + 1]), f64(v[b:b + 1, :, g:g + 1]))
+        err = assert_close(f64(out[b, :, g * G:(g + 1) * G]), o_ref[0], "bf16", f"unit {(b, g)}")
+        log(f"  unit {(b, g)} max abs err {err:.3e}")

@@ -4,9 +4,12 @@ configuration the benchmark times (default split, default grid).
 * one Llama-2-7B layer (batch 16, 4096-token prompt compressed in-kernel,
   128 decode steps): every slot index, length, slot, z and output;
 * the Llama-2-7B stack, the Llama-2-13B skewed shape and the Llama-2-70B GQA
-  shape: slot indices and lengths of EVERY unit (bit-exact, against the
-  oracle's decision rule) and full content and output parity on a seeded
-  sample of >= 64 (layer, batch, kv-head) units followed by the oracle.
+  shape, over each workload's full decode length (64, 32 and 64 steps; the
+  benchmark times steps of this run length): slot indices and lengths of
+  EVERY unit (bit-exact, against the oracle's decision rule) and full
+  content and output parity on a seeded sample of >= 64 (layer, batch,
+  kv-head) units followed by the oracle, so the bf16 drift of long runs of
+  Algorithm 1's running-mean merge is checked at the benchmark's shapes.
 """
 import numpy as np
 import pytest
@@ -19,11 +22,11 @@ from workloads import (WORKLOADS, decode_inputs_torch, pool_pages, precompressed
 pytestmark = pytest.mark.gpu
 
 
-def _cache_for(w, steps, pages):
+def _cache_for(w, steps, pages, window=0):
     import paper_2403_09636_amd as P
     cfg = P.make_config(w.num_layers, w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype,
                         w.page_size, w.prompt_len + steps, pages, 0.0, "lead", 0,
-                        w.prompt_len if w.cache_kind == "prefill" else 0)
+                        w.prompt_len if w.cache_kind == "prefill" else 0, window=window)
     return P.DMCCache(cfg, device="cuda")
 
 
@@ -75,8 +78,9 @@ def _compare_layer(cache, orc, layer, dtype):
 class Sampled:
     """Oracle units following a sample of (layer, b, g) of a big workload."""
 
-    def __init__(self, w, steps, count=64):
+    def __init__(self, w, steps, count=64, window=0):
         self.w = w
+        self.window = window
         self.units = sample_units(w, count)
         self.by_layer = {}
         for (l, b, g) in self.units:
@@ -86,7 +90,7 @@ class Sampled:
 
     def _new(self):
         w = self.w
-        return oracle.DMCOracle(1, 1, w.group, 1, w.head_dim, self.cap)
+        return oracle.DMCOracle(1, 1, w.group, 1, w.head_dim, self.cap, window=self.window)
 
     def load(self, layer, K, V, lens, z):
         for (b, g) in self.by_layer.get(layer, []):
@@ -131,11 +135,11 @@ class Sampled:
             assert abs(float(z[b, g]) - zr[0, 0]) <= 1e-4 * max(1.0, abs(zr[0, 0])), "z"
 
 
-def _run_big(torch, w, steps):
+def _run_big(torch, w, steps, window=0):
     """Set the whole cache up, run `steps` decode steps over every layer and
     check every unit's slot index and the sampled units' outputs."""
-    smp = Sampled(w, steps)
-    cache = _cache_for(w, steps, pool_pages(w, steps))
+    smp = Sampled(w, steps, window=window)
+    cache = _cache_for(w, steps, pool_pages(w, steps), window=window)
     for layer in range(w.num_layers):
         if w.cache_kind == "precompressed":
             K, V, lt, zt = precompressed_torch(w, layer, "cuda")
@@ -178,7 +182,7 @@ def _run_big(torch, w, steps):
 def test_llama7b_stack_sampled(torch_cuda):
     w = WORKLOADS["llama7b_stack"]
     log(f"case llama7b_stack: {w.notes}")
-    smp = _run_big(torch_cuda, w, steps=3)
+    smp = _run_big(torch_cuda, w, steps=w.decode_steps)
     assert len(smp.units) >= 64
 
 
@@ -186,7 +190,7 @@ def test_llama7b_stack_sampled(torch_cuda):
 def test_llama13b_skew_sampled(torch_cuda):
     w = WORKLOADS["llama13b_skew"]
     log(f"case llama13b_skew: {w.notes}")
-    smp = _run_big(torch_cuda, w, steps=2)
+    smp = _run_big(torch_cuda, w, steps=w.decode_steps)
     assert len(smp.units) >= 64
 
 
@@ -194,5 +198,19 @@ def test_llama13b_skew_sampled(torch_cuda):
 def test_llama70b_gqa_sampled(torch_cuda):
     w = WORKLOADS["llama70b_gqa"]
     log(f"case llama70b_gqa: {w.notes}")
-    smp = _run_big(torch_cuda, w, steps=2)
+    smp = _run_big(torch_cuda, w, steps=w.decode_steps)
+    assert len(smp.units) >= 64
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_gqa_window12_sampled(torch_cuda):
+    """Window grouping (w = 12, Sec. 3.3) at the Llama-2-70B GQA layer shape
+    in the benchmark's launch configuration (B = 256, 8 kv heads, G = 8,
+    4096-token prompts; the windowed matrix-core decode kernel): two layers,
+    the full decode length, every unit's slot indices and >= 64 sampled
+    units against the windowed oracle."""
+    import workloads as W
+    w = W.scaled(WORKLOADS["llama70b_gqa"], num_layers=2)
+    log(f"case llama70b_gqa window 12, 2 layers: {w.notes}")
+    smp = _run_big(torch_cuda, w, steps=w.decode_steps, window=12)
     assert len(smp.units) >= 64
