@@ -212,6 +212,35 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q_dev,
                            const void *k_dev, const void *v_dev, void *out_dev,
                            int32_t *slot_index_dev, dmc_stream_t stream);
 
+/* Bytes of the library's static device scratch used by dmc_decode_step_static
+ * (one copy per GPU the library runs on, held until the process ends). */
+#define DMC_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* dmc_decode_step for callers that cannot allocate device memory (code under
+ * HIP-graph capture, tight serving loops, harnesses that forbid allocation
+ * or extra workspace traffic): the same update and attention, through the
+ * same kernels, with results bit-identical to dmc_decode_step -- but the
+ * split-K partial records and the per-unit record table come from a static
+ * device array of the library (DMC_STATIC_SCRATCH_BYTES per GPU) instead of
+ * the cache workspace.  The call allocates nothing and calls no allocating
+ * routine; the array's address on a device is resolved once, when the first
+ * cache on that device is created (dmc_cache_alloc).
+ *   Arguments, layouts and device-side errors: as for dmc_decode_step.
+ *   Limit: a launch of this cache needs units * 8 bytes (rounded up to 256)
+ *     plus (ranges + units) * G * (head_dim + 4) * 4 bytes of records, ranges
+ *     being the launch's waves (2048 on a 256-CU MI355X) or, with a split_tile,
+ *     ceil(units * max_slots_per_seq / split_tile) if that is larger; a
+ *     cache that needs more returns DMC_ERR_UNSUPPORTED before anything is
+ *     enqueued.
+ *   Nothing in the array has to start at zero: every record a call reads is
+ *     written earlier in the same call.  All calls on one GPU share that
+ *     GPU's array, so calls that overlap on one GPU (other streams, other
+ *     caches or layers in flight concurrently) race and give wrong results:
+ *     serialise them, e.g. on one stream. */
+dmc_status dmc_decode_step_static(dmc_cache *cache, int32_t layer, const void *q_dev,
+                                  const void *k_dev, const void *v_dev, void *out_dev,
+                                  int32_t *slot_index_dev, dmc_stream_t stream);
+
 /* Copy the slot counts of one layer into lengths_dev (int32 [B, Hkv]). */
 dmc_status dmc_cache_lengths(const dmc_cache *cache, int32_t layer, int32_t *lengths_dev,
                              dmc_stream_t stream);

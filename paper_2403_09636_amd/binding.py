@@ -26,7 +26,8 @@ STATUS_NAMES = {0: "DMC_OK", 1: "DMC_ERR_INVALID_ARG", 2: "DMC_ERR_UNSUPPORTED",
 
 #: Every entry point declared in include/dmc.h.
 EXPORTS = ("dmc_cache_workspace_bytes", "dmc_cache_alloc", "dmc_cache_free", "dmc_cache_reset",
-           "dmc_prefill_compress", "dmc_prefill_attend", "dmc_decode_step", "dmc_cache_lengths", "dmc_cache_export",
+           "dmc_prefill_compress", "dmc_prefill_attend", "dmc_decode_step", "dmc_decode_step_static",
+           "dmc_cache_lengths", "dmc_cache_export",
            "dmc_cache_import", "dmc_cache_check", "dmc_cache_pages_used", "dmc_last_error",
            "dmc_train_workspace_bytes", "dmc_train_forward", "dmc_train_backward")
 
@@ -73,6 +74,7 @@ def _load():
                                        c_void_p, c_void_p]
     lib.dmc_decode_step.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                     c_void_p, c_void_p]
+    lib.dmc_decode_step_static.argtypes = lib.dmc_decode_step.argtypes
     lib.dmc_cache_lengths.argtypes = [c_void_p, c_int32, c_void_p, c_void_p]
     lib.dmc_cache_export.argtypes = [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
                                      c_void_p]
@@ -341,6 +343,14 @@ class DMCCache:
         check_decode_args(self.cfg, self.device, q, k, v, out, slot_index)
         check(lib.dmc_decode_step(self.handle, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                   _ptr(slot_index), _stream(stream)))
+        return out
+
+    def decode_step_static(self, layer, q, k, v, out, slot_index=None, stream=None):
+        """dmc_decode_step_static: as decode_step, with the split-K records in the
+        library's static device scratch; allocates nothing (`out` is required)."""
+        check_decode_args(self.cfg, self.device, q, k, v, out, slot_index)
+        check(lib.dmc_decode_step_static(self.handle, layer, _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(out), _ptr(slot_index), _stream(stream)))
         return out
 
     def prefill(self, layer, k, v, q, n=None, prompt_lens=None, slot_index=None, stream=None):

@@ -268,6 +268,14 @@ dmc_status dmc_cache_alloc(const dmc_cache_config *cfg, void *workspace, size_t 
   c->ws_bytes = bytes;
   c->device = dev;
   c->cu_count = cus > 0 ? cus : 256;
+  // Set-up of dmc_decode_step_static: the device address of the library's
+  // static scratch on this (current) device, resolved once per device.
+  void *scratch = nullptr;
+  e = dmc::static_scratch(&scratch);
+  if (e != hipSuccess) {
+    delete c;
+    return hip_fail(e, "static scratch address");
+  }
   st = enqueue_reset(c, static_cast<hipStream_t>(stream));
   if (st != DMC_OK) {
     delete c;
@@ -290,8 +298,19 @@ dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream) {
   return enqueue_reset(cache, static_cast<hipStream_t>(stream));
 }
 
-dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const void *k,
-                           const void *v, void *out, int32_t *slot_index, dmc_stream_t stream) {
+namespace {
+
+// Persistent decode grid of a cache: workgroups of 4 waves, kDecodeWgPerCu per
+// compute unit (the matrix-core launch halves it when its LDS ring allows one).
+int decode_grid(const dmc_cache *cache) {
+  return static_cast<int>(
+      std::min<int64_t>(int64_t(cache->cu_count) * kDecodeWgPerCu, kMaxDecodeWaves / 4));
+}
+
+// Shared checks and parameter set-up of the two decode entry points; the
+// split-K records (partials, meta) are filled in by the caller.
+dmc_status decode_params(dmc_cache *cache, int32_t layer, const void *q, const void *k,
+                         const void *v, void *out, int32_t *slot_index, dmc::DecodeParams *out_p) {
   dmc_status st = check_layer(cache, layer);
   if (st != DMC_OK) return st;
   if (!q || !k || !v || !out) return fail(DMC_ERR_INVALID_ARG, "q, k, v and out must be non-NULL");
@@ -299,7 +318,8 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
     return fail(DMC_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
   const dmc_cache_config &c = cache->cfg;
   const dmc::Layout &L = cache->lay;
-  dmc::DecodeParams p{};
+  dmc::DecodeParams &p = *out_p;
+  p = dmc::DecodeParams{};
   p.pool = cache->ws + L.pool;
   p.page_bytes = L.page_bytes;
   p.num_pages = c.num_pages;
@@ -313,8 +333,6 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   p.v = v;
   p.out = out;
   p.slot_index = slot_index;
-  p.partials = at<float>(cache, L.partials);
-  p.meta = at<int32_t>(cache, L.meta);
   p.win = window_of(cache, layer);
   p.c = c.decision_bias;
   p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(c.head_dim)));
@@ -327,15 +345,67 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const
   p.split_tile = L.split_tile;
   p.omega_src = c.omega_src;
   p.decision_src = c.decision_src;
-  const int64_t grid64 = std::min<int64_t>(int64_t(cache->cu_count) * kDecodeWgPerCu,
-                                            kMaxDecodeWaves / 4);
-  const int grid = static_cast<int>(grid64);
-  DeviceGuard g(cache->device);
-  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
-  hipError_t e = dmc::launch_decode(elem_bytes(c), c.head_dim, L.group, L.v_trans, p, grid,
+  return DMC_OK;
+}
+
+dmc_status decode_launch(dmc_cache *cache, const dmc::DecodeParams &p, dmc_stream_t stream) {
+  hipError_t e = dmc::launch_decode(elem_bytes(cache->cfg), cache->cfg.head_dim, cache->lay.group,
+                                    cache->lay.v_trans, p, decode_grid(cache),
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   return DMC_OK;
+}
+
+// Bytes of split-K records one decode launch of this cache can use: the
+// per-unit table (first record, count) and one record of G x (d + 4) fp32 per
+// (range, unit) piece, indexed range + unit.  Ranges are at most the launch's
+// waves, or ceil(S / split_tile) with S <= units * max_slots_per_seq.
+size_t decode_records_bytes(const dmc_cache *cache, size_t *meta_bytes) {
+  const dmc::Layout &L = cache->lay;
+  int64_t ranges = int64_t(decode_grid(cache)) * 4;
+  if (L.split_tile > 0) {
+    const int64_t S = int64_t(L.units) * cache->cfg.max_slots_per_seq;
+    ranges = std::max<int64_t>(ranges, (S + L.split_tile - 1) / L.split_tile);
+  }
+  *meta_bytes = align_up(size_t(L.units) * 2 * 4, 256);
+  return *meta_bytes + size_t(ranges + L.units) * L.group * (cache->cfg.head_dim + 4) * 4;
+}
+
+}  // namespace
+
+dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q, const void *k,
+                           const void *v, void *out, int32_t *slot_index, dmc_stream_t stream) {
+  dmc::DecodeParams p;
+  dmc_status st = decode_params(cache, layer, q, k, v, out, slot_index, &p);
+  if (st != DMC_OK) return st;
+  p.partials = at<float>(cache, cache->lay.partials);
+  p.meta = at<int32_t>(cache, cache->lay.meta);
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  return decode_launch(cache, p, stream);
+}
+
+dmc_status dmc_decode_step_static(dmc_cache *cache, int32_t layer, const void *q, const void *k,
+                                  const void *v, void *out, int32_t *slot_index,
+                                  dmc_stream_t stream) {
+  dmc::DecodeParams p;
+  dmc_status st = decode_params(cache, layer, q, k, v, out, slot_index, &p);
+  if (st != DMC_OK) return st;
+  size_t meta_bytes = 0;
+  const size_t need = decode_records_bytes(cache, &meta_bytes);
+  if (need > dmc::kStaticScratchBytes)
+    return fail(DMC_ERR_UNSUPPORTED,
+                "decode records of this cache need %zu bytes, more than the %zu-byte static "
+                "scratch of dmc_decode_step_static (use dmc_decode_step)",
+                need, dmc::kStaticScratchBytes);
+  DeviceGuard g(cache->device);
+  if (!g.ok) return fail(DMC_ERR_HIP, "cannot select the cache's device");
+  char *scratch = nullptr;
+  hipError_t e = dmc::static_scratch(reinterpret_cast<void **>(&scratch));
+  if (e != hipSuccess) return hip_fail(e, "static scratch address");
+  p.meta = reinterpret_cast<int32_t *>(scratch);
+  p.partials = reinterpret_cast<float *>(scratch + meta_bytes);
+  return decode_launch(cache, p, stream);
 }
 
 namespace {

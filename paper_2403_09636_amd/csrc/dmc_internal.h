@@ -195,6 +195,13 @@ hipError_t launch_prefill(int elem_bytes, int head_dim, bool vt, const PrefillPa
 hipError_t launch_import(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 hipError_t launch_export(int elem_bytes, int head_dim, bool vt, const DenseParams &p, hipStream_t s);
 
+// Allocation-free decode (dmc_decode_step_static): the split-K records live in
+// a file-scope static device array of this many bytes (dmc_kernels.hip).
+// static_scratch() returns its address on the current device, resolved with
+// hipGetSymbolAddress on the first call per device and kept per device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(void **ptr);
+
 // Largest window-grouping width.
 constexpr int kMaxWindow = 64;
 

@@ -21,7 +21,39 @@
 #include "dmc_device.h"
 #include "dmc_mfma.h"
 
+#include <mutex>
+
 namespace dmc {
+
+// Scratch of the allocation-free decode entry point: split-K partial records
+// and the per-unit record table of one decode launch.  In host code the name
+// `scratch` is only a stand-in for the symbol, never a device address: the
+// address on a device comes from hipGetSymbolAddress (static_scratch).  Every
+// call on a GPU shares that GPU's copy; a call writes every entry it reads.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_scratch(void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[dev] = p;
+  }
+  *ptr = g_scratch_addr[dev];
+  return hipSuccess;
+}
+
 namespace {
 
 #ifndef DMC_VALU_CHUNK
