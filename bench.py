@@ -526,6 +526,13 @@ def bench_decode(args, pool):
     cache = P.DMCCache(cfg, device=dev)
     prefill_ms = []
     seg_len0, prompt_reads = [], 0   # window bookkeeping (host side, from the decisions)
+    if w.cache_kind == "prefill":
+        # one untimed prefill first, so that the timed ones exclude loading the kernels
+        k, v, q0 = W.prompt_torch(w, 0, dev)
+        cache.prefill(0, k, v, q0)
+        torch.cuda.synchronize()
+        cache.reset()
+        del k, v, q0
     for layer in range(w.num_layers):
         if w.cache_kind == "precompressed":
             Kd, Vd, lt, zt = W.precompressed_torch(w, layer, dev)
@@ -641,13 +648,25 @@ def bench_decode(args, pool):
         res["cpu_baseline"] = cpu_baseline(w, lens0[:, 0, :], args.cpu_seconds, pool)
     print(json.dumps(res), flush=True)
     if args.calib_copy:
-        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings give
-        # the scale factor between the counters and bytes moved.
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
+        calibration_kernels(torch, dev)
+
+
+def calibration_kernels(torch, dev):
+    """Kernels of known traffic for the counter calibration, after the timed
+    work: plain 1 GiB device copies (their FETCH_SIZE / WRITE_SIZE readings
+    give the scale factors between the counters and bytes moved), then a
+    strided read -- one bf16 element of every 256-byte row of 1 GiB, the
+    access pattern of a decision-neuron read -- to check the scale on a
+    second pattern and to show the fetch granularity of isolated reads."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    rows = src.view(torch.bfloat16).view(-1, 128)      # 4 Mi rows of 256 B
+    for _ in range(3):
+        rows[:, 0].sum()
+    torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -152,6 +152,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.pf_alpha = take(U * size_t(L.max_prompt));
   L.pf_omega = take(U * size_t(L.max_prompt) * 4);
   L.pf_count = take(U * size_t(L.prompt_chunks) * 4);
+  L.pf_mask = take(U * size_t(L.prompt_chunks) * 8);
   L.pf_pagebase = take(U * 4);
   L.pf_carry = take(U * size_t(L.carry_blocks) * dmc::carry_stride(c.head_dim) * 4);
   L.win = take(NL * U * size_t(L.window) * 2 * c.head_dim * es);
@@ -459,6 +460,7 @@ dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const 
   p.alpha = at<uint8_t>(cache, L.pf_alpha);
   p.omega = at<float>(cache, L.pf_omega);
   p.count = at<int32_t>(cache, L.pf_count);
+  p.mask = at<uint64_t>(cache, L.pf_mask);
   p.page_base = at<int32_t>(cache, L.pf_pagebase);
   p.carry = nullptr;
   p.win = window_of(cache, layer);

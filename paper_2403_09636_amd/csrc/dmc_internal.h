@@ -29,8 +29,8 @@ struct Control {
 
 // Byte offsets of the workspace sections (all 256-byte aligned).
 struct Layout {
-  size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_pagebase,
-      pf_carry, win, win_omega, win_len;
+  size_t pool, ptab, lens, z, ctrl, meta, partials, pf_alpha, pf_omega, pf_count, pf_mask,
+      pf_pagebase, pf_carry, win, win_omega, win_len;
   size_t total;
   int64_t page_bytes;     // 2 * P * d * elem_bytes (K rows, then V rows)
   int32_t units;          // B * Hkv per layer
@@ -90,9 +90,10 @@ struct PrefillParams {
   int64_t ks[3], vs[3], qs[3];
   const int32_t *prompt_lens;
   int32_t *slot_index;     // optional [U, n]
-  uint8_t *alpha;          // [U, max_prompt]
-  float *omega;            // [U, max_prompt]
-  int32_t *count;          // [U, prompt_chunks]
+  uint8_t *alpha;          // [U, max_prompt] (staged only for prompt attention / window)
+  float *omega;            // [U, max_prompt] (likewise)
+  int32_t *count;          // [U, prompt_chunks] segment starts per 64-token chunk
+  uint64_t *mask;          // [U, prompt_chunks] bit i: token 64 c + i starts a segment
   int32_t *page_base;      // [U]
   float *carry;            // optional [U, carry_blocks, carry_stride]: open-segment sums at
                            // every 32-token boundary inside a segment (prompt attention)

@@ -21,7 +21,9 @@
 #include "dmc_device.h"
 #include "dmc_mfma.h"
 
+#include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 namespace dmc {
 
@@ -1183,17 +1185,46 @@ __device__ __forceinline__ int prompt_len(const PrefillParams &p, int b, bool ra
   return x;
 }
 
-// Pass 1, one workgroup per unit: decisions (the first token always opens a
-// slot), importance scores, per-64-token start counts and the unit length.
+// Launch-order helpers.  Workgroups are dispatched round-robin over the 8
+// XCDs (workgroup i to XCD i mod 8); xcd_order maps the launch index to a
+// logical one so that consecutive logical workgroups run on the same XCD (its
+// L2), in dispatch order.  A bijection on [0, n) for any n.
+__device__ __forceinline__ int xcd_order(int lin, int n) {
+  const int q = n >> 3, r = n & 7, x = lin & 7, j = lin >> 3;
+  return x < r ? x * (q + 1) + j : r * (q + 1) + (x - r) * q + j;
+}
+
+// Importance omega of token t of unit (b, dg) (Sec. 3.1: sigmoid of the first
+// query neuron), per the configured source; floored at 2^-100.
 template <int ES>
+__device__ __forceinline__ float token_omega(const PrefillParams &p, int b, int t, int dg, int G) {
+  if (p.omega_src == 0)
+    return sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G) * p.qs[2]));
+  if (p.omega_src == 1) {
+    float sum = 0.0f;
+    for (int h = 0; h < G; ++h)
+      sum += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G + h) * p.qs[2]));
+    return fmaxf(sum / G, 0x1p-100f);
+  }
+  return 1.0f;   // uniform weighting
+}
+
+// Pass 1, one workgroup per unit (units in XCD order): decisions from the
+// decision neuron k[0] (the first token always opens a slot), and per 64-token
+// chunk the mask and count of segment starts; the unit length.  STAGE (prompt
+// attention, window grouping) also stores every token's decision and
+// importance for the passes that read them; the exact compaction reads only
+// k[0] here and forms omega itself.
+template <int ES, bool STAGE>
 __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams p) {
   __shared__ int s_tot[kWaves];
-  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int u = xcd_order(blockIdx.x, gridDim.x);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = u / p.hkv, g = u - b * p.hkv, G = p.hq / p.hkv;
   const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
   const int nb = prompt_len(p, b, tid == 0);
   int total = 0;
-  constexpr int kBatch = 8;   // token rows whose decision neurons are in flight per thread
+  constexpr int kBatch = STAGE ? 8 : 16;   // tokens whose decision neurons are in flight per thread
   for (int t00 = 0; t00 < p.n; t00 += kThreads * kBatch) {
     float k0[kBatch], q0[kBatch];
 #pragma unroll
@@ -1203,32 +1234,24 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
       q0[j] = 0.0f;
       if (t < p.n) {
         k0[j] = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + dg * p.ks[2]);
-        if (p.omega_src == 0)
+        if (STAGE && p.omega_src == 0)
           q0[j] = load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G) * p.qs[2]);
       }
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int t0 = t00 + j * kThreads;
-      if (t0 >= p.n) break;
+      if (t0 < p.n) {   // (a wave-uniform condition)
       const int t = t0 + tid;
       int start = 0;
       if (t < p.n) {
         const bool valid = t < nb;
         const int a = (t > 0 && k0[j] > p.c) ? 1 : 0;
-        float om;
-        if (p.omega_src == 0) {
-          om = sigmoid_floor(q0[j]);
-        } else if (p.omega_src == 1) {
-          float sum = 0.0f;
-          for (int h = 0; h < G; ++h)
-            sum += sigmoid_floor(load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G + h) * p.qs[2]));
-          om = fmaxf(sum / G, 0x1p-100f);
-        } else {
-          om = 1.0f;   // uniform weighting
+        if (STAGE) {
+          const float om = p.omega_src == 0 ? sigmoid_floor(q0[j]) : token_omega<ES>(p, b, t, dg, G);
+          p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
+          p.omega[int64_t(u) * p.max_prompt + t] = om;
         }
-        p.alpha[int64_t(u) * p.max_prompt + t] = valid ? a : 1;
-        p.omega[int64_t(u) * p.max_prompt + t] = om;
         if (p.slot_index && !valid) p.slot_index[int64_t(u) * p.n + t] = -1;
         start = (valid && !a) ? 1 : 0;
       }
@@ -1236,7 +1259,9 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
       const int chunk = (t0 >> 6) + wave;
       if (lane == 0 && chunk * 64 < p.n) {
         p.count[int64_t(u) * p.prompt_chunks + chunk] = __popcll(mask);
+        p.mask[int64_t(u) * p.prompt_chunks + chunk] = mask;
         total += __popcll(mask);
+      }
       }
     }
   }
@@ -1320,65 +1345,190 @@ __global__ __launch_bounds__(1024) void alloc_pages_kernel(int32_t *len, float *
   }
 }
 
-// Pass 3, one wave per (unit, 64-token chunk): every segment whose first
-// token lies in the chunk is reduced by this wave -- the omega-weighted sums
-// of its keys (element 0 zeroed) and values divided by its omega sum, which
-// equals the running mean of Algorithm 1 -- reading past the chunk end while
-// the last segment continues.  Each token is read exactly once.  Tokens are
-// streamed in fixed batches whatever the segment lengths; a segment is
-// flushed (slot written) when the next one starts.  The wave that writes
-// the first slot of a page also writes its page-table entry.  With carry
-// records enabled, the running sums of a segment that crosses a 32-token
-// boundary t (t not a segment start) are stored as they stand before t:
-// the prompt-attention pass resumes a segment's running mean from there.
-template <int ES, int D>
-__global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams p) {
-  constexpr int E = D / 64;  // elements per lane
-  constexpr int RB = D * ES;
-  constexpr int kRows = 8;   // token rows in flight per wave
-  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ch = blockIdx.x * kWaves + wave;
-  const int tlo = ch * 64;
-  if (tlo >= p.n) return;
-  const int pb = p.page_base[u];
-  if (pb < 0) return;
-  const int b = u / p.hkv, g = u - b * p.hkv;
-  const int nb = prompt_len(p, b, false);
-  if (tlo >= nb) return;
-  const uint8_t *al = p.alpha + int64_t(u) * p.max_prompt;
-  const float *om = p.omega + int64_t(u) * p.max_prompt;
-  auto starts = [&](int wb) -> unsigned long long {
-    const int t = wb + lane;
-    return __ballot(t < nb && al[t] == 0);
-  };
-  const unsigned long long m0 = starts(tlo);
-  if (m0 == 0) return;
-  int before = 0;
-  for (int j = lane; j < ch; j += 64) before += p.count[int64_t(u) * p.prompt_chunks + j];
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o, 64);
+#ifndef DMC_PF_ROWS
+#define DMC_PF_ROWS 16
+#endif
+#ifndef DMC_PF_BUFFERS
+#define DMC_PF_BUFFERS 1
+#endif
+constexpr int kPfRows = DMC_PF_ROWS;     // prompt rows per batch (each of K and V)
+constexpr int kPfBuf = DMC_PF_BUFFERS;   // batches in a wave's register ring
+static_assert(kPfRows >= 1 && kPfRows <= 32, "prompt rows per batch");
+static_assert(kPfBuf >= 1 && kPfBuf <= 4, "ring depth");
 
-  // Tokens [t0, t_stop): from the chunk's first segment start to the next
-  // start at or after the chunk end (or the prompt end).
-  const int t0 = tlo + __ffsll(static_cast<long long>(m0)) - 1;
-  int t_stop = nb;
-  for (int wb = tlo + 64; wb < nb; wb += 64) {
-    const unsigned long long mk = starts(wb);
-    if (mk) {
-      t_stop = wb + __ffsll(static_cast<long long>(mk)) - 1;
-      break;
+// One lane's E elements of a prompt row as loaded (packed), unpacked at use.
+template <int ES, int E>
+struct RowBits {
+  typedef typename std::conditional<(ES * E > 4), uint2, uint32_t>::type T;
+  T w;
+  __device__ __forceinline__ void load_nt(const char *p) {
+    if constexpr (ES == 2 && E == 2) {
+      w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+    } else if constexpr (ES == 2) {
+      w = __builtin_nontemporal_load(reinterpret_cast<const uint16_t *>(p));
+    } else if constexpr (E == 2) {
+      typedef unsigned int u2_t __attribute__((ext_vector_type(2)));
+      const u2_t x = __builtin_nontemporal_load(reinterpret_cast<const u2_t *>(p));
+      w = make_uint2(x.x, x.y);
+    } else {
+      w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
     }
   }
+  __device__ __forceinline__ void unpack(float *f) const {
+    if constexpr (ES == 2 && E == 2) {
+      f[0] = __uint_as_float(w << 16);
+      f[1] = __uint_as_float(w & 0xffff0000u);
+    } else if constexpr (ES == 2) {
+      f[0] = __uint_as_float(w << 16);
+    } else if constexpr (E == 2) {
+      f[0] = __uint_as_float(w.x);
+      f[1] = __uint_as_float(w.y);
+    } else {
+      f[0] = __uint_as_float(w);
+    }
+  }
+};
 
+// Position of the r-th set bit (r from 0) of m, which holds more than r bits.
+__device__ __forceinline__ int select_bit(unsigned long long m, int r) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    const int c = __popcll(m & ((1ull << w) - 1ull));
+    if (r >= c) {
+      r -= c;
+      m >>= w;
+      pos += w;
+    }
+  }
+  return pos;
+}
+
+__device__ __forceinline__ unsigned long long shfl64(unsigned long long x, int src) {
+  const uint32_t lo = __shfl(static_cast<uint32_t>(x), src, 64);
+  const uint32_t hi = __shfl(static_cast<uint32_t>(x >> 32), src, 64);
+  return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
+// Token that opens segment (slot) s of a unit, s < its length: the unit's
+// start masks are read 64 chunks at a time (lane j: chunk j0 + j) and counted
+// by a wave scan.  Returns `none` if the masks hold no such start.
+__device__ __forceinline__ int start_token(const uint64_t *masks, int chunks, int s, int none) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  for (int j0 = 0; j0 < chunks; j0 += 64) {
+    const unsigned long long mk = j0 + lane < chunks ? masks[j0 + lane] : 0ull;
+    const int c = __popcll(mk);
+    int incl = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    const int tot = __shfl(incl, 63, 64);
+    if (s < base + tot) {
+      const int jl = __ffsll(static_cast<long long>(__ballot(base + incl > s))) - 1;
+      const int before = base + __shfl(incl - c, jl, 64);
+      return (j0 + jl) * 64 + select_bit(shfl64(mk, jl), s - before);
+    }
+    base += tot;
+  }
+  return none;
+}
+
+// Pass 3 (exact Algorithm 1), slot-aligned work items of about kItemTokens
+// prompt tokens.  Unit u of length l is cut into items of S_u slots, S_u =
+// l kItemTokens / n rounded up to a multiple of 32 (so an item of a highly
+// compressed head spans few slots and one of an uncompressed head many, and
+// every item reads about the same number of prompt rows).  32-slot alignment
+// keeps every 32-slot page -- the transposed value pages of grouped-query
+// caches included -- inside one item, written by one wave in whole rows, and
+// no later pass touches it.  The item's tokens run from the start of its first
+// slot's segment to the start of the segment after its last slot (the prompt
+// end for the unit's last slot), located in the start masks of pass 1; each
+// token is read once, by the item holding its segment.  A slot is the
+// omega-weighted sum of its segment's keys (element 0 zeroed) and values over
+// their omega sum, in fp32 -- the running mean Algorithm 1 holds at the
+// segment's end; the unit's last segment gives z.  Omega comes from the first
+// query neuron here.  With carry records enabled, the running sums of a
+// segment that crosses a 32-token boundary t (t not a segment start) are
+// stored as they stand before t, for the prompt-attention pass.  Waves map to
+// (item k, unit u) with k outermost, in plain launch order, so every XCD gets
+// a mix of all units and items.
+#ifndef DMC_PF_ITEM_TOKENS
+#define DMC_PF_ITEM_TOKENS 256
+#endif
+constexpr int kItemTokens = DMC_PF_ITEM_TOKENS;
+
+// Slots per work item of a unit with l slots from a prompt of n tokens.
+__device__ __forceinline__ int item_slots(int l, int n) {
+  const int64_t want = (int64_t(l) * kItemTokens + n - 1) / max(n, 1);
+  return static_cast<int>(max<int64_t>(32, (want + 31) & ~int64_t(31)));
+}
+
+template <int ES, int D, bool VT>
+__global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p, int items) {
+  constexpr int E = D / 64;         // elements per lane
+  constexpr int RB = D * ES;        // bytes per row
+  constexpr int LDR = RB + 4;       // padded LDS row of the V^T staging page
+  static_assert(!VT || ES == 2, "transposed value pages are bf16");
+  __shared__ __align__(16) unsigned char s_vt[VT ? kWaves * 32 * LDR : 16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gw = blockIdx.x * kWaves + wave;
+  const int k = gw / p.units;
+  if (k >= items) return;
+  const int u = gw - k * p.units, b = u / p.hkv, g = u - b * p.hkv;
+  const int l = p.len[u];
   const int P = 1 << p.log2p;
+  const int S = item_slots(l, p.n);
+  const int s_lo = k * S;
+  if (s_lo >= l) return;
+  const int pb = p.page_base[u];
+  if (pb < 0) return;
+  const int s_hi = min(s_lo + S, l);
+  const int nb = prompt_len(p, b, false);
+  const int G = p.hq / p.hkv, dg = p.decision_src ? 0 : g;
+  const uint64_t *um = p.mask + int64_t(u) * p.prompt_chunks;
+  const int nch = (p.n + 63) >> 6;   // chunks written for this prompt
+  const int t_lo = start_token(um, nch, s_lo, nb);
+  const int t_hi = s_hi < l ? start_token(um, nch, s_hi, nb) : nb;
+
+  // page-table entries of the pages whose first slot is in the item
+  const int64_t pt = int64_t(u) * p.maxpages;
+  const int pg0 = (s_lo + P - 1) >> p.log2p, pg1 = (s_hi - 1) >> p.log2p;
+  for (int i = pg0 + lane; i <= pg1; i += 64) p.ptab[pt + i] = pb + i;
+
   const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
   const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
   const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
-  int s = before;
+  unsigned char *stage = s_vt + (VT ? wave * 32 * LDR : 0);
+  int s = s_lo;
   float ak[E], av[E], zs = 0.0f;
 #pragma unroll
   for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
-  auto flush = [&]() {   // write slot s = sums / zs
+
+  // The value page of grouped-query caches, staged as 32 rows in LDS, goes out
+  // as V^T: lane (dim, quarter) gathers 8 slots of one dim -- conflict-free
+  // thanks to the padded rows -- and stores them as one 16-byte piece.
+  auto write_vt_page = [&](char *vtp) {
+    if constexpr (VT) {
+      wave_lds_sync();
+#pragma unroll
+      for (int i = 0; i < D * 4 / 64; ++i) {
+        const int pc = i * 64 + lane, dim = pc >> 2, qq = pc & 3;
+        const unsigned char *col = stage + 8 * qq * LDR + dim * 2;
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          w[j] = uint32_t(*reinterpret_cast<const uint16_t *>(col + 2 * j * LDR)) |
+                 (uint32_t(*reinterpret_cast<const uint16_t *>(col + (2 * j + 1) * LDR)) << 16);
+        __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]},
+                                    reinterpret_cast<u32x4 *>(vtp + dim * 64 + qq * 16));
+      }
+      wave_lds_sync();   // the staging rows are read before they are refilled
+    }
+  };
+  auto flush = [&]() {   // slot s = sums / zs
     const float inv = 1.0f / zs;
     float kq[E], vq[E];
 #pragma unroll
@@ -1386,36 +1536,71 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
       kq[e] = ak[e] * inv;
       vq[e] = av[e] * inv;
     }
-    char *row = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes + int64_t(s & (P - 1)) * RB +
-                lane * E * ES;
-    store_e_nt<ES, E>(row, kq);
-    store_e_nt<ES, E>(row + int64_t(P) * RB, vq);
-    if (lane == 0 && (s & (P - 1)) == 0)
-      p.ptab[int64_t(u) * p.maxpages + (s >> p.log2p)] = pb + (s >> p.log2p);
-  };
-  for (int t2 = t0; t2 < t_stop; t2 += kRows) {
-    const int cnt = min(kRows, t_stop - t2);
-    float kk[kRows][E], vv[kRows][E], ww[kRows];
-#pragma unroll
-    for (int j = 0; j < kRows; ++j) {
-      const int tj = t2 + min(j, cnt - 1);
-      load_e_nt<ES, E>(kbase + tj * kst, kk[j]);   // prompt rows are read once
-      load_e_nt<ES, E>(vbase + tj * vst, vv[j]);
-      ww[j] = om[tj];
+    const int row = s & (P - 1);
+    char *pg = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes;
+    store_e_nt<ES, E>(pg + int64_t(row) * RB + lane * E * ES, kq);
+    if constexpr (VT) {
+      store_e<ES, E>(reinterpret_cast<char *>(stage + row * LDR + lane * E * ES), vq);
+      if (row == 31 || s == s_hi - 1) write_vt_page(pg + 32 * RB);
+    } else {
+      store_e_nt<ES, E>(pg + int64_t(P) * RB + int64_t(row) * RB + lane * E * ES, vq);
     }
+  };
+
+  // Batches of kPfRows tokens stream through a ring of kPfBuf register
+  // buffers: kPfBuf - 1 batches are in flight while one is consumed.  A batch
+  // carries its K and V rows (packed), the lane's first query neuron (lane j:
+  // token t2 + j) and the start-mask words that cover it.
+  struct Batch {
+    RowBits<ES, E> kr[kPfRows], vr[kPfRows];
+    uint32_t q0;
+    unsigned long long m0, m1;
+  };
+  const int nbat = (t_hi - t_lo + kPfRows - 1) / kPfRows;
+  const bool lead_q0 = p.omega_src == 0;
+  auto issue = [&](int bi, Batch &bt) {
+    const int t2 = t_lo + bi * kPfRows, cnt = min(kPfRows, t_hi - t2);
 #pragma unroll
-    for (int j = 0; j < kRows; ++j) {
+    for (int j = 0; j < kPfRows; ++j) {
+      const int tj = t2 + min(j, cnt - 1);
+      bt.kr[j].load_nt(kbase + tj * kst);   // prompt rows are read once
+      bt.vr[j].load_nt(vbase + tj * vst);
+    }
+    bt.q0 = 0;
+    if (lead_q0 && lane < cnt) {
+      const int64_t qi = b * p.qs[0] + int64_t(t2 + lane) * p.qs[1] + (dg * G) * p.qs[2];
+      bt.q0 = ES == 2 ? uint32_t(static_cast<const uint16_t *>(p.q)[qi]) << 16
+                      : __float_as_uint(static_cast<const float *>(p.q)[qi]);
+    }
+    const int c2 = t2 >> 6;
+    bt.m0 = um[c2];
+    bt.m1 = ((t2 & 63) + kPfRows > 64 && c2 + 1 < nch) ? um[c2 + 1] : 0ull;
+  };
+  auto consume = [&](int bi, const Batch &bt) {
+    const int t2 = t_lo + bi * kPfRows, cnt = min(kPfRows, t_hi - t2);
+    // segment starts among the batch's tokens (bit j), the item's first token
+    // (the start of slot s_lo) not counted
+    const int sh = t2 & 63;
+    unsigned long long w = bt.m0 >> sh;
+    if (sh + kPfRows > 64) w |= bt.m1 << (64 - sh);
+    uint32_t sb = static_cast<uint32_t>(w) & (kPfRows == 32 ? ~0u : ((1u << kPfRows) - 1u));
+    if (t2 == t_lo) sb &= ~1u;
+    const float om_lane = lane >= cnt ? 0.0f
+                          : lead_q0 ? sigmoid_floor(__uint_as_float(bt.q0))
+                                    : token_omega<ES>(p, b, t2 + lane, dg, G);
+    if (p.slot_index && lane < cnt)
+      p.slot_index[int64_t(u) * p.n + t2 + lane] = s + __popc(sb & ((2u << lane) - 1u));
+#pragma unroll
+    for (int j = 0; j < kPfRows; ++j) {
       if (j < cnt) {
         const int tj = t2 + j;
-        const int rel = tj - tlo;
-        const bool opens = tj != t0 && rel < 64 && ((m0 >> rel) & 1ull);
-        if (opens) {   // a new segment opens
+        if ((sb >> j) & 1u) {   // the next slot's segment opens
           flush();
           ++s;
           zs = 0.0f;
 #pragma unroll
           for (int e = 0; e < E; ++e) ak[e] = av[e] = 0.0f;
-        } else if (p.carry && tj != t0 && (tj & 31) == 0) {
+        } else if (p.carry && tj != t_lo && (tj & 31) == 0) {
           float *cr = p.carry + (int64_t(u) * p.carry_blocks + (tj >> 5)) * carry_stride(D);
 #pragma unroll
           for (int e = 0; e < E; ++e) {
@@ -1424,19 +1609,35 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(PrefillParams 
           }
           if (lane == 0) cr[2 * D] = zs;
         }
+        const float om = __shfl(om_lane, j, 64);
+        float kf[E], vf[E];
+        bt.kr[j].unpack(kf);
+        bt.vr[j].unpack(vf);
+        if (lane == 0) kf[0] = 0.0f;   // k_t[0] <- 0
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const float kv = (lane * E + e == 0) ? 0.0f : kk[j][e];  // k_t[0] <- 0
-          ak[e] = fmaf(ww[j], kv, ak[e]);
-          av[e] = fmaf(ww[j], vv[j][e], av[e]);
+          ak[e] = fmaf(om, kf[e], ak[e]);
+          av[e] = fmaf(om, vf[e], av[e]);
         }
-        zs += ww[j];
-        if (p.slot_index && lane == 0) p.slot_index[int64_t(u) * p.n + tj] = s;
+        zs += om;
+      }
+    }
+  };
+  Batch ring[kPfBuf];
+#pragma unroll
+  for (int j = 0; j < kPfBuf - 1; ++j)
+    if (j < nbat) issue(j, ring[j]);
+  for (int bi = 0; bi < nbat; bi += kPfBuf) {
+#pragma unroll
+    for (int j = 0; j < kPfBuf; ++j) {
+      if (bi + j < nbat) {
+        if (bi + j + kPfBuf - 1 < nbat) issue(bi + j + kPfBuf - 1, ring[(j + kPfBuf - 1) % kPfBuf]);
+        consume(bi + j, ring[j]);
       }
     }
   }
-  flush();
-  if (t_stop >= nb && lane == 0) p.z[u] = zs;   // the unit's last segment
+  flush();   // slot s_hi - 1
+  if (s_hi == l && lane == 0) p.z[u] = zs;   // the unit's last segment
 }
 
 // Pass 3 with window grouping (Sec. 3.3), one wave per (unit, 64-token
@@ -1776,8 +1977,14 @@ hipError_t decode_by_group(int group, const DecodeParams &p, int grid, bool vt, 
 
 template <int ES, int D>
 hipError_t prefill_impl(const PrefillParams &p, bool vt, hipStream_t s) {
+  // decisions and importances are staged for the passes that read them per
+  // token: prompt attention (carry records enabled) and window grouping
+  const bool stage = p.carry != nullptr || p.win.window > 0;
   if (p.n > 0) {
-    hipLaunchKernelGGL((prefill_decide_kernel<ES>), dim3(p.units), dim3(kThreads), 0, s, p);
+    if (stage)
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, true>), dim3(p.units), dim3(kThreads), 0, s, p);
+    else
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, false>), dim3(p.units), dim3(kThreads), 0, s, p);
   } else {
     hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(p.units)), dim3(kThreads), 0, s, p.len, 0,
                        size_t(p.units));
@@ -1789,16 +1996,29 @@ hipError_t prefill_impl(const PrefillParams &p, bool vt, hipStream_t s) {
                      p.log2p);
   e = hipGetLastError();
   if (e != hipSuccess || p.n == 0) return e;
-  const int nch = (p.n + 63) / 64;
-  if (p.win.window > 0)
+  if (p.win.window > 0) {
+    const int nch = (p.n + 63) / 64;
     hipLaunchKernelGGL((prefill_window_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
                        dim3(kThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL((prefill_reduce_kernel<ES, D>), dim3((nch + kWaves - 1) / kWaves, p.units),
-                       dim3(kThreads), 0, s, p);
-  e = hipGetLastError();
-  if (e != hipSuccess || !vt) return e;
-  return launch_transpose<D>(p.pool, p.page_bytes, p.ctrl, s);
+    e = hipGetLastError();
+    if (e != hipSuccess || !vt) return e;
+    return launch_transpose<D>(p.pool, p.page_bytes, p.ctrl, s);
+  }
+  // items of S_u >= l_u kItemTokens / n slots: at most ceil(n / kItemTokens)
+  // per unit, and at most ceil(n / 32) (S_u >= 32, l_u <= n)
+  const int items = std::min((p.n + kItemTokens - 1) / kItemTokens, (p.n + 31) / 32);
+  const int64_t waves = int64_t(p.units) * items;
+  const int blocks = static_cast<int>((waves + kWaves - 1) / kWaves);
+  if constexpr (ES == 2) {
+    if (vt) {
+      hipLaunchKernelGGL((prefill_pages_kernel<ES, D, true>), dim3(blocks), dim3(kThreads), 0, s, p,
+                         items);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((prefill_pages_kernel<ES, D, false>), dim3(blocks), dim3(kThreads), 0, s, p,
+                     items);
+  return hipGetLastError();
 }
 
 template <int ES, int D>
