@@ -67,6 +67,26 @@ constexpr size_t kMaxLdsPerWorkgroup = 160 * 1024;   // gfx950
 
 int elem_bytes(const dmc_cache_config &c) { return c.dtype == DMC_FP32 ? 4 : 2; }
 
+// Units per entry of the decode kernel's slot-space table in LDS: 1 (every
+// unit's offset) when that table fits beside the kernel's static LDS, else the
+// smallest power of two that makes it fit (exact caches; windowed ones need
+// 1); 0 if none up to kMaxSlotGroup does.
+int slot_group_for(const dmc_cache_config &c) {
+  const int64_t units = int64_t(c.batch) * c.num_kv_heads;
+  const int G = c.num_q_heads / c.num_kv_heads;
+  const bool v_trans = c.dtype == DMC_BF16 && G >= 4 && c.page_size == 32;
+  // windowed caches decode with the full table only
+  const int gmax = c.window > 0 ? 1 : dmc::kMaxSlotGroup;
+  for (int g = 1; g <= gmax; g <<= 1) {
+    const int entries = static_cast<int>((units + g - 1) / g + 1);
+    const size_t dyn = dmc::decode_lds_bytes(entries, G, c.head_dim, c.window > 0);
+    if (dyn <= kMaxDecodeLds &&
+        dyn + dmc::decode_static_lds_bytes(c.head_dim, v_trans) <= kMaxLdsPerWorkgroup)
+      return g;
+  }
+  return 0;
+}
+
 dmc_status validate_config(const dmc_cache_config *c) {
   if (!c) return fail(DMC_ERR_INVALID_ARG, "config is NULL");
   if (c->num_layers < 1 || c->batch < 1 || c->num_kv_heads < 1 || c->num_q_heads < 1)
@@ -103,13 +123,12 @@ dmc_status validate_config(const dmc_cache_config *c) {
     return fail(DMC_ERR_INVALID_ARG, "max_prompt_len must be in [0, max_slots_per_seq]");
   const int64_t units = int64_t(c->batch) * c->num_kv_heads;
   if (units > (int64_t(1) << 20)) return fail(DMC_ERR_UNSUPPORTED, "too many units per layer");
-  const size_t dyn_lds = dmc::decode_lds_bytes(static_cast<int>(units), G, c->head_dim, c->window > 0);
-  const bool v_trans = c->dtype == DMC_BF16 && G >= 4 && c->page_size == 32;
-  if (dyn_lds > kMaxDecodeLds ||
-      dyn_lds + dmc::decode_static_lds_bytes(c->head_dim, v_trans) > kMaxLdsPerWorkgroup)
+  if (slot_group_for(*c) == 0)
     return fail(DMC_ERR_UNSUPPORTED,
-                "batch * num_kv_heads = %lld units exceed the decode kernel's LDS tile table",
-                static_cast<long long>(units));
+                "batch * num_kv_heads = %lld units exceed the decode kernel's LDS slot-space table "
+                "(%s)", static_cast<long long>(units),
+                c->window > 0 ? "a windowed cache keeps one entry per unit"
+                              : "even at 64 units per entry");
   return DMC_OK;
 }
 
@@ -132,6 +151,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   L.prompt_chunks = (L.max_prompt + 63) / 64;
   L.carry_blocks = (L.max_prompt + 31) / 32;
   L.window = c.window;
+  L.slot_group = slot_group_for(c);
   L.page_bytes = int64_t(2) * c.page_size * c.head_dim * es;
   // Grouped-query caches decode on matrix cores with value pages transposed.
   L.v_trans = c.dtype == DMC_BF16 && L.group >= 4 && c.page_size == 32;
@@ -346,6 +366,7 @@ dmc_status decode_params(dmc_cache *cache, int32_t layer, const void *q, const v
   p.split_tile = L.split_tile;
   p.omega_src = c.omega_src;
   p.decision_src = c.decision_src;
+  p.slot_group = L.slot_group;
   return DMC_OK;
 }
 

@@ -42,6 +42,7 @@ struct Layout {
   int32_t prompt_chunks;  // ceil(max_prompt / 64)
   int32_t carry_blocks;   // ceil(max_prompt / 32)
   int32_t window;         // window-grouping width (0 = exact Algorithm 1)
+  int32_t slot_group;     // units per entry of the decode's slot-space table in LDS
   bool v_trans;           // value pages stored transposed (matrix-core decode)
 };
 
@@ -76,6 +77,7 @@ struct DecodeParams {
   float c;                 // decision bias
   float scale_log2;        // log2(e) / sqrt(d)
   int32_t units, hkv, hq, maxpages, max_slots, log2p, split_tile, omega_src, decision_src;
+  int32_t slot_group;      // units per entry of the slot-space table in LDS (1, or 2..64)
 };
 
 struct PrefillParams {
@@ -215,9 +217,12 @@ constexpr int kPromptMaxPages = 1024;
 hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt,
                                 const PromptParams &p, const Control *ctrl, hipStream_t s);
 
-// Dynamic LDS bytes of the decode kernel for a unit count / group / head dim
-// (and whether the cache has a window).
-size_t decode_lds_bytes(int units, int group, int head_dim, bool window);
+// Dynamic LDS bytes of the decode kernel for a slot-space table of
+// `table_entries` ints (ceil(units / slot_group) + 1) / group / head dim (and
+// whether the cache has a window).
+size_t decode_lds_bytes(int table_entries, int group, int head_dim, bool window);
+// Largest units per slot-space table entry.
+constexpr int kMaxSlotGroup = 64;
 // Static LDS of the decode kernel that runs such a cache (matrix-core kernel:
 // its chunk ring and staging rows).
 size_t decode_static_lds_bytes(int head_dim, bool v_trans);

@@ -64,6 +64,7 @@ namespace {
 #ifndef DMC_VALU_BUFFERS
 #define DMC_VALU_BUFFERS 3
 #endif
+constexpr int kRangesPerWave = 1;   // slot-space ranges per decode wave (2 and 3 measured slower)
 constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
 constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
 
@@ -167,9 +168,14 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float *a, float 
 // Slot space of a layer: unit u owns positions [off_u, off_u + n_u) with
 // n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
 // unit's open slot (or, for an empty unit, the slot its first token opens).
-// Every workgroup builds the exclusive prefix s_off[0..U] in LDS and gets S.
+// Every workgroup builds the exclusive prefix in LDS and gets S.  The table
+// holds every unit's offset (s_off[0..U]); layers whose full table would not
+// fit in LDS run the GRP kernels, which keep only every g-th entry (g =
+// p.slot_group, a power of two <= 64): s_off[j] = off of unit j g, for
+// j <= NG = ceil(U / g), s_off[NG] = S.
+template <bool GRP>
 __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_off, int *s_wsum) {
-  const int U = p.units;
+  const int U = p.units, g = GRP ? p.slot_group : 1, NG = (U + g - 1) / g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   constexpr int kBatch = 8;     // coalesced loads in flight per thread
   for (int i0 = 0; i0 < U; i0 += kThreads * kBatch) {
@@ -181,13 +187,15 @@ __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_of
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      const int i = i0 + j * kThreads + tid;
-      if (i < U) s_off[i] = max(v[j], 1);
+      const int i = i0 + j * kThreads + tid;   // units of a wave are 64 consecutive ones
+      int n = i < U ? max(v[j], 1) : 0;
+      for (int o = 1; o < g; o <<= 1) n += __shfl_xor(n, o, 64);   // sum over the g-unit group
+      if (i < U && (i & (g - 1)) == 0) s_off[i / g] = n;
     }
   }
   __syncthreads();
-  const int per = (U + kThreads - 1) / kThreads;
-  const int i0 = min(tid * per, U), i1 = min(i0 + per, U);
+  const int per = (NG + kThreads - 1) / kThreads;
+  const int i0 = min(tid * per, NG), i1 = min(i0 + per, NG);
   int sum = 0;
   for (int i = i0; i < i1; ++i) sum += s_off[i];
   int incl = sum;
@@ -208,22 +216,38 @@ __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_of
     s_off[i] = run;
     run += n;
   }
-  if (tid == 0) s_off[U] = total;
+  if (tid == 0) s_off[NG] = total;
   __syncthreads();
-  return s_off[U];
+  return s_off[NG];
 }
 
-// Unit holding slot-space position pos (s_off[u] <= pos < s_off[u + 1]).
-__device__ __forceinline__ int unit_at(const int *s_off, int U, int pos) {
-  int lo = 0, hi = U - 1;
+// Unit holding slot-space position pos (off_u <= pos < off_u + n_u); its
+// offset goes to `off`.  Grouped tables: the group by binary search, then the
+// unit inside it from the group's lengths (one wave-wide load, a scan).
+template <bool GRP>
+__device__ __forceinline__ int unit_at(const DecodeParams &p, const int *s_off, int pos, int &off) {
+  const int U = p.units, g = GRP ? p.slot_group : 1, NG = (U + g - 1) / g;
+  int lo = 0, hi = NG - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (s_off[mid] <= pos) lo = mid; else hi = mid - 1;
   }
-  return lo;
+  off = s_off[lo];
+  if (!GRP) return lo;
+  const int lane = threadIdx.x & 63, u0 = lo * g;
+  const int n = (lane < g && u0 + lane < U) ? max(p.len_in[u0 + lane], 1) : 0;
+  int incl = n;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  const int jl = __ffsll(static_cast<long long>(__ballot(lane < g && off + incl > pos))) - 1;
+  off += __shfl(incl - n, jl, 64);
+  return u0 + jl;
 }
 
-template <int ES, int D, int G, bool WIN>
+template <int ES, int D, int G, bool WIN, bool GRP>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   using V = V16<ES>;
   constexpr int VN = V::N;        // elements per 16-byte lane chunk
@@ -237,8 +261,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
 
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_wsum[kWaves];
-  const int U = p.units;
-  int *s_off = reinterpret_cast<int *>(smem);   // [U + 1] unit offsets in the slot space
+  int *s_off = reinterpret_cast<int *>(smem);   // slot-space table (build_slot_space)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane / LPR, part = lane % LPR;
@@ -246,17 +269,19 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int CS = P < kValuChunk ? P : kValuChunk;
   const int log2cs = p.log2p < kLog2Chunk ? p.log2p : kLog2Chunk;
 
-  const int S = build_slot_space(p, s_off, s_wsum);
+  const int S = build_slot_space<GRP>(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
-  int span = (S + nwaves - 1) / nwaves;          // equal share of actual slots per range
+  int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);   // equal shares
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
   const int nranges = (S + span - 1) / span;
 
   for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
     int pos = r * span;
     const int pos_end = min(pos + span, S);
-    for (int u = unit_at(s_off, U, pos); pos < pos_end; ++u) {
-      const int off = s_off[u], n_u = s_off[u + 1] - off;
+    int off;   // the piece's unit's offset; a later piece of the range starts its unit
+    for (int u = unit_at<GRP>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
+      if constexpr (!GRP) off = s_off[u];
+      const int n_u = GRP ? max(p.len_in[u], 1) : s_off[u + 1] - off;
       const int start = pos - off;
       const int stop = min(pos_end, off + n_u) - off;   // this piece: [start, stop)
       pos = off + stop;
@@ -646,7 +671,7 @@ constexpr int mfma_stage_bytes() { return kWaves * 2 * D * 2; }
 template <int D>
 constexpr int mfma_decode_wg_per_cu() { return D == 128 ? 1 : 2; }
 
-template <int D, int G, bool WIN>
+template <int D, int G, bool WIN, bool GRP>
 __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_mfma_kernel(DecodeParams p) {
   constexpr int KS = D / 32;      // k-steps of the score product
   constexpr int NT = D / 16;      // 16-dim tiles of the value product
@@ -663,24 +688,27 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
   __shared__ __align__(16) unsigned char s_ring[mfma_ring_bytes<D>() + mfma_stage_bytes<D>()];
   const int U = p.units;
   int *s_off = reinterpret_cast<int *>(smem);
-  const size_t win_lds_off = align_up(size_t(U + 1) * 4, 16);   // windowed means, 2 D fp32 per wave
+  const int ng = GRP ? (U + p.slot_group - 1) / p.slot_group : U;   // slot-space table entries - 1
+  const size_t win_lds_off = align_up(size_t(ng + 1) * 4, 16);   // windowed means, 2 D fp32 per wave
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, q = lane >> 4;      // MFMA column (head or dim) and k-group
   const int P = 1 << p.log2p;
   const int krow = 8 * (n >> 2) + (n & 3);     // this lane's key row in score tile 0 (+4 in tile 1)
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
-  const int S = build_slot_space(p, s_off, s_wsum);
+  const int S = build_slot_space<GRP>(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
-  int span = (S + nwaves - 1) / nwaves;
+  int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
   const int nranges = (S + span - 1) / span;
 
   for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
     int pos = r * span;
     const int pos_end = min(pos + span, S);
-    for (int u = unit_at(s_off, U, pos); pos < pos_end; ++u) {
-      const int off = s_off[u], n_u = s_off[u + 1] - off;
+    int off;
+    for (int u = unit_at<GRP>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
+      if constexpr (!GRP) off = s_off[u];
+      const int n_u = GRP ? max(p.len_in[u], 1) : s_off[u + 1] - off;
       const int start = pos - off;
       const int stop = min(pos_end, off + n_u) - off;
       pos = off + stop;
@@ -1929,20 +1957,21 @@ hipError_t launch_transpose(char *pool, int64_t page_bytes, const Control *ctrl,
   return hipGetLastError();
 }
 
-template <int ES, int D, int G, bool WIN>
+template <int ES, int D, int G, bool WIN, bool GRP>
 void launch_decode_kernel(const DecodeParams &p, int grid, bool vt, size_t lds, hipStream_t s) {
   if constexpr (ES == 2 && G >= 4) {
     if (vt) {
-      hipLaunchKernelGGL((decode_mfma_kernel<D, G, WIN>), dim3(grid), dim3(kThreads), lds, s, p);
+      hipLaunchKernelGGL((decode_mfma_kernel<D, G, WIN, GRP>), dim3(grid), dim3(kThreads), lds, s, p);
       return;
     }
   }
-  hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN>), dim3(grid), dim3(kThreads), lds, s, p);
+  hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN, GRP>), dim3(grid), dim3(kThreads), lds, s, p);
 }
 
 template <int ES, int D, int G>
 hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) {
-  const size_t lds = decode_lds_bytes(p.units, G, D, p.win.window > 0);
+  const size_t lds = decode_lds_bytes((p.units + p.slot_group - 1) / p.slot_group + 1, G, D,
+                                      p.win.window > 0);
   if (vt && !(ES == 2 && G >= 4)) return hipErrorInvalidValue;
   // The matrix-core kernel adds its chunk ring to the LDS of a workgroup.  When
   // two such workgroups do not fit a compute unit (always at d = 128), the grid
@@ -1950,10 +1979,14 @@ hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) 
   constexpr size_t kLdsPerCu = 160 * 1024;
   if (vt && 2 * (lds + mfma_ring_bytes<D>() + mfma_stage_bytes<D>() + 64) > kLdsPerCu && grid > 1)
     grid /= 2;
+  // grouped slot-space tables are built for exact (window-free) caches only
+  if (p.win.window > 0 && p.slot_group > 1) return hipErrorInvalidValue;
   if (p.win.window > 0)
-    launch_decode_kernel<ES, D, G, true>(p, grid, vt, lds, s);
+    launch_decode_kernel<ES, D, G, true, false>(p, grid, vt, lds, s);
+  else if (p.slot_group > 1)
+    launch_decode_kernel<ES, D, G, false, true>(p, grid, vt, lds, s);
   else
-    launch_decode_kernel<ES, D, G, false>(p, grid, vt, lds, s);
+    launch_decode_kernel<ES, D, G, false, false>(p, grid, vt, lds, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int batch = p.units / p.hkv;
@@ -2049,11 +2082,11 @@ hipError_t export_impl(const DenseParams &p, bool vt, hipStream_t s) {
 
 }  // namespace
 
-size_t decode_lds_bytes(int units, int group, int head_dim, bool window) {
+size_t decode_lds_bytes(int table_entries, int group, int head_dim, bool window) {
   (void)group;
-  // slot-space prefix [units + 1]; with a window, 2 * head_dim fp32 per wave
-  // for the matrix-core decode's windowed means
-  return align_up(size_t(units + 1) * 4, 16) + (window ? size_t(kWaves) * 2 * head_dim * 4 : 0);
+  // slot-space table; with a window, 2 * head_dim fp32 per wave for the
+  // matrix-core decode's windowed means
+  return align_up(size_t(table_entries) * 4, 16) + (window ? size_t(kWaves) * 2 * head_dim * 4 : 0);
 }
 
 size_t decode_static_lds_bytes(int head_dim, bool v_trans) {

@@ -74,21 +74,36 @@ def test_invalid_config(P, field, value, msg):
 
 
 def test_too_many_units_for_decode_table(P):
-    cfg = P.make_config(1, 4096, 8, 8, 128)
-    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(cfg)) == 0
+    """Layers whose slot-space table would not fit in LDS keep every g-th entry
+    (g up to 64); beyond that, and beyond 2^20 units, they are refused."""
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(P.make_config(1, 4096, 8, 8, 128))) > 0
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(P.make_config(1, 512, 32, 32, 128))) > 0
+    huge = P.make_config(1, 1 << 18, 8, 8, 64, max_slots_per_seq=8, num_pages=1024)   # 2^21 units
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(huge)) == 0
     assert "units" in P.binding.last_error()
+
+
+def test_windowed_cache_needs_the_full_table(P):
+    big = P.make_config(1, 512, 32, 32, 128, window=12)       # 16384 units: over 64 KB with the
+                                                              # windowed means beside the table
+    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(big)) == 0
+    assert "units" in P.binding.last_error()
+    assert P.binding.lib.dmc_cache_workspace_bytes(
+        ctypes.byref(P.make_config(1, 470, 32, 32, 128, window=12))) > 0
 
 
 def test_matrix_core_cache_unit_limit(P):
     """bf16 grouped-query caches (G >= 4, 32-slot pages) decode with a 128 KB
-    chunk ring in LDS at d = 128, which leaves room for the slot-space table of
-    about 7600 units; the same shapes in fp32 run the vector kernel."""
-    ok = P.make_config(1, 950, 64, 8, 128, "bf16")        # 7600 units
-    assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(ok)) > 0
-    big = P.make_config(1, 1024, 64, 8, 128, "bf16")      # 8192 units
+    chunk ring in LDS at d = 128; the slot-space table beside it holds about
+    7600 entries, i.e. up to 7600 units with one entry each, and up to 64
+    times that with grouped entries.  fp32 caches run the vector kernel."""
+    for batch in (950, 1024, 60000):                          # 7600, 8192, 480000 units
+        cfg = P.make_config(1, batch, 64, 8, 128, "bf16", max_slots_per_seq=8, num_pages=1024)
+        assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(cfg)) > 0, batch
+    big = P.make_config(1, 62000, 64, 8, 128, "bf16", max_slots_per_seq=8, num_pages=1024)
     assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(big)) == 0
     assert "units" in P.binding.last_error()
-    vec = P.make_config(1, 1024, 64, 8, 128, "fp32")
+    vec = P.make_config(1, 62000, 64, 8, 128, "fp32", max_slots_per_seq=8, num_pages=1024)
     assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(vec)) > 0
 
 
