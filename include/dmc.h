@@ -229,7 +229,7 @@ dmc_status dmc_decode_step(dmc_cache *cache, int32_t layer, const void *q_dev,
  *   Limit: a launch of this cache needs units * 8 bytes (rounded up to 256)
  *     plus (ranges + units) * G * (head_dim + 4) * 4 bytes of records, ranges
  *     being the launch's waves (2048 on a 256-CU MI355X) or, with a split_tile,
- *     ceil(units * max_slots_per_seq / split_tile) if that is larger; a
+ *     ceil(units * (max_slots_per_seq + 32) / split_tile) if that is larger; a
  *     cache that needs more returns DMC_ERR_UNSUPPORTED before anything is
  *     enqueued.
  *   Nothing in the array has to start at zero: every record a call reads is

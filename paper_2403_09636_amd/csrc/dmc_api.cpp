@@ -142,7 +142,7 @@ dmc::Layout make_layout(const dmc_cache_config &c) {
   {
     // ranges <= max(waves, ceil(S / split_tile)) with S <= U * max_slots; one
     // record per (range, unit) piece is indexed range + unit.
-    const int64_t S = int64_t(L.units) * c.max_slots_per_seq;
+    const int64_t S = int64_t(L.units) * (c.max_slots_per_seq + dmc::kDecodeUnitOverhead);
     int64_t ranges = kMaxDecodeWaves;
     if (c.split_tile > 0) ranges = std::max<int64_t>(ranges, (S + c.split_tile - 1) / c.split_tile);
     L.max_records = ranges + L.units + 1;
@@ -381,12 +381,13 @@ dmc_status decode_launch(dmc_cache *cache, const dmc::DecodeParams &p, dmc_strea
 // Bytes of split-K records one decode launch of this cache can use: the
 // per-unit table (first record, count) and one record of G x (d + 4) fp32 per
 // (range, unit) piece, indexed range + unit.  Ranges are at most the launch's
-// waves, or ceil(S / split_tile) with S <= units * max_slots_per_seq.
+// waves, or ceil(S / split_tile) with S <= units * (max_slots_per_seq + the
+// decode kernels' virtual positions per unit).
 size_t decode_records_bytes(const dmc_cache *cache, size_t *meta_bytes) {
   const dmc::Layout &L = cache->lay;
   int64_t ranges = int64_t(decode_grid(cache)) * 4;
   if (L.split_tile > 0) {
-    const int64_t S = int64_t(L.units) * cache->cfg.max_slots_per_seq;
+    const int64_t S = int64_t(L.units) * (cache->cfg.max_slots_per_seq + dmc::kDecodeUnitOverhead);
     ranges = std::max<int64_t>(ranges, (S + L.split_tile - 1) / L.split_tile);
   }
   *meta_bytes = align_up(size_t(L.units) * 2 * 4, 256);

@@ -223,6 +223,9 @@ hipError_t launch_prompt_attend(int elem_bytes, int head_dim, int group, bool vt
 size_t decode_lds_bytes(int table_entries, int group, int head_dim, bool window);
 // Largest units per slot-space table entry.
 constexpr int kMaxSlotGroup = 64;
+// Largest number of virtual slot-space positions a decode kernel appends to a
+// unit (bounds the split-K ranges: S <= units * (max_slots_per_seq + this)).
+constexpr int kDecodeUnitOverhead = 32;
 // Static LDS of the decode kernel that runs such a cache (matrix-core kernel:
 // its chunk ring and staging rows).
 size_t decode_static_lds_bytes(int head_dim, bool v_trans);

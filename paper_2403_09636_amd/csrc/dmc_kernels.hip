@@ -65,6 +65,16 @@ namespace {
 #define DMC_VALU_BUFFERS 3
 #endif
 constexpr int kRangesPerWave = 1;   // slot-space ranges per decode wave (2 and 3 measured slower)
+// Virtual positions appended to every unit in the slot space, standing for a
+// piece's fixed cost (its page-table and first-chunk round trips, the owner's
+// update), so that equal ranges carry equal cost rather than equal slots:
+// 32 for the vector-ALU decode (7B stack 180.5 -> 178.9 us per call; 16 and
+// 64 in between), none for the matrix-core decode, whose ranges span about
+// two units of 2000+ slots (no change measured).  At most kDecodeUnitOverhead.
+constexpr int kValuUnitOverhead = 32;
+constexpr int kMfmaUnitOverhead = 0;
+static_assert(kValuUnitOverhead <= kDecodeUnitOverhead && kMfmaUnitOverhead <= kDecodeUnitOverhead,
+              "slot-space overhead bound");
 constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
 constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
 
@@ -166,14 +176,16 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float *a, float 
 
 
 // Slot space of a layer: unit u owns positions [off_u, off_u + n_u) with
-// n_u = max(l_u, 1) (pre-step lengths); position off_u + n_u - 1 is the
-// unit's open slot (or, for an empty unit, the slot its first token opens).
+// n_u = max(l_u, 1) + OVH (pre-step lengths, OVH virtual positions for the
+// piece's fixed cost); position off_u + max(l_u, 1) - 1 is the unit's open
+// slot (or, for an empty unit, the slot its first token opens), and the piece
+// holding the unit's last position owns it.
 // Every workgroup builds the exclusive prefix in LDS and gets S.  The table
 // holds every unit's offset (s_off[0..U]); layers whose full table would not
 // fit in LDS run the GRP kernels, which keep only every g-th entry (g =
 // p.slot_group, a power of two <= 64): s_off[j] = off of unit j g, for
 // j <= NG = ceil(U / g), s_off[NG] = S.
-template <bool GRP>
+template <bool GRP, int OVH>
 __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_off, int *s_wsum) {
   const int U = p.units, g = GRP ? p.slot_group : 1, NG = (U + g - 1) / g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -188,7 +200,7 @@ __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_of
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int i = i0 + j * kThreads + tid;   // units of a wave are 64 consecutive ones
-      int n = i < U ? max(v[j], 1) : 0;
+      int n = i < U ? max(v[j], 1) + OVH : 0;
       for (int o = 1; o < g; o <<= 1) n += __shfl_xor(n, o, 64);   // sum over the g-unit group
       if (i < U && (i & (g - 1)) == 0) s_off[i / g] = n;
     }
@@ -224,7 +236,7 @@ __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_of
 // Unit holding slot-space position pos (off_u <= pos < off_u + n_u); its
 // offset goes to `off`.  Grouped tables: the group by binary search, then the
 // unit inside it from the group's lengths (one wave-wide load, a scan).
-template <bool GRP>
+template <bool GRP, int OVH>
 __device__ __forceinline__ int unit_at(const DecodeParams &p, const int *s_off, int pos, int &off) {
   const int U = p.units, g = GRP ? p.slot_group : 1, NG = (U + g - 1) / g;
   int lo = 0, hi = NG - 1;
@@ -235,7 +247,7 @@ __device__ __forceinline__ int unit_at(const DecodeParams &p, const int *s_off, 
   off = s_off[lo];
   if (!GRP) return lo;
   const int lane = threadIdx.x & 63, u0 = lo * g;
-  const int n = (lane < g && u0 + lane < U) ? max(p.len_in[u0 + lane], 1) : 0;
+  const int n = (lane < g && u0 + lane < U) ? max(p.len_in[u0 + lane], 1) + OVH : 0;
   int incl = n;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -269,7 +281,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int CS = P < kValuChunk ? P : kValuChunk;
   const int log2cs = p.log2p < kLog2Chunk ? p.log2p : kLog2Chunk;
 
-  const int S = build_slot_space<GRP>(p, s_off, s_wsum);
+  constexpr int OVH = kValuUnitOverhead;
+  const int S = build_slot_space<GRP, OVH>(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
   int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);   // equal shares
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
@@ -279,9 +292,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     int pos = r * span;
     const int pos_end = min(pos + span, S);
     int off;   // the piece's unit's offset; a later piece of the range starts its unit
-    for (int u = unit_at<GRP>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
+    for (int u = unit_at<GRP, OVH>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
       if constexpr (!GRP) off = s_off[u];
-      const int n_u = GRP ? max(p.len_in[u], 1) : s_off[u + 1] - off;
+      const int n_u = GRP ? max(p.len_in[u], 1) + OVH : s_off[u + 1] - off;
       const int start = pos - off;
       const int stop = min(pos_end, off + n_u) - off;   // this piece: [start, stop)
       pos = off + stop;
@@ -289,7 +302,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
       const int l = p.len_in[u];
       const int b = u / p.hkv, g = u - b * p.hkv;
       const int64_t pt = int64_t(u) * p.maxpages;
-      int end = owner ? n_u - 1 : stop;                 // closed slots [start, end)
+      // closed slots [start, end): the open slot and the virtual tail are not streamed
+      int end = min(owner ? n_u - 1 : stop, n_u - OVH - 1);
 
       // The unit's query heads (this lane's slice), element 0 zeroed.  Scores
       // are scaled by log2(e)/sqrt(d) after the row sum.
@@ -696,7 +710,8 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
   const int krow = 8 * (n >> 2) + (n & 3);     // this lane's key row in score tile 0 (+4 in tile 1)
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
-  const int S = build_slot_space<GRP>(p, s_off, s_wsum);
+  constexpr int OVH = kMfmaUnitOverhead;
+  const int S = build_slot_space<GRP, OVH>(p, s_off, s_wsum);
   const int nwaves = gridDim.x * kWaves;
   int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
@@ -706,9 +721,9 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
     int pos = r * span;
     const int pos_end = min(pos + span, S);
     int off;
-    for (int u = unit_at<GRP>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
+    for (int u = unit_at<GRP, OVH>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
       if constexpr (!GRP) off = s_off[u];
-      const int n_u = GRP ? max(p.len_in[u], 1) : s_off[u + 1] - off;
+      const int n_u = GRP ? max(p.len_in[u], 1) + OVH : s_off[u + 1] - off;
       const int start = pos - off;
       const int stop = min(pos_end, off + n_u) - off;
       pos = off + stop;
@@ -716,7 +731,7 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
       const int l = p.len_in[u];
       const int b = u / p.hkv, g = u - b * p.hkv;
       const int64_t pt = int64_t(u) * p.maxpages;
-      const int end = owner ? n_u - 1 : stop;          // closed slots [start, end)
+      const int end = min(owner ? n_u - 1 : stop, n_u - OVH - 1);   // closed slots
 
       // Q^T operand: lane (n, q) holds Q[head n][32 ks + 8q .. +8]; heads >= G are 0.
       uint4 qb[KS];
