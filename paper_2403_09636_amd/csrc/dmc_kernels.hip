@@ -676,9 +676,6 @@ __device__ __forceinline__ int key_perm(int r) {
 
 template <int D>
 constexpr int mfma_ring_bytes() { return kWaves * 2 * 2 * 32 * D * 2; }   // 2 slots per wave
-// Per-wave staging rows of the owner's current key and value (after the ring).
-template <int D>
-constexpr int mfma_stage_bytes() { return kWaves * 2 * D * 2; }
 
 // Occupancy: at d = 128 the chunk ring (128 KB) leaves room for one workgroup
 // per compute unit (one wave per SIMD); at d = 64 two fit.
@@ -699,7 +696,10 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
 
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_wsum[kWaves];
-  __shared__ __align__(16) unsigned char s_ring[mfma_ring_bytes<D>() + mfma_stage_bytes<D>()];
+  // The chunk ring: slot 0 and slot 1 of every wave in arrays of their own
+  // (see the LDS transfer helpers).
+  static_assert(mfma_ring_bytes<D>() == 2 * kWaves * 2 * CH, "ring layout");
+  __shared__ __align__(16) unsigned char s_ring0[kWaves * 2 * CH], s_ring1[kWaves * 2 * CH];
   const int U = p.units;
   int *s_off = reinterpret_cast<int *>(smem);
   const int ng = GRP ? (U + p.slot_group - 1) / p.slot_group : U;   // slot-space table entries - 1
@@ -802,12 +802,12 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
       };
 
       // Owner inputs are issued before the stream so that they arrive while it runs:
-      // k_t[0], q_t[0] of the deciding heads, z, the open slot's page, and the current
-      // key and value rows (copied into this wave's staging rows).
+      // k_t[0], q_t[0] of the deciding heads, z, the open slot's page, and the lane's
+      // parts of the current key and value rows (as B operand and value tiles).
       float k0 = 0.0f, q0 = 0.0f, zold = 0.0f;
       int open_page = -1;
-      const unsigned char *lst = s_ring + mfma_ring_bytes<D>() + wave * 2 * RB;
-      const int c_first = start >> 5;
+      uint4 kt[KS];
+      uint16_t vt[NT];
       if (owner) {
         const int dg = p.decision_src ? 0 : g;   // head whose neurons decide for this unit
         k0 = load_elem<2>(p.k, int64_t(b * p.hkv + dg) * D);
@@ -816,15 +816,22 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
           zold = p.z[u];
           open_page = p.ptab[pt + ((l - 1) >> p.log2p)];
         }
-        const uint32_t st = __builtin_amdgcn_readfirstlane(lds_offset(lst));
-        if (lane < RB / 16) {
-          dma16_s(st, uniform_ptr(static_cast<const char *>(p.k) + int64_t(u) * RB), lane * 16);
-          dma16_s(st + RB, uniform_ptr(static_cast<const char *>(p.v) + int64_t(u) * RB), lane * 16);
-        }
+        const char *kr = static_cast<const char *>(p.k) + int64_t(u) * RB;
+        const uint16_t *vr = reinterpret_cast<const uint16_t *>(static_cast<const char *>(p.v) +
+                                                                int64_t(u) * RB);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kt[ks] = ld16(kr + ks * 64 + q * 16);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) vt[nt] = vr[16 * nt + n];
       }
 
-      const int c_last = end > start ? (end - 1) >> 5 : -1;   // chunk left in the slot
-      const unsigned char *lk = s_ring + (wave * 2 + ((c_last - c_first) & 1)) * 2 * CH, *lv = lk + CH;
+      const int c_last = end > start ? (end - 1) >> 5 : -1;   // the piece's last chunk
+      // The owner's open slot: copied from the ring when its chunk streams by
+      // (the slot's last 32 rows are its page), else read from its page below.
+      const int so = (l - 1) & (P - 1);
+      const int c_open = (owner && l > 0 && ((l - 1) >> 5) == c_last) ? c_last : -1;
+      uint4 ko[KS];
+      uint16_t vo[NT];
       if (end > start) {
         const int c0 = start >> 5, c1 = c_last;
         auto range_of = [&](int ch, int &rlo, int &rhi) {
@@ -834,9 +841,8 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
         };
         // The whole chunk (one page: P == 32) is transferred; rows outside
         // [start, end) are page memory of this unit whose scores and values
-        // the validity bits mask.
-        const uint32_t slot_k0 =
-            __builtin_amdgcn_readfirstlane(lds_offset(s_ring) + wave * 4 * CH);
+        // the validity bits mask.  Every step issues the 2 NX transfers of
+        // the chunk two ahead (switched off past the piece's last chunk).
         // Page-table entries of the piece's chunks, one per lane, 64 chunks per batch with the
         // next batch loaded one batch ahead: no chunk transfer waits on a table lookup.
         int cb = c0;
@@ -850,18 +856,22 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
           }
           return __builtin_amdgcn_readlane(pcur, ch - cb);
         };
-        auto issue = [&](int ch, int sl) {
-          const uint32_t slot_k = slot_k0 + sl * 2 * CH, slot_v = slot_k + CH;
-          const char *pg = uniform_ptr(p.pool + int64_t(page_of(ch)) * p.page_bytes);
+        auto ring_slot = [&](auto sl_c) -> unsigned char * {
+          return (decltype(sl_c)::value ? s_ring1 : s_ring0) + wave * 2 * CH;
+        };
+        auto issue = [&](int ch, auto sl_c) {
+          const bool on = ch <= c1;
+          unsigned char *slot_k = ring_slot(sl_c), *slot_v = slot_k + CH;
+          const char *pg = uniform_ptr(p.pool + int64_t(page_of(min(ch, c1))) * p.page_bytes);
 #pragma unroll
           for (int i = 0; i < NX; ++i) {
             const int o = 1024 * i + 16 * lane, r = o / RB, c = (o % RB) / 16;
-            dma16_s_nt(slot_k + 1024 * i, pg, uint32_t(r * RB + 16 * (c ^ key_perm<CPR>(r))));
+            dma16_s_nt(slot_k + 1024 * i, pg, uint32_t(r * RB + 16 * (c ^ key_perm<CPR>(r))), on);
           }
 #pragma unroll
           for (int i = 0; i < NX; ++i) {
             const int r = 16 * i + (lane >> 2), c = lane & 3;
-            dma16_s_nt(slot_v + 1024 * i, pg + CH, uint32_t(r * 64 + 16 * (c ^ ((r >> 2) & 3))));
+            dma16_s_nt(slot_v + 1024 * i, pg + CH, uint32_t(r * 64 + 16 * (c ^ ((r >> 2) & 3))), on);
           }
         };
         auto bits = [&](int ch) -> uint32_t {
@@ -871,14 +881,12 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
           return hi_mask & ~((1u << rlo) - 1u);
         };
         uint4 ka[2][KS], va[NT];
-        issue(c0, 0);
-        if (c0 < c1) issue(c0 + 1, 1);
-        for (int ch = c0; ch <= c1; ++ch) {
-          const int sl = (ch - c0) & 1;
-          if (ch < c1) wait_vmcnt<2 * NX>();   // this chunk has landed; the next may be in flight
-          else wait_vmcnt<0>();
-          wave_lds_sync();
-          const unsigned char *ck = s_ring + (wave * 2 + sl) * 2 * CH, *cv = ck + CH;
+        issue(c0, std::integral_constant<int, 0>{});
+        issue(c0 + 1, std::integral_constant<int, 1>{});
+        auto step = [&](auto sl_c, int ch) {
+          wait_vmcnt<2 * NX>();   // this chunk has landed; the next may be in flight
+          wave_ring_sync();
+          const unsigned char *ck = ring_slot(sl_c), *cv = ck + CH;
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             const int rr = krow + 4 * t;
@@ -891,42 +899,37 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
           for (int nt = 0; nt < NT; ++nt)
             va[nt] = *reinterpret_cast<const uint4 *>(cv + (16 * nt + n) * 64 +
                                                       16 * (q ^ ((n >> 2) & 3)));
-          if (ch + 2 <= c1) {
-            wave_lds_sync();   // the slot's reads are done before it is refilled
-            issue(ch + 2, sl);
-          }
-          float sraw[8];
-          scores(ka, sraw);
-          values(sraw, va, bits(ch));
-        }
-      }
-
-      // Owner: the current rows from the staging area; the open slot from the chunk
-      // left in the slot when it is the open slot's page, else from its page.
-      int seg_len = 0;
-      uint4 kt[KS], ko[KS];
-      uint16_t vt[NT], vo[NT];
-      if (owner) {
-        if (WIN && l > 0) seg_len = p.win.seg_len[u];
-        wait_vmcnt<0>();
-        wave_lds_sync();
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kt[ks] = *reinterpret_cast<const uint4 *>(lst + ks * 64 + q * 16);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-          vt[nt] = *reinterpret_cast<const uint16_t *>(lst + RB + (16 * nt + n) * 2);
-        if (l > 0) {
-          const int so = (l - 1) & (P - 1);
-          if (((l - 1) >> 5) == c_last) {
+          if (ch == c_open) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
               ko[ks] = *reinterpret_cast<const uint4 *>(
-                  lk + so * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(so)));
+                  ck + so * RB + 16 * ((4 * ks + q) ^ key_perm<CPR>(so)));
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
               vo[nt] = *reinterpret_cast<const uint16_t *>(
-                  lv + (16 * nt + n) * 64 + 16 * ((so >> 3) ^ ((n >> 2) & 3)) + (so & 7) * 2);
-          } else {
+                  cv + (16 * nt + n) * 64 + 16 * ((so >> 3) ^ ((n >> 2) & 3)) + (so & 7) * 2);
+          }
+          wave_ring_sync();   // the slot's reads come before its refill
+          issue(ch + 2, sl_c);
+          if (ch > c1) return;   // past the piece's last chunk (odd count)
+          float sraw[8];
+          scores(ka, sraw);
+          values(sraw, va, bits(ch));
+        };
+        // Pairs of steps, one per slot (a step past the last chunk only keeps
+        // the transfer count in step).
+        for (int ch = c0; ch <= c1; ch += 2) {
+          step(std::integral_constant<int, 0>{}, ch);
+          step(std::integral_constant<int, 1>{}, ch + 1);
+        }
+      }
+
+      // Owner: the open slot copied from the ring above, else from its page.
+      int seg_len = 0;
+      if (owner) {
+        if (WIN && l > 0) seg_len = p.win.seg_len[u];
+        if (l > 0) {
+          if (c_open < 0) {
             const char *pg = p.pool + int64_t(open_page) * p.page_bytes;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) ko[ks] = ld16(pg + int64_t(so) * RB + ks * 64 + q * 16);
@@ -1992,7 +1995,7 @@ hipError_t decode_impl(const DecodeParams &p, int grid, bool vt, hipStream_t s) 
   // two such workgroups do not fit a compute unit (always at d = 128), the grid
   // is halved so that every workgroup is resident at once.
   constexpr size_t kLdsPerCu = 160 * 1024;
-  if (vt && 2 * (lds + mfma_ring_bytes<D>() + mfma_stage_bytes<D>() + 64) > kLdsPerCu && grid > 1)
+  if (vt && 2 * (lds + mfma_ring_bytes<D>() + 64) > kLdsPerCu && grid > 1)
     grid /= 2;
   // grouped slot-space tables are built for exact (window-free) caches only
   if (p.win.window > 0 && p.slot_group > 1) return hipErrorInvalidValue;
@@ -2106,8 +2109,7 @@ size_t decode_lds_bytes(int table_entries, int group, int head_dim, bool window)
 
 size_t decode_static_lds_bytes(int head_dim, bool v_trans) {
   if (!v_trans) return 64;
-  return head_dim == 128 ? mfma_ring_bytes<128>() + mfma_stage_bytes<128>() + 64
-                         : mfma_ring_bytes<64>() + mfma_stage_bytes<64>() + 64;
+  return head_dim == 128 ? mfma_ring_bytes<128>() + 64 : mfma_ring_bytes<64>() + 64;
 }
 
 hipError_t launch_fill_i32(int32_t *p, int32_t value, size_t count, hipStream_t s) {

@@ -43,44 +43,90 @@ __device__ __forceinline__ uint32_t lds_offset(const void *p) {
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char *)p));
 }
 
-// 16 bytes per lane from global memory straight into LDS at
-// lds_base + 16 * lane (lds_base wave-uniform), by the compiler's
-// global_load_lds builtin: the compiler sets m0 from lds_base itself and
-// inserts no wait for the transfer, so completion is awaited explicitly with
-// wait_vmcnt before the LDS is read.  aux carries the cache-policy bits
+// Direct global -> LDS transfers: each lane's 16 (or 4, 2) bytes land at
+// lds + BYTES * lane, lds wave-uniform (the compiler moves it into m0).  lds
+// must point into a __shared__ array: the compiler then knows which array a
+// transfer writes and, before each later LDS access of this wave, waits only
+// for the transfers into the array accessed (its own vmcnt bookkeeping).  The
+// kernels keep every ring slot in an array of its own and issue a fixed
+// number of transfers per step (a transfer past the data is switched off,
+// not skipped), so that reading one slot does not wait for the transfers in
+// flight into the others.  Across waves, completion is awaited explicitly:
+// wait_vmcnt, then ring_barrier.  aux carries the cache-policy bits
 // (kNontemporal for data streamed once).
 constexpr int kCachePolicyDefault = 0;
 constexpr int kNontemporal = 2;   // nt (sc0 | nt and sc1 | nt measured the same)
+constexpr uint32_t kOutOfRange = 0x80000000u;   // a lane offset past every buffer range
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef const __attribute__((address_space(1))) char global_cchar_t;
 
+// Per-lane 64-bit global addresses (the compiler cannot attribute these to
+// a slot as precisely; used where every transfer is awaited before the LDS
+// is read).
 template <int AUX = kCachePolicyDefault>
-__device__ __forceinline__ void dma16(uint32_t lds_base, const void *g) {
-  __builtin_amdgcn_global_load_lds((global_cchar_t *)g, (lds_void_t *)(size_t)lds_base, 16, 0, AUX);
+__device__ __forceinline__ void dma16(void *lds, const void *g) {
+  __builtin_amdgcn_global_load_lds((global_cchar_t *)g, (lds_void_t *)lds, 16, 0, AUX);
 }
 
-// Same, with a wave-uniform 64-bit base (SGPRs, see uniform_ptr) and a 32-bit
-// per-lane offset, by the buffer form of the transfer: the base goes into a
-// raw buffer resource (SGPRs; stride 0, no practical bound) and the lane's
-// offset stays one 32-bit VGPR.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const char *sbase) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(sbase), static_cast<short>(0),
-                                           0x7fffffff, 0x00020000);
+// A wave-uniform 64-bit base (SGPRs, see uniform_ptr) and a 32-bit per-lane
+// offset, by the buffer form of the transfer: the base goes into a raw
+// buffer resource (stride 0, range 2^31 - 1 bytes, or 0 when the transfer is
+// off: then every lane is out of range and nothing is read).  A lane offset
+// of kOutOfRange switches that lane off alone.  Out-of-range lanes read no
+// memory; what their LDS bytes then hold is not relied upon.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const char *sbase, bool on = true) {
+  // on is wave-uniform: made visibly so, else the compiler loops over lanes
+  const int range = __builtin_amdgcn_readfirstlane(on ? 0x7fffffff : 0);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(sbase), static_cast<short>(0), range,
+                                           0x00020000);
 }
-template <int AUX = kCachePolicyDefault>
-__device__ __forceinline__ void dma16_so(uint32_t lds_base, const char *sbase, uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(raw_rsrc(sbase), (lds_void_t *)(size_t)lds_base, 16,
-                                           voff, 0, 0, AUX);
+template <int AUX = kCachePolicyDefault, int BYTES = 16>
+__device__ __forceinline__ void dma_so(void *lds, const char *sbase, uint32_t voff, bool on = true) {
+  static_assert(BYTES == 16 || BYTES == 4 || BYTES == 2, "transfer width");
+  if constexpr (BYTES == 16)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(raw_rsrc(sbase, on), (lds_void_t *)lds, 16, voff, 0, 0,
+                                             AUX);
+  else if constexpr (BYTES == 4)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(raw_rsrc(sbase, on), (lds_void_t *)lds, 4, voff, 0, 0,
+                                             AUX);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(raw_rsrc(sbase, on), (lds_void_t *)lds, 2, voff, 0, 0,
+                                             AUX);
 }
-__device__ __forceinline__ void dma16_s(uint32_t lds_base, const char *sbase, uint32_t voff) {
-  dma16_so<kCachePolicyDefault>(lds_base, sbase, voff);
+__device__ __forceinline__ void dma16_s(void *lds, const char *sbase, uint32_t voff, bool on = true) {
+  dma_so<kCachePolicyDefault>(lds, sbase, voff, on);
 }
 
 // dma16_s with the nontemporal policy, for data streamed once (no reuse
 // through the caches).
-__device__ __forceinline__ void dma16_s_nt(uint32_t lds_base, const char *sbase, uint32_t voff) {
-  dma16_so<kNontemporal>(lds_base, sbase, voff);
+__device__ __forceinline__ void dma16_s_nt(void *lds, const char *sbase, uint32_t voff,
+                                           bool on = true) {
+  dma_so<kNontemporal>(lds, sbase, voff, on);
+}
+
+// Workgroup barrier of the block rings.  This wave's LDS reads and writes
+// are complete before it (lgkmcnt(0)) and none moves across it (compiler
+// fences), but transfers still in flight into other ring slots are not
+// awaited: the release fence of __syncthreads would wait for every
+// outstanding global -> LDS transfer of the wave.  Every wave awaits its own
+// transfers into the slot that is read next (wait_vmcnt) before the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0) only
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// The one-wave counterpart: this wave's LDS reads and writes are complete
+// (lgkmcnt(0)) and none moves across it, without a wait for transfers.  The
+// compiler waits for a transfer before reading its array, but it does not
+// order a transfer after earlier reads of the same array: a slot is refilled
+// only after this sync (a transfer that is switched off, or served from a
+// cache, can land within cycles).
+__device__ __forceinline__ void wave_ring_sync() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0) only
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // A wave-uniform pointer, made visibly uniform (SGPRs) for dma16_s.

@@ -263,13 +263,12 @@ __device__ __forceinline__ void open_state_mfma(const PromptParams &p, int u, in
   const int64_t kst = p.ks[1] * 2, vst = p.vs[1] * 2;
 
   // Raw value rows bs .. bs + 31 into this wave's staging block.
-  const uint32_t vdst = lds_offset(vstage);
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
     const int c = i * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     const int trow = min(bs + row, last);
-    dma16(vdst + i * 1024, vbase + trow * vst + (pc ^ v_swizzle<CPR>(row)) * 16);
+    dma16(vstage + i * 1024, vbase + trow * vst + (pc ^ v_swizzle<CPR>(row)) * 16);
   }
   // Raw key row bs + pi(col) as this lane's A operand.
   uint4 kop[KS];
@@ -395,8 +394,11 @@ __device__ __forceinline__ void open_state_mfma(const PromptParams &p, int u, in
   }
 }
 
-template <int D, int G, bool VT>
+// BIG: pages of >= 32 slots (one page per 32-slot block); VT: value pages
+// stored transposed (32-slot pages only).
+template <int D, int G, bool VT, bool BIG>
 __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p, int ntiles) {
+  static_assert(!VT || BIG, "transposed value pages hold 32 slots");
   constexpr int T = 32 / G;            // tokens per wave
   constexpr int TW = kWaves * T;       // tokens per workgroup
   constexpr int KS = D / 16;           // 16-dim k-steps of the score product
@@ -405,12 +407,21 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   constexpr int CPR = D / 8;           // 16-byte chunks per row
   constexpr int BLK = 32 * RB;         // bytes of one block's keys (and of its values)
   constexpr int DPW = BLK / 16 / kThreads;   // transfers per thread per block half
-  constexpr int SBYTES = kStages * 2 * BLK;
+  constexpr int SLOT = 2 * BLK;         // one ring slot: a block's keys, then its values
   constexpr int STAGE = 8 * 2 * D;     // floats per wave: 8 tokens x (key mean, value mean)
-  static_assert(kWaves * STAGE * 4 <= SBYTES, "open-state staging fits the block ring");
+  static_assert(STAGE * 4 == BLK && kWaves == 4, "open-state staging: two waves per ring slot");
   static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
-  static_assert(kStages >= 2 && kStages <= 4, "ring depth");
-  __shared__ __align__(16) unsigned char smem[SBYTES];
+  static_assert(kStages == 3 || kStages == 4, "ring depth");
+  // The block ring, one array per slot (see dma16_s).
+  __shared__ __align__(16) unsigned char ring0[SLOT], ring1[SLOT], ring2[SLOT];
+  __shared__ __align__(16) unsigned char ring3[kStages > 3 ? SLOT : 16];
+  auto slot = [&](auto st_c) -> unsigned char * {
+    constexpr int S = decltype(st_c)::value;
+    if constexpr (S == 0) return ring0;
+    else if constexpr (S == 1) return ring1;
+    else if constexpr (S == 2) return ring2;
+    else return ring3;
+  };
   __shared__ int s_hi[kWaves];
   __shared__ int s_pt[kPtabLds];
 
@@ -429,6 +440,8 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   const int a = tile * TW + wave * T;
   const int cnt = ok ? max(0, min(T, nb - a)) : 0;
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  // This wave's staging area for the open states (before the ring runs).
+  unsigned char *wstage = (wave < 2 ? ring0 : ring1) + (wave & 1) * BLK;
 
   // The tile's page-table slice, loaded now for a bound on the slots it can
   // see (a token's slot never exceeds the token) and stored to LDS before the
@@ -471,13 +484,13 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   // Open state of each column's token.
   if (cnt > 0 && p.window == 0) {
     open_state_mfma<D, G>(p, u, b, g, a, nb, col, hb, tok, colv, qop,
-                          reinterpret_cast<char *>(smem) + wave * BLK, m, ls, acc);
+                          reinterpret_cast<char *>(wstage), m, ls, acc);
   } else if (cnt > 0) {
     // Window grouping: the walk stages key and value means of 8 tokens at a
     // time (fp32, this wave's part of the block ring); then every lane takes
     // its column's score (dot with its Q^T slice, summed over the two halves)
     // and its slice of the value mean.
-    float *stage = reinterpret_cast<float *>(smem) + wave * STAGE;
+    float *stage = reinterpret_cast<float *>(wstage);
     constexpr int E = D / 64;
     auto snap = [&](int t, const float *ak, const float *av, float zs) {
           const float inv = 1.0f / zs;
@@ -548,10 +561,9 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   // Transfers of block kb into ring slot st.  This thread's chunks and their
   // byte offsets within a 32-row block (rows XOR-swizzled; LDS position =
   // chunk index).  Pages of >= 32 slots hold a block in one page: one
-  // wave-uniform base plus fixed per-lane offsets.  Smaller pages are looked
-  // up per row, rows past the closed slots reading the last closed one (in
-  // bounds; masked or zeroed when used).
-  const uint32_t ring = lds_offset(smem);
+  // wave-uniform base plus fixed per-lane offsets.  Smaller pages: one base
+  // per transfer (below).  Rows past the closed slots are masked or zeroed
+  // when used.
   uint32_t koff[DPW], voff[DPW];
   int krow_of[DPW];
 #pragma unroll
@@ -567,29 +579,40 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
       voff[i] = row * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
     }
   }
-  const bool big_pages = p.log2p >= 5;
-  auto issue = [&](int kb, int st) {
-    if (big_pages) {
+  // Every call issues the same 2 DPW transfers per wave; those of blocks
+  // past the last one are switched off (no memory read).  Pages of fewer
+  // than 32 slots: one transfer covers 1024 / RB <= 8 consecutive rows,
+  // which lie in one page (pages hold >= 8 slots), so its base is that
+  // page; rows past the closed slots are switched off per lane.
+  auto issue = [&](int kb, auto st_c) {
+    unsigned char *dst = slot(st_c);
+    const bool on = kb < nblk;
+    if constexpr (BIG) {
       const int s0 = kb * 32;
-      const int pg = __builtin_amdgcn_readfirstlane(s_pt[s0 >> p.log2p]);
+      const int pg = on ? __builtin_amdgcn_readfirstlane(s_pt[min(s0 >> p.log2p, kPtabLds - 1)]) : 0;
       const char *page = p.pool + int64_t(pg) * p.page_bytes;
-      const char *kb_base = page + int64_t(s0 & (P - 1)) * RB;
-      const char *vb_base = VT ? page + int64_t(P) * RB : kb_base + int64_t(P) * RB;
+      const char *kb_base = uniform_ptr(page + int64_t(s0 & (P - 1)) * RB);
+      const char *vb_base = uniform_ptr(VT ? page + int64_t(P) * RB : kb_base + int64_t(P) * RB);
 #pragma unroll
       for (int i = 0; i < DPW; ++i) {
-        const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
-        dma16_s(kdst, kb_base, koff[i]);
-        dma16_s(kdst + BLK, vb_base, voff[i]);
+        unsigned char *kdst = dst + (i * kWaves + wave) * 1024;
+        dma16_s(kdst, kb_base, koff[i], on);
+        dma16_s(kdst + BLK, vb_base, voff[i], on);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < DPW; ++i) {
-        const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
-        const int s = min(kb * 32 + krow_of[i], s_top - 1);
-        const char *pg = p.pool + int64_t(s_pt[s >> p.log2p]) * p.page_bytes +
-                         int64_t((s & (P - 1)) - krow_of[i]) * RB;
-        dma16(kdst, pg + koff[i]);
-        dma16(kdst + BLK, pg + int64_t(P) * RB + voff[i]);
+        unsigned char *kdst = dst + (i * kWaves + wave) * 1024;
+        const int r0 = (i * kWaves + wave) * (1024 / RB);   // first row of the transfer
+        const int s = kb * 32 + r0;
+        const bool live = on && s < s_top;
+        const int pg = live ? __builtin_amdgcn_readfirstlane(s_pt[s >> p.log2p]) : 0;
+        const char *base = uniform_ptr(p.pool + int64_t(pg) * p.page_bytes +
+                                       int64_t(live ? s & (P - 1) : 0) * RB);
+        const bool lane_on = kb * 32 + krow_of[i] < s_top;
+        const uint32_t rel = uint32_t(r0 * RB);
+        dma16_s(kdst, base, lane_on ? koff[i] - rel : kOutOfRange, live);
+        dma16_s(kdst + BLK, base, lane_on ? uint32_t(P * RB) + voff[i] - rel : kOutOfRange, live);
       }
     }
   };
@@ -618,12 +641,6 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   }
 
   const float sl2 = p.scale_log2;
-  // Waits until at most `after` blocks issued behind the awaited one are in flight.
-  auto wait_after = [&](int after) {
-    if (after >= 2) wait_vmcnt<4 * DPW>();
-    else if (after == 1) wait_vmcnt<2 * DPW>();
-    else wait_vmcnt<0>();
-  };
   auto scores = [&](const char *kd) {
     f32x16_t sc = f32x16_t{};
 #pragma unroll
@@ -636,21 +653,25 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
   // score MFMAs of block kb + 1 (one accumulator chain, order pinned by
   // scheduling barriers, key operands read two ahead), then block kb's value
   // product.
-  for (int kb = 0; kb < kStages - 1 && kb < nblk; ++kb) issue(kb, kb);
+  // kStages - 1 blocks are always in flight ahead of the one multiplied
+  // (2 DPW transfers each), so the waits are fixed counts.
+  issue(0, std::integral_constant<int, 0>{});
+  issue(1, std::integral_constant<int, 1>{});
+  if constexpr (kStages > 3) issue(2, std::integral_constant<int, 2>{});
   f32x16_t scn = f32x16_t{};
   if (nblk > 0) {
-    wait_after(min(nblk - 1, kStages - 2));
-    __syncthreads();   // block 0 is in LDS for every wave
-    if (wave_hi > 0) scn = scores(reinterpret_cast<const char *>(smem));
+    wait_vmcnt<(kStages - 2) * 2 * DPW>();
+    ring_barrier();   // block 0 is in LDS for every wave
+    if (wave_hi > 0) scn = scores(reinterpret_cast<const char *>(ring0));
   }
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value, SN = (ST + 1) % kStages;
-    if (kb + 1 < nblk) wait_after(min(kStages - 3, nblk - 2 - kb));   // block kb + 1 has landed
-    __syncthreads();   // every wave is past step kb - 1: the ring slot of kb - 1 is free
-    if (kb + kStages - 1 < nblk) issue(kb + kStages - 1, (ST + kStages - 1) % kStages);
+    wait_vmcnt<(kStages - 3) * 2 * DPW>();   // block kb + 1 has landed
+    ring_barrier();   // every wave is past step kb - 1: the ring slot of kb - 1 is free
+    issue(kb + kStages - 1, std::integral_constant<int, (ST + kStages - 1) % kStages>{});
     if (kb * 32 >= wave_hi) return;
-    const char *vd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK + BLK;
-    const char *kn = reinterpret_cast<const char *>(smem) + SN * 2 * BLK;   // block kb + 1's keys
+    const char *vd = reinterpret_cast<const char *>(slot(stage_c)) + BLK;
+    const char *kn = reinterpret_cast<const char *>(slot(std::integral_constant<int, SN>{}));   // block kb + 1's keys
 
     // Raw scores; slots past this column's limit are masked only in blocks
     // that reach the staircase.
@@ -746,13 +767,14 @@ __global__ __launch_bounds__(kThreads, 2) void prompt_mfma_kernel(PromptParams p
       for (int kk = 0; kk < 2; ++kk) acc[t] = mfma_32x32x16(va[t][kk], pb[kk], acc[t]);
   };
 
-  static_assert(kStages == 3 || kStages == 4, "the block loop below is unrolled for 3 or 4 slots");
+  // Whole rounds of kStages steps (a step past the last block only keeps the
+  // barriers and transfer counts in step), so that no transfer is issued on
+  // one path and not on another.
   for (int kb = 0; kb < nblk; kb += kStages) {
     step(std::integral_constant<int, 0>{}, kb);
-    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
-    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
-    if constexpr (kStages > 3)
-      if (kb + 3 < nblk) step(std::integral_constant<int, kStages - 1>{}, kb + 3);
+    step(std::integral_constant<int, 1>{}, kb + 1);
+    step(std::integral_constant<int, 2>{}, kb + 2);
+    if constexpr (kStages > 3) step(std::integral_constant<int, 3>{}, kb + 3);
   }
 
   // Normalise and store: lane holds dims 32 t + 8 i + 4 hb .. + 4 of its column.
@@ -900,11 +922,14 @@ hipError_t prompt_mfma(const PromptParams &p, bool vt, hipStream_t s) {
   const int64_t blocks = int64_t(8) * ((p.units + 7) / 8) * ntiles;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   if (vt)
-    hipLaunchKernelGGL((prompt_mfma_kernel<D, G, true>), dim3(unsigned(blocks)), dim3(kThreads), 0,
-                       s, p, ntiles);
+    hipLaunchKernelGGL((prompt_mfma_kernel<D, G, true, true>), dim3(unsigned(blocks)),
+                       dim3(kThreads), 0, s, p, ntiles);
+  else if (p.log2p >= 5)
+    hipLaunchKernelGGL((prompt_mfma_kernel<D, G, false, true>), dim3(unsigned(blocks)),
+                       dim3(kThreads), 0, s, p, ntiles);
   else
-    hipLaunchKernelGGL((prompt_mfma_kernel<D, G, false>), dim3(unsigned(blocks)), dim3(kThreads), 0,
-                       s, p, ntiles);
+    hipLaunchKernelGGL((prompt_mfma_kernel<D, G, false, false>), dim3(unsigned(blocks)),
+                       dim3(kThreads), 0, s, p, ntiles);
   return hipGetLastError();
 }
 

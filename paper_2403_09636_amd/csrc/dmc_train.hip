@@ -214,14 +214,13 @@ __global__ __launch_bounds__(64) void train_states_mfma_kernel(TrainParams p) {
   const char *kb = static_cast<const char *>(p.k) + row_k(p, b, 0, g, D) * 2;
   const char *vb = static_cast<const char *>(p.v) + row_k(p, b, 0, g, D) * 2;
   const int64_t rs = int64_t(p.hkv) * D * 2;
-  const uint32_t kst = lds_offset(smem), vst = kst + ROWS * RB;
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
     const int c = i * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     const int64_t src = min(max(tb + row, 0), last) * rs + (pc ^ v_swizzle<CPR>(row)) * 16;
-    dma16(kst + i * 1024, kb + src);
-    dma16(vst + i * 1024, vb + src);
+    dma16(smem + i * 1024, kb + src);
+    dma16(smem + ROWS * RB + i * 1024, vb + src);
   }
 
   // Weights of position j for staged rows 0 .. ROWS - 1, from the top down.
@@ -690,14 +689,13 @@ __global__ __launch_bounds__(64, (tokens_mfma_waves<D, NK>())) void train_tokens
   uint4 xa[KS];
   auto issue = [&](int m) {
     const char *hp = reinterpret_cast<const char *>(m == 0 ? p.dks : p.dvs);
-    const uint32_t dst = lds_offset(smem);
 #pragma unroll
     for (int i = 0; i < ROWS * CPR / 64; ++i) {
       const int c = i * 64 + lane;
       const int row = c / CPR, pc = c - row * CPR;
       const int64_t src = (un + min(t0 + row, last)) * RB + (pc ^ v_swizzle<CPR>(row)) * 16;
-      dma16(dst + i * 1024, hp + src);
-      dma16(dst + PLANE + i * 1024, hp + plane_bytes + src);
+      dma16(smem + i * 1024, hp + src);
+      dma16(smem + PLANE + i * 1024, hp + plane_bytes + src);
     }
     const char *xr = static_cast<const char *>(m == 0 ? p.k : p.v) +
                      row_k(p, b, min(t0 + col, last), g, D) * 2 + hb * 16;
@@ -1021,7 +1019,17 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   constexpr int VSW = MODE == 0 ? 1 : KSW;   // forward reads values transposed; dq as rows,
                                              // laid out like the keys (shared offsets)
   static_assert(DPW >= 1 && BLK % (16 * kThreads) == 0, "block split");
-  __shared__ __align__(16) unsigned char smem[kSt * 2 * BLK];
+  static_assert(kSt == 4, "the block loop below is unrolled for four slots");
+  // The state ring, one array per slot (see dma16_s): keys, then values.
+  __shared__ __align__(16) unsigned char ring0[2 * BLK], ring1[2 * BLK], ring2[2 * BLK],
+      ring3[2 * BLK];
+  auto slot = [&](auto st_c) -> unsigned char * {
+    constexpr int S = decltype(st_c)::value;
+    if constexpr (S == 0) return ring0;
+    else if constexpr (S == 1) return ring1;
+    else if constexpr (S == 2) return ring2;
+    else return ring3;
+  };
 
   const int U = p.batch * p.hkv;
   const int bid = blockIdx.x;
@@ -1085,8 +1093,9 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   for (int i = 0; i < NTL; ++i) acc[i] = f32x16_t{};
 
   // Block transfers (same chunk mapping as prompt attention; the unit's
-  // states are contiguous, so one wave-uniform base per block).
-  const uint32_t ring = lds_offset(smem);
+  // states are contiguous, so one wave-uniform base per block).  Every call
+  // issues 2 DPW transfers per wave; those of blocks past the last one are
+  // switched off.
   uint32_t koff[DPW], voff[MODE == 0 ? DPW : 1];
 #pragma unroll
   for (int i = 0; i < DPW; ++i) {
@@ -1097,12 +1106,13 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   }
   const char *kst = static_cast<const char *>(p.ks) + int64_t(u) * p.n * RB;
   const char *vst = static_cast<const char *>(p.vs) + int64_t(u) * p.n * RB;
-  auto issue = [&](int kb, int st) {
+  auto issue = [&](int kb, auto st_c) {
+    const bool on = kb < nblk;
 #pragma unroll
     for (int i = 0; i < DPW; ++i) {
-      const uint32_t kdst = ring + st * 2 * BLK + (i * kWaves + wave) * 1024;
-      dma16_s(kdst, uniform_ptr(kst + int64_t(kb) * BLK), koff[i]);
-      dma16_s(kdst + BLK, uniform_ptr(vst + int64_t(kb) * BLK), MODE == 0 ? voff[i] : koff[i]);
+      unsigned char *kdst = slot(st_c) + (i * kWaves + wave) * 1024;
+      dma16_s(kdst, uniform_ptr(kst + int64_t(kb) * BLK), koff[i], on);
+      dma16_s(kdst + BLK, uniform_ptr(vst + int64_t(kb) * BLK), MODE == 0 ? voff[i] : koff[i], on);
     }
   };
 
@@ -1118,11 +1128,11 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
   // One block of the dq kernel.
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
-    wait_block<2 * DPW>(min(nblk - 1 - kb, kSt - 2));
-    __syncthreads();   // block kb is in LDS for every wave; the slot of kb - 1 is free
-    if (kb + kSt - 1 < nblk) issue(kb + kSt - 1, (ST + kSt - 1) % kSt);
+    wait_vmcnt<(kSt - 2) * 2 * DPW>();   // block kb has landed
+    ring_barrier();   // block kb is in LDS for every wave; the slot of kb - 1 is free
+    issue(kb + kSt - 1, std::integral_constant<int, (ST + kSt - 1) % kSt>{});
     if (kb * 32 >= wave_hi) return;
-    const char *kd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK;
+    const char *kd = reinterpret_cast<const char *>(slot(stage_c));
     const char *vd = kd + BLK;
 
     f32x16_t sc = f32x16_t{};
@@ -1179,30 +1189,32 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
     }
   };
 
-  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(kb, kb);
+  issue(0, std::integral_constant<int, 0>{});
+  issue(1, std::integral_constant<int, 1>{});
+  issue(2, std::integral_constant<int, 2>{});
   if constexpr (MODE == 0) {
     // Step kb runs block kb's exponentials between the score MFMAs of block
     // kb + 1 (one accumulator chain; order pinned by scheduling barriers),
     // then block kb's value product.
     f32x16_t scn = f32x16_t{};
     if (nblk > 0) {
-      wait_block<2 * DPW>(min(nblk - 1, kSt - 2));
-      __syncthreads();
+      wait_vmcnt<(kSt - 2) * 2 * DPW>();   // block 0 has landed
+      ring_barrier();
       if (wave_hi > 0) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           scn = mfma_32x32x16(*reinterpret_cast<const uint4 *>(
-                                  reinterpret_cast<const char *>(smem) + kaddr[ks]), qop[ks], scn);
+                                  reinterpret_cast<const char *>(ring0) + kaddr[ks]), qop[ks], scn);
       }
     }
     auto step0 = [&](auto stage_c, int kb) {
       constexpr int ST = decltype(stage_c)::value, SN = (ST + 1) % kSt;
-      if (kb + 1 < nblk) wait_block<2 * DPW>(min(kSt - 3, nblk - 2 - kb));   // block kb + 1 landed
-      __syncthreads();   // every wave is past step kb - 1: the slot of kb - 1 is free
-      if (kb + kSt - 1 < nblk) issue(kb + kSt - 1, (ST + kSt - 1) % kSt);
+      wait_vmcnt<(kSt - 3) * 2 * DPW>();   // block kb + 1 has landed
+      ring_barrier();   // every wave is past step kb - 1: the slot of kb - 1 is free
+      issue(kb + kSt - 1, std::integral_constant<int, (ST + kSt - 1) % kSt>{});
       if (kb * 32 >= wave_hi) return;
-      const char *vd = reinterpret_cast<const char *>(smem) + ST * 2 * BLK + BLK;
-      const char *kn = reinterpret_cast<const char *>(smem) + SN * 2 * BLK;   // block kb + 1's keys
+      const char *vd = reinterpret_cast<const char *>(slot(stage_c)) + BLK;
+      const char *kn = reinterpret_cast<const char *>(slot(std::integral_constant<int, SN>{}));   // block kb + 1's keys
       float sv[16];
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) sv[rr] = scn[rr];
@@ -1263,20 +1275,20 @@ __global__ __launch_bounds__(kThreads, 2) void train_qmajor_kernel(TrainParams p
         for (int kk = 0; kk < 2; ++kk)
           acc[i] = mfma_32x32x16(tr_operand<RB>(vd, traddr[i], kk), pb[kk], acc[i]);
     };
+    // Whole rounds of four steps (a step past the last block only keeps the
+    // barriers and transfer counts in step).
     for (int kb = 0; kb < nblk; kb += kSt) {
       step0(std::integral_constant<int, 0>{}, kb);
-      if (kb + 1 < nblk) step0(std::integral_constant<int, 1>{}, kb + 1);
-      if (kb + 2 < nblk) step0(std::integral_constant<int, 2>{}, kb + 2);
-      if constexpr (kSt > 3)
-        if (kb + 3 < nblk) step0(std::integral_constant<int, kSt - 1>{}, kb + 3);
+      step0(std::integral_constant<int, 1>{}, kb + 1);
+      step0(std::integral_constant<int, 2>{}, kb + 2);
+      step0(std::integral_constant<int, 3>{}, kb + 3);
     }
   } else {
     for (int kb = 0; kb < nblk; kb += kSt) {
       step(std::integral_constant<int, 0>{}, kb);
-      if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
-      if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
-      if constexpr (kSt > 3)
-        if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
+      step(std::integral_constant<int, 1>{}, kb + 1);
+      step(std::integral_constant<int, 2>{}, kb + 2);
+      step(std::integral_constant<int, 3>{}, kb + 3);
     }
   }
 
@@ -1315,9 +1327,18 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   constexpr int kSt = kDkvStages;
   constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
-  constexpr int SLOT = 2 * BLK + 256;   // query rows, dO rows, 32 x (L, D) statistics
+  // One ring slot: query rows, dO rows, then per wave its own copy of the
+  // block's statistics (32 L, 32 D, each followed by an unused duplicate).
+  constexpr int SLOT = 2 * BLK + kWaves * 512;
   static_assert(DPW >= 1, "block split");
-  __shared__ __align__(16) unsigned char smem[kSt * SLOT];
+  static_assert(kSt == 3, "the block loop below is unrolled for three slots");
+  __shared__ __align__(16) unsigned char ring0[SLOT], ring1[SLOT], ring2[SLOT];
+  auto slot = [&](auto st_c) -> unsigned char * {
+    constexpr int S = decltype(st_c)::value;
+    if constexpr (S == 0) return ring0;
+    else if constexpr (S == 1) return ring1;
+    else return ring2;
+  };
 
   const int U = p.batch * p.hkv;
   const int bid = blockIdx.x;
@@ -1360,48 +1381,45 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   const int nrows = p.n * G;
   const int qb0 = row_lo >> 5, qb1 = (nrows + 31) >> 5;
   const int nblk = qb1 - qb0;
-  const uint32_t ring = lds_offset(smem);
-  // This thread's chunks: block row loff, byte offset lofs from the block's
-  // first row (a block's rows r = t G + h are 32 / G whole tokens).
-  uint32_t qoff[DPW], loff[DPW], lofs[DPW];
+  // This thread's chunks: block row loff, byte offset qoff within the row (a
+  // block's rows r = t G + h are 32 / G whole tokens).
+  uint32_t qoff[DPW], loff[DPW];
 #pragma unroll
   for (int i = 0; i < DPW; ++i) {
     const int c = (i * kWaves + wave) * 64 + lane;
     const int row = c / CPR, pc = c - row * CPR;
     loff[i] = row;
     qoff[i] = (pc ^ dual_swizzle<CPR>(row)) * 16;
-    lofs[i] = uint32_t(((row / G) * p.hq + row % G) * D * 2) + qoff[i];
   }
   const int64_t row0 = row_q(p, b, 0, g * G, D) * 2;   // bytes to (b, token 0, head g G)
   const int64_t tokb = int64_t(p.hq) * D * 2;          // bytes per token
-  // Statistics of rows 8 wave .. 8 wave + 7 of a block: lanes 0, 1 move their
-  // L (32 bytes), lanes 2, 3 their D ([U][n][G] is row-contiguous and padded
-  // by 32 rows), so every wave issues the same number of transfers.
-  const char *stat_src = reinterpret_cast<const char *>(lane < 2 ? p.lse : p.dsum) +
-                         (int64_t(u) * p.n * G + 8 * wave) * 4 + (lane & 1) * 16;
-  auto issue = [&](int qb, int st) {
-    if (qb * 32 + 32 <= nrows) {   // whole block: one base, fixed offsets
-      const int64_t bb = row0 + int64_t(qb * (32 / G)) * tokb;
-      const char *qp = uniform_ptr(static_cast<const char *>(p.q) + bb);
-      const char *dp = uniform_ptr(static_cast<const char *>(p.dout) + bb);
+  // Every call issues 2 DPW + 2 transfers per wave; those of blocks past the
+  // last one are switched off.  Rows past the sequence (the last block) read
+  // its last row: in bounds and finite, masked when used.  Each wave copies
+  // the block's statistics ([U][n][G] rows, padded by 32) into its own area
+  // by two 4-byte transfers: L of the 32 rows (lanes 32..63 repeat them),
+  // then D.
+  const char *lse_u = reinterpret_cast<const char *>(p.lse) + int64_t(u) * p.n * G * 4;
+  const char *dsum_u = reinterpret_cast<const char *>(p.dsum) + int64_t(u) * p.n * G * 4;
+  auto issue = [&](int qb, auto st_c) {
+    const bool on = qb < qb1;
+    unsigned char *dst = slot(st_c);
+    const int64_t bb = row0 + int64_t(qb * (32 / G)) * tokb;
+    const char *qp = uniform_ptr(static_cast<const char *>(p.q) + bb);
+    const char *dp = uniform_ptr(static_cast<const char *>(p.dout) + bb);
+    const int last_rel = nrows - 1 - qb * 32;   // the block's last row inside the sequence
 #pragma unroll
-      for (int i = 0; i < DPW; ++i) {
-        const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
-        dma16_s(dst, qp, lofs[i]);
-        dma16_s(dst + BLK, dp, lofs[i]);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < DPW; ++i) {
-        const uint32_t dst = ring + st * SLOT + (i * kWaves + wave) * 1024;
-        const int rg = min(qb * 32 + int(loff[i]), nrows - 1);   // rows past the sequence: in bounds, masked
-        const int tq = rg / G, h = rg - tq * G;
-        const int64_t ro = row_q(p, b, tq, g * G + h, D) * 2 + qoff[i];
-        dma16(dst, static_cast<const char *>(p.q) + ro);
-        dma16(dst + BLK, static_cast<const char *>(p.dout) + ro);
-      }
+    for (int i = 0; i < DPW; ++i) {
+      unsigned char *cdst = dst + (i * kWaves + wave) * 1024;
+      const int rel = min(int(loff[i]), last_rel);
+      const uint32_t off = uint32_t(((rel / G) * p.hq + rel % G) * D * 2) + qoff[i];
+      dma16_s(cdst, qp, off, on);
+      dma16_s(cdst + BLK, dp, off, on);
     }
-    if (lane < 4) dma16(ring + st * SLOT + 2 * BLK + wave * 64, stat_src + int64_t(qb) * 128);
+    unsigned char *sdst = dst + 2 * BLK + wave * 512;
+    const uint32_t soff = uint32_t(qb * 32 + (lane & 31)) * 4;
+    dma_so<kCachePolicyDefault, 4>(sdst, uniform_ptr(lse_u), soff, on);
+    dma_so<kCachePolicyDefault, 4>(sdst + 256, uniform_ptr(dsum_u), soff, on);
   };
   const int qrow = score_slot(col);
   uint32_t raddr[KS];
@@ -1417,19 +1435,20 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
 
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
-    wait_block<2 * DPW + 1>(min(nblk - 1 - kb, kSt - 2));
-    __syncthreads();
-    if (kb + kSt - 1 < nblk) issue(qb0 + kb + kSt - 1, (ST + kSt - 1) % kSt);
+    wait_vmcnt<(kSt - 2) * (2 * DPW + 2)>();   // block kb has landed
+    ring_barrier();   // block kb is in LDS for every wave; the slot of kb - 1 is free
+    issue(qb0 + kb + kSt - 1, std::integral_constant<int, (ST + kSt - 1) % kSt>{});
     const int rb = (qb0 + kb) * 32;                  // first row of the block
-    if (rb + 31 < s0 * G) return;                    // every row precedes this wave's states
-    const char *qd = reinterpret_cast<const char *>(smem) + ST * SLOT;
+    if (kb >= nblk || rb + 31 < s0 * G) return;      // past the last block, or every row
+                                                     // precedes this wave's states
+    const char *qd = reinterpret_cast<const char *>(slot(stage_c));
     const char *dd = qd + BLK;
     const bool interior = rb / G > s0 + 31 && rb + 32 <= nrows && s0 + 32 <= p.n;
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
     // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
-    // 8 hb + q (pi-permuted rows), from the block's LDS statistics area
-    // ([4][8 L, 8 D] floats).
-    const float *sd = reinterpret_cast<const float *>(qd + 2 * BLK);
+    // 8 hb + q (pi-permuted rows), from this wave's copy of the block's
+    // statistics (L rows at sl, D rows at sl + 64).
+    const float *sl = reinterpret_cast<const float *>(qd + 2 * BLK + wave * 512);
     uint4 pa[2], da[2];
     if (PART == 2 && interior) {
       // Scores first; then dP's MFMAs with P's exponentials between them
@@ -1443,11 +1462,11 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       float Lr[16], Dr[16];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const float *e8 = sd + (2 * kk + hb) * 16;
+        const float *e8 = sl + 16 * kk + 8 * hb;
 #pragma unroll
         for (int c4 = 0; c4 < 2; ++c4) {
           const float4 l4 = *reinterpret_cast<const float4 *>(e8 + 4 * c4);
-          const float4 d4 = *reinterpret_cast<const float4 *>(e8 + 8 + 4 * c4);
+          const float4 d4 = *reinterpret_cast<const float4 *>(e8 + 64 + 4 * c4);
           Lr[8 * kk + 4 * c4 + 0] = l4.x; Lr[8 * kk + 4 * c4 + 1] = l4.y;
           Lr[8 * kk + 4 * c4 + 2] = l4.z; Lr[8 * kk + 4 * c4 + 3] = l4.w;
           Dr[8 * kk + 4 * c4 + 0] = d4.x; Dr[8 * kk + 4 * c4 + 1] = d4.y;
@@ -1496,14 +1515,14 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     for (int kk = 0; kk < 2; ++kk) {
       float Lr[16], Dr[16];   // indexed by register 8 kk + q: only this kk's half is loaded
       {
-        const float *e8 = sd + (2 * kk + hb) * 16;
+        const float *e8 = sl + 16 * kk + 8 * hb;
         const float4 l0 = *reinterpret_cast<const float4 *>(e8);
         const float4 l1 = *reinterpret_cast<const float4 *>(e8 + 4);
         Lr[8 * kk + 0] = l0.x; Lr[8 * kk + 1] = l0.y; Lr[8 * kk + 2] = l0.z; Lr[8 * kk + 3] = l0.w;
         Lr[8 * kk + 4] = l1.x; Lr[8 * kk + 5] = l1.y; Lr[8 * kk + 6] = l1.z; Lr[8 * kk + 7] = l1.w;
         if constexpr (PART != 1) {
-          const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 8);
-          const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 12);
+          const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 64);
+          const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 68);
           Dr[8 * kk + 0] = d0.x; Dr[8 * kk + 1] = d0.y; Dr[8 * kk + 2] = d0.z; Dr[8 * kk + 3] = d0.w;
           Dr[8 * kk + 4] = d1.x; Dr[8 * kk + 5] = d1.y; Dr[8 * kk + 6] = d1.z; Dr[8 * kk + 7] = d1.w;
         } else {
@@ -1558,13 +1577,14 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       }
   };
 
-  for (int kb = 0; kb < kSt - 1 && kb < nblk; ++kb) issue(qb0 + kb, kb);
+  issue(qb0, std::integral_constant<int, 0>{});
+  issue(qb0 + 1, std::integral_constant<int, 1>{});
+  // Whole rounds of three steps (a step past the last block only keeps the
+  // barriers and transfer counts in step).
   for (int kb = 0; kb < nblk; kb += kSt) {
     step(std::integral_constant<int, 0>{}, kb);
-    if (kb + 1 < nblk) step(std::integral_constant<int, 1>{}, kb + 1);
-    if (kb + 2 < nblk) step(std::integral_constant<int, 2>{}, kb + 2);
-    if constexpr (kSt > 3)
-      if (kb + 3 < nblk) step(std::integral_constant<int, kSt - 1>{}, kb + 3);
+    step(std::integral_constant<int, 1>{}, kb + 1);
+    step(std::integral_constant<int, 2>{}, kb + 2);
   }
 
   // Outputs: C[state][dim] -- lane holds dim 32 i + col of states

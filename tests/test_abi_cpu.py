@@ -94,16 +94,16 @@ def test_windowed_cache_needs_the_full_table(P):
 
 def test_matrix_core_cache_unit_limit(P):
     """bf16 grouped-query caches (G >= 4, 32-slot pages) decode with a 128 KB
-    chunk ring in LDS at d = 128; the slot-space table beside it holds about
-    7600 entries, i.e. up to 7600 units with one entry each, and up to 64
-    times that with grouped entries.  fp32 caches run the vector kernel."""
-    for batch in (950, 1024, 60000):                          # 7600, 8192, 480000 units
+    chunk ring in LDS at d = 128; the slot-space table beside it holds 8176
+    entries, i.e. up to 8175 units with one entry each, and up to 64 times
+    that with grouped entries.  fp32 caches run the vector kernel."""
+    for batch in (1021, 1024, 65400):                         # 8168, 8192, 523200 units
         cfg = P.make_config(1, batch, 64, 8, 128, "bf16", max_slots_per_seq=8, num_pages=1024)
         assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(cfg)) > 0, batch
-    big = P.make_config(1, 62000, 64, 8, 128, "bf16", max_slots_per_seq=8, num_pages=1024)
+    big = P.make_config(1, 65401, 64, 8, 128, "bf16", max_slots_per_seq=8, num_pages=1024)
     assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(big)) == 0
     assert "units" in P.binding.last_error()
-    vec = P.make_config(1, 62000, 64, 8, 128, "fp32", max_slots_per_seq=8, num_pages=1024)
+    vec = P.make_config(1, 65401, 64, 8, 128, "fp32", max_slots_per_seq=8, num_pages=1024)
     assert P.binding.lib.dmc_cache_workspace_bytes(ctypes.byref(vec)) > 0
 
 

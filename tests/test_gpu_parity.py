@@ -279,12 +279,13 @@ def test_bad_import_length_sets_flag(torch_cuda):
 
 def test_largest_matrix_core_unit_table(torch_cuda):
     """Grouped-query bf16 caches decode on matrix cores with a 128 KB chunk ring
-    in LDS at d = 128; the largest accepted slot-space table (7600 units) fills
-    the rest of the compute unit's LDS.  Imported caches of 40-70 slots (two or
-    three pages per unit), three steps, every unit against the oracle."""
+    in LDS at d = 128; the largest slot-space table of one entry per unit
+    (8175 units; here 8168) fills the rest of the compute unit's LDS.  Imported
+    caches of 40-70 slots (two or three pages per unit), three steps, every
+    unit against the oracle."""
     import torch
     log("case largest matrix-core unit table")
-    B, Hkv, G, d, steps = 950, 8, 8, 128, 3
+    B, Hkv, G, d, steps = 1021, 8, 8, 128, 3
     rng = np.random.default_rng(78)
     lens = rng.integers(40, 71, size=(B, Hkv)).astype(np.int32)
     dense = int(lens.max())
