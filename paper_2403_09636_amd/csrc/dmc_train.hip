@@ -1328,8 +1328,9 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   constexpr int KS = D / 16, NTL = D / 32, RB = D * 2, CPR = D / 8, BLK = 32 * RB;
   constexpr int DPW = BLK / 16 / kThreads;
   // One ring slot: query rows, dO rows, then per wave its own copy of the
-  // block's statistics (32 L, 32 D, each followed by an unused duplicate).
-  constexpr int SLOT = 2 * BLK + kWaves * 512;
+  // block's statistics (32 L, then 32 D).  Three workgroups (3 x 52 KB at
+  // d = 128) share a compute unit.
+  constexpr int SLOT = 2 * BLK + kWaves * 256;
   static_assert(DPW >= 1, "block split");
   static_assert(kSt == 3, "the block loop below is unrolled for three slots");
   __shared__ __align__(16) unsigned char ring0[SLOT], ring1[SLOT], ring2[SLOT];
@@ -1393,14 +1394,17 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
   }
   const int64_t row0 = row_q(p, b, 0, g * G, D) * 2;   // bytes to (b, token 0, head g G)
   const int64_t tokb = int64_t(p.hq) * D * 2;          // bytes per token
-  // Every call issues 2 DPW + 2 transfers per wave; those of blocks past the
+  // Every call issues 2 DPW + 1 transfers per wave; those of blocks past the
   // last one are switched off.  Rows past the sequence (the last block) read
   // its last row: in bounds and finite, masked when used.  Each wave copies
   // the block's statistics ([U][n][G] rows, padded by 32) into its own area
-  // by two 4-byte transfers: L of the 32 rows (lanes 32..63 repeat them),
-  // then D.
+  // by one 4-byte transfer: lanes 0..31 L of the 32 rows, lanes 32..63 their
+  // D, which lies a fixed distance after L in the workspace (under 2^28
+  // bytes: the API limits the query tensor to 2^31 elements).
   const char *lse_u = reinterpret_cast<const char *>(p.lse) + int64_t(u) * p.n * G * 4;
-  const char *dsum_u = reinterpret_cast<const char *>(p.dsum) + int64_t(u) * p.n * G * 4;
+  const uint32_t dsum_delta = static_cast<uint32_t>(reinterpret_cast<const char *>(p.dsum) -
+                                                    reinterpret_cast<const char *>(p.lse));
+  const uint32_t soff_lane = uint32_t(lane & 31) * 4 + (lane >= 32 ? dsum_delta : 0u);
   auto issue = [&](int qb, auto st_c) {
     const bool on = qb < qb1;
     unsigned char *dst = slot(st_c);
@@ -1416,10 +1420,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
       dma16_s(cdst, qp, off, on);
       dma16_s(cdst + BLK, dp, off, on);
     }
-    unsigned char *sdst = dst + 2 * BLK + wave * 512;
-    const uint32_t soff = uint32_t(qb * 32 + (lane & 31)) * 4;
-    dma_so<kCachePolicyDefault, 4>(sdst, uniform_ptr(lse_u), soff, on);
-    dma_so<kCachePolicyDefault, 4>(sdst + 256, uniform_ptr(dsum_u), soff, on);
+    dma_so<kCachePolicyDefault, 4>(dst + 2 * BLK + wave * 256, uniform_ptr(lse_u),
+                                   soff_lane + uint32_t(qb) * 128, on);
   };
   const int qrow = score_slot(col);
   uint32_t raddr[KS];
@@ -1435,7 +1437,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
 
   auto step = [&](auto stage_c, int kb) {
     constexpr int ST = decltype(stage_c)::value;
-    wait_vmcnt<(kSt - 2) * (2 * DPW + 2)>();   // block kb has landed
+    wait_vmcnt<(kSt - 2) * (2 * DPW + 1)>();   // block kb has landed
     ring_barrier();   // block kb is in LDS for every wave; the slot of kb - 1 is free
     issue(qb0 + kb + kSt - 1, std::integral_constant<int, (ST + kSt - 1) % kSt>{});
     const int rb = (qb0 + kb) * 32;                  // first row of the block
@@ -1447,8 +1449,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
     f32x16_t sc = f32x16_t{}, dp = f32x16_t{};
     // Softmax statistics of register 8 kk + q of this lane: row rb + 16 kk +
     // 8 hb + q (pi-permuted rows), from this wave's copy of the block's
-    // statistics (L rows at sl, D rows at sl + 64).
-    const float *sl = reinterpret_cast<const float *>(qd + 2 * BLK + wave * 512);
+    // statistics (L rows at sl, D rows at sl + 32).
+    const float *sl = reinterpret_cast<const float *>(qd + 2 * BLK + wave * 256);
     uint4 pa[2], da[2];
     if (PART == 2 && interior) {
       // Scores first; then dP's MFMAs with P's exponentials between them
@@ -1466,7 +1468,7 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
 #pragma unroll
         for (int c4 = 0; c4 < 2; ++c4) {
           const float4 l4 = *reinterpret_cast<const float4 *>(e8 + 4 * c4);
-          const float4 d4 = *reinterpret_cast<const float4 *>(e8 + 64 + 4 * c4);
+          const float4 d4 = *reinterpret_cast<const float4 *>(e8 + 32 + 4 * c4);
           Lr[8 * kk + 4 * c4 + 0] = l4.x; Lr[8 * kk + 4 * c4 + 1] = l4.y;
           Lr[8 * kk + 4 * c4 + 2] = l4.z; Lr[8 * kk + 4 * c4 + 3] = l4.w;
           Dr[8 * kk + 4 * c4 + 0] = d4.x; Dr[8 * kk + 4 * c4 + 1] = d4.y;
@@ -1521,8 +1523,8 @@ __global__ __launch_bounds__(kThreads, 2) void train_dkv_mfma_kernel(TrainParams
         Lr[8 * kk + 0] = l0.x; Lr[8 * kk + 1] = l0.y; Lr[8 * kk + 2] = l0.z; Lr[8 * kk + 3] = l0.w;
         Lr[8 * kk + 4] = l1.x; Lr[8 * kk + 5] = l1.y; Lr[8 * kk + 6] = l1.z; Lr[8 * kk + 7] = l1.w;
         if constexpr (PART != 1) {
-          const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 64);
-          const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 68);
+          const float4 d0 = *reinterpret_cast<const float4 *>(e8 + 32);
+          const float4 d1 = *reinterpret_cast<const float4 *>(e8 + 36);
           Dr[8 * kk + 0] = d0.x; Dr[8 * kk + 1] = d0.y; Dr[8 * kk + 2] = d0.z; Dr[8 * kk + 3] = d0.w;
           Dr[8 * kk + 4] = d1.x; Dr[8 * kk + 5] = d1.y; Dr[8 * kk + 6] = d1.z; Dr[8 * kk + 7] = d1.w;
         } else {
