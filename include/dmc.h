@@ -150,6 +150,9 @@ dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream);
  *   q_dev: logical [B, n, Hq, d] with q_strides for B, n, Hq; only element 0
  *     of each query row is read (a [B, n, Hq] tensor of q[..., 0] with
  *     strides (n*Hq, Hq, 1) is accepted), no alignment requirement.
+ *   The token (n-axis) strides of k, v and q are below 32 MiB, else
+ *   DMC_ERR_UNSUPPORTED (the kernels address up to 64 consecutive tokens from
+ *   one base with 32-bit offsets).
  *   n: prompt length, 0 <= n <= max_prompt_len.
  *   prompt_lens_dev: optional int32 [B]; row b uses tokens t < prompt_lens[b]
  *     (values outside [0, n] raise the invalid-argument device flag and are

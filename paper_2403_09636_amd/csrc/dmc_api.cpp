@@ -459,6 +459,11 @@ dmc_status prefill_params(dmc_cache *cache, int32_t layer, const void *k, const 
       if (full_q && q_strides[i] % 8)
         return fail(DMC_ERR_INVALID_ARG, "q strides must be multiples of 8 elements");
     }
+    // the compaction addresses up to 64 consecutive tokens from one base with
+    // 32-bit offsets
+    const int64_t es = c.dtype == DMC_FP32 ? 4 : 2, lim = int64_t(1) << 25;
+    if (k_strides[1] * es >= lim || v_strides[1] * es >= lim || q_strides[1] * es >= lim)
+      return fail(DMC_ERR_UNSUPPORTED, "k, v and q token strides must be below 32 MiB");
   }
   dmc::PrefillParams &p = *out;
   p = dmc::PrefillParams{};

@@ -1260,8 +1260,11 @@ __device__ __forceinline__ float token_omega(const PrefillParams &p, int b, int 
 // chunk the mask and count of segment starts; the unit length.  STAGE (prompt
 // attention, window grouping) also stores every token's decision and
 // importance for the passes that read them; the exact compaction reads only
-// k[0] here and forms omega itself.
-template <int ES, bool STAGE>
+// k[0] here and forms omega itself.  AUX is the neuron loads' cache
+// policy: each load brings in the first 128-byte line of a key row, which the
+// pages pass reads again; while those lines fit the last-level cache they are
+// kept (default policy), otherwise they are streamed (nontemporal).
+template <int ES, bool STAGE, int AUX>
 __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams p) {
   __shared__ int s_tot[kWaves];
   const int u = xcd_order(blockIdx.x, gridDim.x);
@@ -1271,18 +1274,32 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
   const int nb = prompt_len(p, b, tid == 0);
   int total = 0;
   constexpr int kBatch = STAGE ? 8 : 16;   // tokens whose decision neurons are in flight per thread
+  // Neurons by nontemporal buffer loads: per batch and wave a resource based
+  // at the wave's first token (SGPRs) and one lane offset lane * token stride
+  // (below 2^31: the host bounds token strides), lanes past the prompt
+  // switched off by an out-of-range offset -- no 64-bit address per load and
+  // lane, so that every workgroup of a large layer is resident at once.
+  const char *kb = static_cast<const char *>(p.k) + (b * p.ks[0] + dg * p.ks[2]) * ES;
+  const char *qb = static_cast<const char *>(p.q) + (b * p.qs[0] + (dg * G) * p.qs[2]) * ES;
+  const int64_t kst = p.ks[1] * ES, qst = p.qs[1] * ES;
+  const uint32_t koff = lane * static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(kst)));
+  const uint32_t qoff = lane * static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(qst)));
+  auto neuron = [&](const char *base, int64_t st, uint32_t off, int tw) {
+    const bool on = tw < p.n;   // wave-uniform
+    const __amdgpu_buffer_rsrc_t rs = raw_rsrc(uniform_ptr(base + int64_t(on ? tw : 0) * st), on);
+    const uint32_t vo = tw + lane < p.n ? off : kOutOfRange;
+    if constexpr (ES == 2)
+      return __uint_as_float(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rs, vo, 0, AUX)) << 16);
+    else
+      return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, vo, 0, AUX));
+  };
   for (int t00 = 0; t00 < p.n; t00 += kThreads * kBatch) {
     float k0[kBatch], q0[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      const int t = t00 + j * kThreads + tid;
-      k0[j] = 0.0f;
-      q0[j] = 0.0f;
-      if (t < p.n) {
-        k0[j] = load_elem<ES>(p.k, b * p.ks[0] + t * p.ks[1] + dg * p.ks[2]);
-        if (STAGE && p.omega_src == 0)
-          q0[j] = load_elem<ES>(p.q, b * p.qs[0] + t * p.qs[1] + (dg * G) * p.qs[2]);
-      }
+      const int tw = t00 + j * kThreads + wave * 64;   // the wave's first token
+      k0[j] = neuron(kb, kst, koff, tw);
+      q0[j] = STAGE && p.omega_src == 0 ? neuron(qb, qst, qoff, tw) : 0.0f;
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
@@ -1407,17 +1424,18 @@ template <int ES, int E>
 struct RowBits {
   typedef typename std::conditional<(ES * E > 4), uint2, uint32_t>::type T;
   T w;
-  __device__ __forceinline__ void load_nt(const char *p) {
+  // Nontemporal buffer load at rsrc + voff (lane) + soff (wave-uniform).
+  __device__ __forceinline__ void load_nt(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff) {
     if constexpr (ES == 2 && E == 2) {
-      w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+      w = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, kNontemporal);
     } else if constexpr (ES == 2) {
-      w = __builtin_nontemporal_load(reinterpret_cast<const uint16_t *>(p));
+      w = __builtin_amdgcn_raw_buffer_load_b16(rs, voff, soff, kNontemporal);
     } else if constexpr (E == 2) {
       typedef unsigned int u2_t __attribute__((ext_vector_type(2)));
-      const u2_t x = __builtin_nontemporal_load(reinterpret_cast<const u2_t *>(p));
+      const u2_t x = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, kNontemporal);
       w = make_uint2(x.x, x.y);
     } else {
-      w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
+      w = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, kNontemporal);
     }
   }
   __device__ __forceinline__ void unpack(float *f) const {
@@ -1502,7 +1520,7 @@ __device__ __forceinline__ int start_token(const uint64_t *masks, int chunks, in
 // (item k, unit u) with k outermost, in plain launch order, so every XCD gets
 // a mix of all units and items.
 #ifndef DMC_PF_ITEM_TOKENS
-#define DMC_PF_ITEM_TOKENS 256
+#define DMC_PF_ITEM_TOKENS 128
 #endif
 constexpr int kItemTokens = DMC_PF_ITEM_TOKENS;
 
@@ -1536,17 +1554,26 @@ __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p
   const int G = p.hq / p.hkv, dg = p.decision_src ? 0 : g;
   const uint64_t *um = p.mask + int64_t(u) * p.prompt_chunks;
   const int nch = (p.n + 63) >> 6;   // chunks written for this prompt
-  const int t_lo = start_token(um, nch, s_lo, nb);
-  const int t_hi = s_hi < l ? start_token(um, nch, s_hi, nb) : nb;
+  // wave-uniform (the batch bounds below select SGPR row offsets)
+  const int t_lo = __builtin_amdgcn_readfirstlane(start_token(um, nch, s_lo, nb));
+  const int t_hi = __builtin_amdgcn_readfirstlane(s_hi < l ? start_token(um, nch, s_hi, nb) : nb);
 
   // page-table entries of the pages whose first slot is in the item
   const int64_t pt = int64_t(u) * p.maxpages;
   const int pg0 = (s_lo + P - 1) >> p.log2p, pg1 = (s_hi - 1) >> p.log2p;
   for (int i = pg0 + lane; i <= pg1; i += 64) p.ptab[pt + i] = pb + i;
 
-  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2] + lane * E) * ES;
-  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2] + lane * E) * ES;
+  // Prompt rows are read by buffer loads: a resource based at the batch's
+  // first row (SGPRs), a 32-bit row offset in an SGPR and one shared lane
+  // offset -- a 64-bit address per row and lane took 64 of the kernel's
+  // registers and halved its waves per SIMD.  Row offsets within a batch stay
+  // below 2^31 bytes (the host bounds the row stride).
+  const char *kbase = static_cast<const char *>(p.k) + (b * p.ks[0] + g * p.ks[2]) * ES;
+  const char *vbase = static_cast<const char *>(p.v) + (b * p.vs[0] + g * p.vs[2]) * ES;
+  const uint32_t lane_off = lane * E * ES;
   const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
+  const int kst32 = __builtin_amdgcn_readfirstlane(static_cast<int>(kst));
+  const int vst32 = __builtin_amdgcn_readfirstlane(static_cast<int>(vst));
   unsigned char *stage = s_vt + (VT ? wave * 32 * LDR : 0);
   int s = s_lo;
   float ak[E], av[E], zs = 0.0f;
@@ -1606,11 +1633,13 @@ __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p
   const bool lead_q0 = p.omega_src == 0;
   auto issue = [&](int bi, Batch &bt) {
     const int t2 = t_lo + bi * kPfRows, cnt = min(kPfRows, t_hi - t2);
+    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(uniform_ptr(kbase + t2 * kst));
+    const __amdgpu_buffer_rsrc_t vrs = raw_rsrc(uniform_ptr(vbase + t2 * vst));
 #pragma unroll
     for (int j = 0; j < kPfRows; ++j) {
-      const int tj = t2 + min(j, cnt - 1);
-      bt.kr[j].load_nt(kbase + tj * kst);   // prompt rows are read once
-      bt.vr[j].load_nt(vbase + tj * vst);
+      const int jj = min(j, cnt - 1);
+      bt.kr[j].load_nt(krs, lane_off, jj * kst32);   // prompt rows are read once
+      bt.vr[j].load_nt(vrs, lane_off, jj * vst32);
     }
     bt.q0 = 0;
     if (lead_q0 && lane < cnt) {
@@ -2031,11 +2060,21 @@ hipError_t prefill_impl(const PrefillParams &p, bool vt, hipStream_t s) {
   // decisions and importances are staged for the passes that read them per
   // token: prompt attention (carry records enabled) and window grouping
   const bool stage = p.carry != nullptr || p.win.window > 0;
+  // the neuron lines (one 128-byte line per token and unit) are kept for the
+  // pages pass while they fit about twice the 256 MiB last-level cache:
+  // measured, a Llama-2-7B layer (268 MB of lines) gains 50 us in the pages
+  // pass from kept lines, a 70B GQA layer (1.07 GB) 28 us in this pass from
+  // streamed ones
+  const bool keep = int64_t(p.units) * p.n * 128 <= (int64_t(512) << 20);
   if (p.n > 0) {
-    if (stage)
-      hipLaunchKernelGGL((prefill_decide_kernel<ES, true>), dim3(p.units), dim3(kThreads), 0, s, p);
+    if (stage && keep)
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, true, kCachePolicyDefault>), dim3(p.units), dim3(kThreads), 0, s, p);
+    else if (stage)
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, true, kNontemporal>), dim3(p.units), dim3(kThreads), 0, s, p);
+    else if (keep)
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, false, kCachePolicyDefault>), dim3(p.units), dim3(kThreads), 0, s, p);
     else
-      hipLaunchKernelGGL((prefill_decide_kernel<ES, false>), dim3(p.units), dim3(kThreads), 0, s, p);
+      hipLaunchKernelGGL((prefill_decide_kernel<ES, false, kNontemporal>), dim3(p.units), dim3(kThreads), 0, s, p);
   } else {
     hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(p.units)), dim3(kThreads), 0, s, p.len, 0,
                        size_t(p.units));

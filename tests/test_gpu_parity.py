@@ -277,6 +277,31 @@ def test_bad_import_length_sets_flag(torch_cuda):
     assert pr.gpu.lengths(0).cpu().numpy().tolist() == [[3, 0]]
 
 
+def test_prompt_token_stride_bound(torch_cuda):
+    """Up to 64 consecutive prompt tokens are addressed from one base with
+    32-bit offsets: a k or v token stride of 32 MiB or more is refused before
+    anything is enqueued, one just below is accepted."""
+    import torch
+    import paper_2403_09636_amd as P
+    log("case prompt token stride bound")
+    pr = Pair(1, 1, 1, 1, 64, "bf16", max_slots=8, num_pages=8, max_prompt_len=2)
+    big = 1 << 24                      # elements: 32 MiB of bf16
+    buf = torch.zeros(big + 64, dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros((1, 2, 1, 64), dtype=torch.bfloat16, device="cuda")
+    for stride, ok in ((big, False), (big - 64, True)):
+        k = torch.as_strided(buf, (1, 2, 1, 64), (2 * big, stride, 64, 1))
+        v = torch.zeros((1, 2, 1, 64), dtype=torch.bfloat16, device="cuda")
+        for kk, vv in ((k, v), (v, k)):
+            if ok:
+                pr.gpu.prefill(0, kk, vv, q)
+            else:
+                with pytest.raises(P.DMCError) as e:
+                    pr.gpu.prefill(0, kk, vv, q)
+                assert e.value.status == P.binding.DMC_ERR_UNSUPPORTED
+    pr.ok()
+    assert pr.gpu.lengths(0).cpu().numpy().tolist() == [[2]]   # k[0] = 0: both tokens append
+
+
 def test_largest_matrix_core_unit_table(torch_cuda):
     """Grouped-query bf16 caches decode on matrix cores with a 128 KB chunk ring
     in LDS at d = 128; the largest slot-space table of one entry per unit
