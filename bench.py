@@ -268,6 +268,7 @@ def bench_prompt(args):
         for _ in range(reps):
             cache.reset()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            host_lead(torch)
             e0.record(stream)
             fn()
             e1.record(stream)
@@ -402,6 +403,7 @@ def bench_train(args, pool=None):
         ms = []
         for _ in range(reps):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            host_lead(torch)
             e0.record(stream)
             fn()
             e1.record(stream)
@@ -468,6 +470,27 @@ def main():
         if pool is not None:
             pool.close()
             pool.join()
+
+
+_LEAD_CYCLES = None
+
+
+def host_lead(torch):
+    """Enqueue a device-side spin of about 0.5 ms just before a timed call, so
+    that the host's argument checks and kernel launches for that call overlap
+    it and the events around the call bracket GPU work only (otherwise an
+    idle GPU records the first event, then waits for the host)."""
+    global _LEAD_CYCLES
+    if _LEAD_CYCLES is None:
+        torch.cuda._sleep(1000)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.cuda._sleep(200000)
+        e1.record()
+        torch.cuda.synchronize()
+        _LEAD_CYCLES = max(1000, int(200000 * 0.5 / max(e0.elapsed_time(e1), 1e-3)))
+    torch.cuda._sleep(_LEAD_CYCLES)
 
 
 def hbm_context(torch, dev):
@@ -546,6 +569,7 @@ def bench_decode(args, pool):
                 if layer == 0:
                     prompt_reads = windowed_prompt_reads(k0p, args.window)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            host_lead(torch)
             e0.record()
             cache.prefill(layer, k, v, q0)
             e1.record()

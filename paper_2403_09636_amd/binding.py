@@ -56,6 +56,10 @@ class DMCError(RuntimeError):
 
 
 def _load():
+    # torch first: its HIP runtime is then the one the library binds to (one
+    # runtime per process; loading the library first can bring in a second
+    # copy, which then finds no device)
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                           "or python paper_2403_09636_amd/csrc/build.py")
