@@ -75,6 +75,17 @@ constexpr int kValuUnitOverhead = 32;
 constexpr int kMfmaUnitOverhead = 0;
 static_assert(kValuUnitOverhead <= kDecodeUnitOverhead && kMfmaUnitOverhead <= kDecodeUnitOverhead,
               "slot-space overhead bound");
+#ifndef DMC_VALU_DECODE_WAVES
+#define DMC_VALU_DECODE_WAVES 8
+#endif
+// Workgroup size of the vector-ALU decode.  The launch keeps the waves of the
+// persistent grid (kDecodeWgPerCu workgroups of 4 waves per compute unit)
+// and packs them into workgroups of this many threads; groups of more than
+// two query heads keep 4 waves (their registers need the 512-VGPR budget of
+// one wave per SIMD in a 4-wave workgroup).
+template <int G>
+constexpr int valu_decode_threads() { return G <= 2 ? 64 * DMC_VALU_DECODE_WAVES : kThreads; }
+static_assert(64 * DMC_VALU_DECODE_WAVES % kThreads == 0 && DMC_VALU_DECODE_WAVES <= 16, "decode workgroup");
 constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
 constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
 
@@ -185,28 +196,29 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float *a, float 
 // fit in LDS run the GRP kernels, which keep only every g-th entry (g =
 // p.slot_group, a power of two <= 64): s_off[j] = off of unit j g, for
 // j <= NG = ceil(U / g), s_off[NG] = S.
-template <bool GRP, int OVH>
+template <bool GRP, int OVH, int NT = kThreads>
 __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_off, int *s_wsum) {
+  constexpr int NW = NT / 64;
   const int U = p.units, g = GRP ? p.slot_group : 1, NG = (U + g - 1) / g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   constexpr int kBatch = 8;     // coalesced loads in flight per thread
-  for (int i0 = 0; i0 < U; i0 += kThreads * kBatch) {
+  for (int i0 = 0; i0 < U; i0 += NT * kBatch) {
     int v[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      const int i = i0 + j * kThreads + tid;
+      const int i = i0 + j * NT + tid;
       v[j] = i < U ? p.len_in[i] : 0;
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      const int i = i0 + j * kThreads + tid;   // units of a wave are 64 consecutive ones
+      const int i = i0 + j * NT + tid;   // units of a wave are 64 consecutive ones
       int n = i < U ? max(v[j], 1) + OVH : 0;
       for (int o = 1; o < g; o <<= 1) n += __shfl_xor(n, o, 64);   // sum over the g-unit group
       if (i < U && (i & (g - 1)) == 0) s_off[i / g] = n;
     }
   }
   __syncthreads();
-  const int per = (NG + kThreads - 1) / kThreads;
+  const int per = (NG + NT - 1) / NT;
   const int i0 = min(tid * per, NG), i1 = min(i0 + per, NG);
   int sum = 0;
   for (int i = i0; i < i1; ++i) sum += s_off[i];
@@ -219,7 +231,7 @@ __device__ __forceinline__ int build_slot_space(const DecodeParams &p, int *s_of
   if (lane == 63) s_wsum[wave] = incl;
   __syncthreads();
   int run = incl - sum, total = 0;
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     if (w < wave) run += s_wsum[w];
     total += s_wsum[w];
   }
@@ -260,7 +272,8 @@ __device__ __forceinline__ int unit_at(const DecodeParams &p, const int *s_off, 
 }
 
 template <int ES, int D, int G, bool WIN, bool GRP>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(valu_decode_threads<G>()) void decode_kernel(DecodeParams p) {
+  constexpr int NT = valu_decode_threads<G>(), NW = NT / 64;   // threads, waves per workgroup
   using V = V16<ES>;
   constexpr int VN = V::N;        // elements per 16-byte lane chunk
   constexpr int LPR = D / VN;     // lanes per cache row
@@ -272,7 +285,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   static_assert(kValuChunk == (1 << kLog2Chunk) && NI >= 1, "chunk rows");
 
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int s_wsum[kWaves];
+  __shared__ int s_wsum[NW];
   int *s_off = reinterpret_cast<int *>(smem);   // slot-space table (build_slot_space)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -282,13 +295,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
   const int log2cs = p.log2p < kLog2Chunk ? p.log2p : kLog2Chunk;
 
   constexpr int OVH = kValuUnitOverhead;
-  const int S = build_slot_space<GRP, OVH>(p, s_off, s_wsum);
-  const int nwaves = gridDim.x * kWaves;
+  const int S = build_slot_space<GRP, OVH, NT>(p, s_off, s_wsum);
+  const int nwaves = gridDim.x * NW;
   int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);   // equal shares
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
   const int nranges = (S + span - 1) / span;
 
-  for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
+  for (int r = blockIdx.x * NW + wave; r < nranges; r += nwaves) {
     int pos = r * span;
     const int pos_end = min(pos + span, S);
     int off;   // the piece's unit's offset; a later piece of the range starts its unit
@@ -2012,7 +2025,11 @@ void launch_decode_kernel(const DecodeParams &p, int grid, bool vt, size_t lds, 
       return;
     }
   }
-  hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN, GRP>), dim3(grid), dim3(kThreads), lds, s, p);
+  // grid counts workgroups of kThreads; the vector kernel packs the same waves
+  // into workgroups of valu_decode_threads<G>()
+  constexpr int NT = valu_decode_threads<G>();
+  const int vgrid = std::max(1, grid / (NT / kThreads));
+  hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN, GRP>), dim3(vgrid), dim3(NT), lds, s, p);
 }
 
 template <int ES, int D, int G>
