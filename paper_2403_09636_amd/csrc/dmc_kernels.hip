@@ -80,11 +80,11 @@ static_assert(kValuUnitOverhead <= kDecodeUnitOverhead && kMfmaUnitOverhead <= k
 #endif
 // Workgroup size of the vector-ALU decode.  The launch keeps the waves of the
 // persistent grid (kDecodeWgPerCu workgroups of 4 waves per compute unit)
-// and packs them into workgroups of this many threads; groups of more than
-// two query heads keep 4 waves (their registers need the 512-VGPR budget of
-// one wave per SIMD in a 4-wave workgroup).
-template <int G>
-constexpr int valu_decode_threads() { return G <= 2 ? 64 * DMC_VALU_DECODE_WAVES : kThreads; }
+// and packs them into workgroups of this many threads; fp32 caches and groups
+// of more than two query heads keep 4 waves (their registers need more than
+// the 256 VGPRs per wave an 8-wave workgroup leaves).
+template <int ES, int G>
+constexpr int valu_decode_threads() { return ES == 2 && G <= 2 ? 64 * DMC_VALU_DECODE_WAVES : kThreads; }
 static_assert(64 * DMC_VALU_DECODE_WAVES % kThreads == 0 && DMC_VALU_DECODE_WAVES <= 16, "decode workgroup");
 constexpr int kValuChunk = DMC_VALU_CHUNK;  // rows per chunk of the vector-ALU decode
 constexpr int kBuf = DMC_VALU_BUFFERS;      // chunk buffers in flight per wave
@@ -272,8 +272,8 @@ __device__ __forceinline__ int unit_at(const DecodeParams &p, const int *s_off, 
 }
 
 template <int ES, int D, int G, bool WIN, bool GRP>
-__global__ __launch_bounds__(valu_decode_threads<G>()) void decode_kernel(DecodeParams p) {
-  constexpr int NT = valu_decode_threads<G>(), NW = NT / 64;   // threads, waves per workgroup
+__global__ __launch_bounds__((valu_decode_threads<ES, G>())) void decode_kernel(DecodeParams p) {
+  constexpr int NT = valu_decode_threads<ES, G>(), NW = NT / 64;   // threads, waves per workgroup
   using V = V16<ES>;
   constexpr int VN = V::N;        // elements per 16-byte lane chunk
   constexpr int LPR = D / VN;     // lanes per cache row
@@ -2026,8 +2026,8 @@ void launch_decode_kernel(const DecodeParams &p, int grid, bool vt, size_t lds, 
     }
   }
   // grid counts workgroups of kThreads; the vector kernel packs the same waves
-  // into workgroups of valu_decode_threads<G>()
-  constexpr int NT = valu_decode_threads<G>();
+  // into workgroups of valu_decode_threads<ES, G>()
+  constexpr int NT = valu_decode_threads<ES, G>();
   const int vgrid = std::max(1, grid / (NT / kThreads));
   hipLaunchKernelGGL((decode_kernel<ES, D, G, WIN, GRP>), dim3(vgrid), dim3(NT), lds, s, p);
 }
