@@ -1547,9 +1547,8 @@ template <int ES, int D, bool VT>
 __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p, int items) {
   constexpr int E = D / 64;         // elements per lane
   constexpr int RB = D * ES;        // bytes per row
-  constexpr int LDR = RB + 4;       // padded LDS row of the V^T staging page
   static_assert(!VT || ES == 2, "transposed value pages are bf16");
-  __shared__ __align__(16) unsigned char s_vt[VT ? kWaves * 32 * LDR : 16];
+  __shared__ __align__(16) unsigned char s_vt[VT ? kWaves * 32 * RB : 16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gw = blockIdx.x * kWaves + wave;
   const int k = gw / p.units;
@@ -1587,7 +1586,15 @@ __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p
   const int64_t kst = p.ks[1] * ES, vst = p.vs[1] * ES;
   const int kst32 = __builtin_amdgcn_readfirstlane(static_cast<int>(kst));
   const int vst32 = __builtin_amdgcn_readfirstlane(static_cast<int>(vst));
-  unsigned char *stage = s_vt + (VT ? wave * 32 * LDR : 0);
+  unsigned char *stage = s_vt + (VT ? wave * 32 * RB : 0);
+  // Byte offset of element e of staging row r: rows of RB bytes, unpadded (32 KB per
+  // workgroup, so that five fit a compute unit), with the 4-byte word index XORed by
+  // 8 (r / 8 mod 4).  A row write (64 lanes, consecutive words) and a column gather
+  // (lanes over 16 elements x 4 row groups) then touch distinct banks.
+  auto stage_at = [&](int r, int e) {
+    const int byte = 2 * e;
+    return r * RB + ((((byte >> 2) ^ (8 * ((r >> 3) & 3))) << 2) | (byte & 3));
+  };
   int s = s_lo;
   float ak[E], av[E], zs = 0.0f;
 #pragma unroll
@@ -1595,19 +1602,20 @@ __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p
 
   // The value page of grouped-query caches, staged as 32 rows in LDS, goes out
   // as V^T: lane (dim, quarter) gathers 8 slots of one dim -- conflict-free
-  // thanks to the padded rows -- and stores them as one 16-byte piece.
+  // thanks to the swizzle -- and stores them as one 16-byte piece.  The loop is
+  // not unrolled: unrolled, its 64 reads in flight took 21 more VGPRs.
   auto write_vt_page = [&](char *vtp) {
     if constexpr (VT) {
       wave_lds_sync();
-#pragma unroll
+#pragma unroll 1
       for (int i = 0; i < D * 4 / 64; ++i) {
         const int pc = i * 64 + lane, dim = pc >> 2, qq = pc & 3;
-        const unsigned char *col = stage + 8 * qq * LDR + dim * 2;
         uint32_t w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          w[j] = uint32_t(*reinterpret_cast<const uint16_t *>(col + 2 * j * LDR)) |
-                 (uint32_t(*reinterpret_cast<const uint16_t *>(col + (2 * j + 1) * LDR)) << 16);
+          w[j] = uint32_t(*reinterpret_cast<const uint16_t *>(stage + stage_at(8 * qq + 2 * j, dim))) |
+                 (uint32_t(*reinterpret_cast<const uint16_t *>(stage + stage_at(8 * qq + 2 * j + 1, dim)))
+                  << 16);
         __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]},
                                     reinterpret_cast<u32x4 *>(vtp + dim * 64 + qq * 16));
       }
@@ -1626,7 +1634,7 @@ __global__ __launch_bounds__(kThreads) void prefill_pages_kernel(PrefillParams p
     char *pg = p.pool + int64_t(pb + (s >> p.log2p)) * p.page_bytes;
     store_e_nt<ES, E>(pg + int64_t(row) * RB + lane * E * ES, kq);
     if constexpr (VT) {
-      store_e<ES, E>(reinterpret_cast<char *>(stage + row * LDR + lane * E * ES), vq);
+      store_e<ES, E>(reinterpret_cast<char *>(stage + stage_at(row, lane * E)), vq);
       if (row == 31 || s == s_hi - 1) write_vt_page(pg + 32 * RB);
     } else {
       store_e_nt<ES, E>(pg + int64_t(P) * RB + int64_t(row) * RB + lane * E * ES, vq);
