@@ -58,8 +58,10 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 #ifndef DMC_DECODE_WG_PER_CU
 #define DMC_DECODE_WG_PER_CU 2
 #endif
-// Persistent decode grid: workgroups per compute unit (4 waves each), and
-// the largest number of waves a decode launch uses.
+// Persistent decode grid, counted in workgroups of 4 waves per compute unit
+// (the vector-ALU launch packs them into 8-wave workgroups for bf16 caches
+// with up to two query heads per kv head), and the largest number of waves a
+// decode launch uses.
 constexpr int kDecodeWgPerCu = DMC_DECODE_WG_PER_CU;
 constexpr int64_t kMaxDecodeWaves = 8192;
 constexpr size_t kMaxDecodeLds = 64 * 1024;
@@ -322,7 +324,8 @@ dmc_status dmc_cache_reset(dmc_cache *cache, dmc_stream_t stream) {
 namespace {
 
 // Persistent decode grid of a cache: workgroups of 4 waves, kDecodeWgPerCu per
-// compute unit (the matrix-core launch halves it when its LDS ring allows one).
+// compute unit (the matrix-core launch halves it when its LDS ring allows one;
+// the vector-ALU launch may pack the same waves into larger workgroups).
 int decode_grid(const dmc_cache *cache) {
   return static_cast<int>(
       std::min<int64_t>(int64_t(cache->cu_count) * kDecodeWgPerCu, kMaxDecodeWaves / 4));

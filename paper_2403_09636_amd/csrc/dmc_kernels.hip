@@ -1287,11 +1287,11 @@ __global__ __launch_bounds__(kThreads) void prefill_decide_kernel(PrefillParams 
   const int nb = prompt_len(p, b, tid == 0);
   int total = 0;
   constexpr int kBatch = STAGE ? 8 : 16;   // tokens whose decision neurons are in flight per thread
-  // Neurons by nontemporal buffer loads: per batch and wave a resource based
-  // at the wave's first token (SGPRs) and one lane offset lane * token stride
-  // (below 2^31: the host bounds token strides), lanes past the prompt
-  // switched off by an out-of-range offset -- no 64-bit address per load and
-  // lane, so that every workgroup of a large layer is resident at once.
+  // Neurons by buffer loads with cache policy AUX: per batch and wave a
+  // resource based at the wave's first token (SGPRs) and one lane offset
+  // lane * token stride (below 2^31: the host bounds token strides), lanes past
+  // the prompt switched off by an out-of-range offset -- no 64-bit address per
+  // load and lane, so that every workgroup of a large layer is resident at once.
   const char *kb = static_cast<const char *>(p.k) + (b * p.ks[0] + dg * p.ks[2]) * ES;
   const char *qb = static_cast<const char *>(p.q) + (b * p.qs[0] + (dg * G) * p.qs[2]) * ES;
   const int64_t kst = p.ks[1] * ES, qst = p.qs[1] * ES;
