@@ -481,6 +481,8 @@ def host_lead(torch):
     it and the events around the call bracket GPU work only (otherwise an
     idle GPU records the first event, then waits for the host)."""
     global _LEAD_CYCLES
+    if not hasattr(torch.cuda, "_sleep"):   # (a torch build without it: time as is)
+        return
     if _LEAD_CYCLES is None:
         torch.cuda._sleep(1000)
         torch.cuda.synchronize()
