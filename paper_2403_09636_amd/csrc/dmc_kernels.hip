@@ -73,6 +73,9 @@ constexpr int kRangesPerWave = 1;   // slot-space ranges per decode wave (2 and 
 // two units of 2000+ slots (no change measured).  At most kDecodeUnitOverhead.
 constexpr int kValuUnitOverhead = 32;
 constexpr int kMfmaUnitOverhead = 0;
+// Largest excess, in percent of the equal slot share, at which the matrix-core
+// decode gives every wave whole units instead of equal slot ranges.
+constexpr int kWholeUnitSlack = 10;
 static_assert(kValuUnitOverhead <= kDecodeUnitOverhead && kMfmaUnitOverhead <= kDecodeUnitOverhead,
               "slot-space overhead bound");
 #ifndef DMC_VALU_DECODE_WAVES
@@ -728,13 +731,40 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
   const int nwaves = gridDim.x * kWaves;
   int span = (S + kRangesPerWave * nwaves - 1) / (kRangesPerWave * nwaves);
   if (p.split_tile > 0 && span > p.split_tile) span = p.split_tile;
-  const int nranges = (S + span - 1) / span;
+  // Whole units when that balances: wave w takes units [w U / W, (w + 1) U / W)
+  // in full if no wave's share then exceeds the equal slot share by more than
+  // kWholeUnitSlack.  Split units cost this kernel a piece start, an owner
+  // epilogue and a partial record each (measured: a 70B-shaped layer of
+  // lengths 2048 +- 32 at 407-426 us per call against 345-348 us at 2048
+  // exactly), so near-uniform lengths -- one compression ratio for every head
+  // -- stream faster without them.  Grouped tables and forced split sizes keep
+  // the equal-slot ranges.
+  bool whole = false;
+  if constexpr (!GRP) {
+    if (p.split_tile == 0 && U >= nwaves) {
+      int mx = 0;
+      for (int w = threadIdx.x; w < nwaves; w += kThreads) {
+        const int u0 = static_cast<int>(int64_t(w) * U / nwaves);
+        const int u1 = static_cast<int>(int64_t(w + 1) * U / nwaves);
+        mx = max(mx, s_off[u1] - s_off[u0]);
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o, 64));
+      if (lane == 0) s_wsum[wave] = mx;
+      __syncthreads();
+      for (int w = 0; w < kWaves; ++w) mx = max(mx, s_wsum[w]);
+      whole = int64_t(mx) * 100 <= int64_t(span) * (100 + kWholeUnitSlack);
+    }
+  }
+  const int nranges = whole ? nwaves : (S + span - 1) / span;
 
   for (int r = blockIdx.x * kWaves + wave; r < nranges; r += nwaves) {
-    int pos = r * span;
-    const int pos_end = min(pos + span, S);
+    const int wu0 = whole ? static_cast<int>(int64_t(r) * U / nwaves) : 0;
+    int pos = whole ? s_off[wu0] : r * span;
+    const int pos_end = whole ? s_off[static_cast<int>(int64_t(r + 1) * U / nwaves)] : min(pos + span, S);
     int off;
-    for (int u = unit_at<GRP, OVH>(p, s_off, pos, off); pos < pos_end; ++u, off = pos) {
+    for (int u = whole ? (off = pos, wu0) : unit_at<GRP, OVH>(p, s_off, pos, off); pos < pos_end;
+         ++u, off = pos) {
       if constexpr (!GRP) off = s_off[u];
       const int n_u = GRP ? max(p.len_in[u], 1) + OVH : s_off[u + 1] - off;
       const int start = pos - off;
@@ -1085,7 +1115,7 @@ __global__ __launch_bounds__(kThreads, mfma_decode_wg_per_cu<D>()) void decode_m
           p.len_out[u] = (has_cur && !alpha) ? l + 1 : l;
           if (p.slot_index) p.slot_index[u] = has_cur ? slot : -1;
           if (flag) atomicOr(&p.ctrl->flags, flag);
-          const int r0 = off / span;
+          const int r0 = whole ? r : off / span;
           p.meta[2 * u] = r0 + u;
           p.meta[2 * u + 1] = r - r0 + 1;
         }

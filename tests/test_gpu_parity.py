@@ -302,6 +302,35 @@ def test_prompt_token_stride_bound(torch_cuda):
     assert pr.gpu.lengths(0).cpu().numpy().tolist() == [[2]]   # k[0] = 0: both tokens append
 
 
+@pytest.mark.parametrize("d,jitter", [(128, 4), (128, 0), (64, 3)])
+def test_whole_unit_partition(torch_cuda, d, jitter):
+    """The matrix-core decode gives every wave whole units when unit lengths are
+    near-uniform (here 2048 units of 100 +- jitter slots: two per wave at d = 128,
+    one at d = 64), so no unit is split and every output is written by its owner
+    directly.  Every unit's output, slot index, length, slots and z against the
+    oracle over three steps, with appends crossing page boundaries."""
+    import torch
+    log(f"case whole-unit partition d={d} jitter={jitter}")
+    B, Hkv, G, steps = 256, 8, 8, 3
+    rng = np.random.default_rng(91 + d + jitter)
+    lens = (100 + rng.integers(-jitter, jitter + 1, size=(B, Hkv))).astype(np.int32)
+    dense = int(lens.max())
+    pr = Pair(1, B, Hkv * G, Hkv, d, "bf16", max_slots=dense + steps)
+    K = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    V = torch.randn((B, Hkv, dense, d)).to(torch.bfloat16).cuda()
+    K[..., 0] = 0
+    z = torch.rand((B, Hkv)).cuda() * 3 + 0.1
+    pr.gpu.import_(0, K, V, torch.from_numpy(lens).cuda(), z)
+    pr.orc.load(0, f64(K), f64(V), lens, f64(z))
+    err = 0.0
+    for _ in range(steps):
+        err = max(err, pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, np.full(Hkv, 2.0), "bf16",
+                                                 "cuda")))
+    pr.compare_cache(0)
+    pr.ok()
+    log(f"  max abs err {err:.3e}")
+
+
 def test_largest_matrix_core_unit_table(torch_cuda):
     """Grouped-query bf16 caches decode on matrix cores with a 128 KB chunk ring
     in LDS at d = 128; the largest slot-space table of one entry per unit
