@@ -16,7 +16,7 @@ from workloads import decision_logits
 
 pytestmark = pytest.mark.gpu
 
-CASES = 96
+CASES = 256
 
 
 def _draw(seed):
