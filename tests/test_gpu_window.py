@@ -73,6 +73,31 @@ def test_window_prefill_then_decode(torch_cuda, dtype, d, G, w, page):
     log(f"  max abs err {err:.3e}")
 
 
+@pytest.mark.parametrize("dtype,G,w", [("bf16", 4, 64), ("fp32", 1, 5)])
+def test_window_prefill_long_segments(torch_cuda, dtype, G, w):
+    """An 8300-token prompt whose segments run to hundreds of tokens: one
+    compaction work item then covers more than 64 start-mask words (4096
+    tokens), and most of its rows lie outside every window and are not read.
+    One unit keeps a single segment, so the open segment's token ring is
+    filled from the prompt's last tokens."""
+    log(f"case window prefill long segments dtype={dtype} G={G} w={w}")
+    B, Hkv, d, n = 1, 2, 128, 8300
+    crs = [150.0, 1e9]
+    rng = np.random.default_rng(900 + G + w)
+    pr = Pair(1, B, Hkv * G, Hkv, d, dtype, page_size=32, max_slots=n + 16, max_prompt_len=n,
+              window=w)
+    k, v, q = _prompt(rng, B, n, Hkv, G, d, crs, dtype)
+    pr.prefill(0, k, v, q[..., 0].contiguous())
+    pr.compare_cache(0)
+    err = 0.0
+    for _ in range(6):
+        err = max(err, pr.decode(0, *random_step(rng, B, Hkv * G, Hkv, d, np.array(crs), dtype,
+                                                 "cuda")))
+    pr.compare_cache(0)
+    pr.ok()
+    log(f"  lengths {pr.gpu.lengths(0).cpu().numpy().tolist()}, max abs err {err:.3e}")
+
+
 @pytest.mark.parametrize("dtype,d,G,w,page", [
     ("bf16", 128, 1, 12, 32), ("bf16", 128, 2, 12, 32), ("bf16", 128, 4, 12, 32),
     ("bf16", 128, 8, 12, 32), ("bf16", 64, 1, 3, 16), ("bf16", 128, 1, 40, 8),
