@@ -73,7 +73,7 @@ def test_window_prefill_then_decode(torch_cuda, dtype, d, G, w, page):
     log(f"  max abs err {err:.3e}")
 
 
-@pytest.mark.parametrize("dtype,G,w", [("bf16", 4, 64), ("fp32", 1, 5)])
+@pytest.mark.parametrize("dtype,G,w", [("bf16", 4, 64), ("bf16", 8, 1), ("fp32", 1, 5)])
 def test_window_prefill_long_segments(torch_cuda, dtype, G, w):
     """An 8300-token prompt whose segments run to hundreds of tokens: one
     compaction work item then covers more than 64 start-mask words (4096
